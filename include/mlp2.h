@@ -1,0 +1,163 @@
+/*
+ * mlp2.h - C ABI of the tile-pipelined two-layer MLP for AMD MI355X (gfx950).
+ *
+ * The operation is the two-layer product that CTA-pipelining (arXiv
+ * 2607.07862) uses as its workload (Sec. IV: Y = X A B standing for an LLM MLP
+ * layer), with an activation between the layers:
+ *
+ *     Z = act(X . W1)        first GEMM, fused activation epilogue
+ *     Y = Z . W2             second GEMM
+ *
+ * Two execution modes compute bit-identical Y:
+ *   MLP2_MODE_SEQUENTIAL      GEMM1 then GEMM2, two kernels on the stream.
+ *   MLP2_MODE_TILE_PIPELINED  one persistent launch; a GEMM2 work-group
+ *                             consumes each K-slice of Z as soon as the GEMM1
+ *                             tiles producing it have signalled a per-tile
+ *                             ready counter (Sec. III-A: producer epilogue
+ *                             fences, then signals; consumer prologue polls;
+ *                             Sec. III-A.5 host organisation; Sec. III-B.2
+ *                             persistent kernels fetching work tiles).
+ *
+ * Data layout (all device memory, row-major, bf16, 16-byte aligned):
+ *   X   [M, H]            input activations             (caller owns)
+ *   W1  [H, F]            first weight                  (caller owns)
+ *       [2, H, F]         SwiGLU: Wg then Wu, packed    (caller owns)
+ *   W2  [F, H]            second weight                 (caller owns)
+ *   Y   [M, H]            output, fully overwritten     (caller owns)
+ * Arithmetic: bf16 inputs, fp32 accumulation, fp32 activation, the
+ * intermediate Z stored as bf16 (round to nearest even), bf16 output
+ * (Sec. III-C and Sec. IV fix bf16 in/out with fp32 accumulation).
+ *
+ * Activations: identity; GELU tanh form 0.5 z (1 + tanh(sqrt(2/pi)(z + 0.044715 z^3)));
+ * SwiGLU silu(X.Wg) * (X.Wu) with silu(g) = g / (1 + exp(-g)).
+ *
+ * Error behaviour: every entry point validates its arguments on the host
+ * before it enqueues anything; a failing call has no side effect and returns
+ * a negative MLP2_ERR_* code (mlp2_plan returns NULL and records the code for
+ * mlp2_last_error()).  Device-side failures (a bounded flag wait that timed
+ * out) are latched in the plan and reported by mlp2_check().
+ *
+ * Threading: a plan may be used from one host thread at a time and must not
+ * be run concurrently on two streams (its workspace is shared).  Different
+ * plans are independent.
+ */
+#ifndef MLP2_H
+#define MLP2_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct mlp2_plan_s* mlp2_plan_t; /* opaque; created by mlp2_plan, freed by mlp2_destroy */
+
+enum mlp2_act { MLP2_ACT_IDENTITY = 0, MLP2_ACT_GELU_TANH = 1, MLP2_ACT_SWIGLU = 2 };
+enum mlp2_dtype { MLP2_DTYPE_BF16 = 0 };
+enum mlp2_mode { MLP2_MODE_SEQUENTIAL = 0, MLP2_MODE_TILE_PIPELINED = 1 };
+
+enum mlp2_status {
+  MLP2_OK = 0,
+  MLP2_ERR_INVALID_ARG = -1, /* null plan/pointer, bad enum, non-positive size, aliasing Y */
+  MLP2_ERR_UNSUPPORTED = -2, /* sizes outside the supported range (H, F multiples of 64) */
+  MLP2_ERR_ALIGNMENT = -3,   /* a data pointer not 16-byte aligned */
+  MLP2_ERR_HIP = -4,         /* a HIP runtime call failed (allocation, launch) */
+  MLP2_ERR_TIMEOUT = -5,     /* a bounded flag wait on the device gave up (see mlp2_check) */
+  MLP2_ERR_DEVICE = -6       /* no usable gfx950 device, or the plan belongs to another device */
+};
+
+/* GEMM1 tile-ordering policies of the pipelined mode (Sec. III-A.5: the first
+ * kernel may take its tiles from a predefined source order). */
+enum mlp2_order {
+  MLP2_ORDER_COLUMN_FIRST = 0, /* every row block of column block 0, then column block 1, ... */
+  MLP2_ORDER_ROW_FIRST = 1,    /* every column block of row block 0, then row block 1, ...    */
+  MLP2_ORDER_REVERSED = 2,     /* column-first, last column block first (stress order)         */
+  MLP2_ORDER_SHUFFLED = 3      /* a seeded permutation (stress order)                          */
+};
+
+/* Optional tuning for mlp2_plan_ex; a zero field means "choose automatically". */
+typedef struct mlp2_tuning {
+  int bm;        /* row-block height shared by both GEMMs: 32, 64, 128 or 256            */
+  int bn1;       /* GEMM1 column-block width (= GEMM2 K-slice granularity): 64 or 128     */
+  int splitk1;   /* GEMM1 split-K factor (>= 1)                                           */
+  int bn2;       /* GEMM2 column-block width: 64 or 128                                   */
+  int splitk2;   /* GEMM2 split-K factor (>= 1)                                           */
+  int grid;      /* persistent grid of the pipelined launch (work-groups)                 */
+  int order;     /* enum mlp2_order                                                       */
+  int reserved[7];
+} mlp2_tuning_t;
+
+/* What a plan chose, for reports and tests. */
+typedef struct mlp2_info {
+  int64_t M, H, F;
+  int act;
+  int bm, bn1, splitk1, bn2, splitk2, bk;
+  int row_blocks;        /* ceil(M / bm)                                    */
+  int col_blocks1;       /* F / bn1                                         */
+  int col_blocks2;       /* H / bn2                                         */
+  int items1, items2;    /* GEMM1 work items (tiles x splitk1), GEMM2 items */
+  int grid_pipelined;    /* persistent work-groups of the pipelined launch  */
+  int occupancy;         /* resident work-groups per CU of that kernel      */
+  int num_cus;
+  int order;
+  int64_t workspace_bytes;
+  uint32_t spin_limit;
+  int reserved[8];
+} mlp2_info_t;
+
+/* Create a plan for Y[M,H] = act(X[M,H] . W1) . W2 on the current HIP device.
+ * Requires 1 <= M <= 1<<20, H and F multiples of 64 in [64, 1<<18], act in
+ * enum mlp2_act and dtype == MLP2_DTYPE_BF16.  Allocates the workspace (the
+ * bf16 intermediate Z, split-K partials, counters) on the current device.
+ * Returns NULL on failure; mlp2_last_error() gives the code. */
+mlp2_plan_t mlp2_plan(int64_t M, int64_t H, int64_t F, int act, int dtype);
+
+/* As mlp2_plan with explicit tuning (NULL = automatic).  Invalid tuning
+ * (a tile that does not divide H or F, bm not in the list, ...) fails with
+ * MLP2_ERR_UNSUPPORTED. */
+mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, const mlp2_tuning_t* tuning);
+
+/* Enqueue one evaluation on `stream` (a hipStream_t; NULL = the default
+ * stream) in `mode`.  Asynchronous: no host synchronisation, no allocation.
+ * X, W1, W2, Y are device pointers laid out as described above; Y must not
+ * overlap any input.  Runs of one plan on one stream are ordered; the plan
+ * keeps its counters consistent across runs and modes without host resets. */
+int mlp2_run(mlp2_plan_t plan, const void* X, const void* W1, const void* W2, void* Y, void* stream, int mode);
+
+/* Free the plan and its workspace (synchronises the device first).  NULL-safe. */
+void mlp2_destroy(mlp2_plan_t plan);
+
+/* Code of the last failing call on this host thread (MLP2_OK if none). */
+int mlp2_last_error(void);
+
+/* A static, never-NULL description of a status code. */
+const char* mlp2_strerror(int code);
+
+/* After the caller has synchronised the stream: MLP2_OK, or MLP2_ERR_TIMEOUT
+ * if a flag wait gave up during an earlier run.  On a timeout it clears the
+ * latched error and resets the plan's counters so the plan is usable again. */
+int mlp2_check(mlp2_plan_t plan);
+
+/* Fill *out with what the plan chose. */
+int mlp2_plan_info(mlp2_plan_t plan, mlp2_info_t* out);
+
+/* Device pointer to the plan's bf16 intermediate Z, laid out [row_blocks*bm, F]
+ * row-major (rows >= M are padding).  Valid until mlp2_destroy.  For tests and
+ * diagnostics; NULL on a NULL plan. */
+const void* mlp2_intermediate(mlp2_plan_t plan);
+
+/* Debug and failure-injection knobs (tests only).  Keys:
+ *   MLP2_OPT_SPIN_LIMIT   polls before a flag wait gives up (default ~1 s of polling)
+ *   MLP2_OPT_DROP_SIGNAL  GEMM1 tile index whose ready signal is skipped (-1 = none)
+ *   MLP2_OPT_ORDER        enum mlp2_order (rebuilds the order table)
+ *   MLP2_OPT_GRID         persistent grid size of the pipelined launch (>= 1)
+ * Returns MLP2_OK or MLP2_ERR_INVALID_ARG. */
+enum mlp2_option { MLP2_OPT_SPIN_LIMIT = 1, MLP2_OPT_DROP_SIGNAL = 2, MLP2_OPT_ORDER = 3, MLP2_OPT_GRID = 4 };
+int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MLP2_H */

@@ -1,0 +1,236 @@
+"""ctypes binding of ``libmlp2.so`` (the C ABI in ``include/mlp2.h``).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of the library.  PyTorch supplies device memory and the stream.  When
+the compiled library is missing, ``load()`` raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libmlp2.so")
+
+ACT_IDENTITY, ACT_GELU_TANH, ACT_SWIGLU = 0, 1, 2
+DTYPE_BF16 = 0
+MODE_SEQUENTIAL, MODE_TILE_PIPELINED = 0, 1
+MODES = {"sequential": MODE_SEQUENTIAL, "tile_pipelined": MODE_TILE_PIPELINED}
+ORDER_COLUMN_FIRST, ORDER_ROW_FIRST, ORDER_REVERSED, ORDER_SHUFFLED = 0, 1, 2, 3
+OPT_SPIN_LIMIT, OPT_DROP_SIGNAL, OPT_ORDER, OPT_GRID = 1, 2, 3, 4
+
+OK = 0
+ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_ALIGNMENT, ERR_HIP, ERR_TIMEOUT, ERR_DEVICE = -1, -2, -3, -4, -5, -6
+
+# Every symbol include/mlp2.h declares.
+EXPORTS = (
+    "mlp2_plan",
+    "mlp2_plan_ex",
+    "mlp2_run",
+    "mlp2_destroy",
+    "mlp2_last_error",
+    "mlp2_strerror",
+    "mlp2_check",
+    "mlp2_plan_info",
+    "mlp2_intermediate",
+    "mlp2_set_option",
+)
+
+
+class Tuning(ctypes.Structure):
+    _fields_ = [
+        ("bm", ctypes.c_int),
+        ("bn1", ctypes.c_int),
+        ("splitk1", ctypes.c_int),
+        ("bn2", ctypes.c_int),
+        ("splitk2", ctypes.c_int),
+        ("grid", ctypes.c_int),
+        ("order", ctypes.c_int),
+        ("reserved", ctypes.c_int * 7),
+    ]
+
+
+class Info(ctypes.Structure):
+    _fields_ = [
+        ("M", ctypes.c_int64),
+        ("H", ctypes.c_int64),
+        ("F", ctypes.c_int64),
+        ("act", ctypes.c_int),
+        ("bm", ctypes.c_int),
+        ("bn1", ctypes.c_int),
+        ("splitk1", ctypes.c_int),
+        ("bn2", ctypes.c_int),
+        ("splitk2", ctypes.c_int),
+        ("bk", ctypes.c_int),
+        ("row_blocks", ctypes.c_int),
+        ("col_blocks1", ctypes.c_int),
+        ("col_blocks2", ctypes.c_int),
+        ("items1", ctypes.c_int),
+        ("items2", ctypes.c_int),
+        ("grid_pipelined", ctypes.c_int),
+        ("occupancy", ctypes.c_int),
+        ("num_cus", ctypes.c_int),
+        ("order", ctypes.c_int),
+        ("workspace_bytes", ctypes.c_int64),
+        ("spin_limit", ctypes.c_uint32),
+        ("reserved", ctypes.c_int * 8),
+    ]
+
+
+class Mlp2Error(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(f"{what}: {strerror(code)} ({code})")
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the compiled library (raises if it was not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2607_07862_amd.build`")
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    lib.mlp2_plan.restype = P
+    lib.mlp2_plan.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_int]
+    lib.mlp2_plan_ex.restype = P
+    lib.mlp2_plan_ex.argtypes = lib.mlp2_plan.argtypes + [ctypes.POINTER(Tuning)]
+    lib.mlp2_run.restype = ctypes.c_int
+    lib.mlp2_run.argtypes = [P, P, P, P, P, P, ctypes.c_int]
+    lib.mlp2_destroy.restype = None
+    lib.mlp2_destroy.argtypes = [P]
+    lib.mlp2_last_error.restype = ctypes.c_int
+    lib.mlp2_last_error.argtypes = []
+    lib.mlp2_strerror.restype = ctypes.c_char_p
+    lib.mlp2_strerror.argtypes = [ctypes.c_int]
+    lib.mlp2_check.restype = ctypes.c_int
+    lib.mlp2_check.argtypes = [P]
+    lib.mlp2_plan_info.restype = ctypes.c_int
+    lib.mlp2_plan_info.argtypes = [P, ctypes.POINTER(Info)]
+    lib.mlp2_intermediate.restype = P
+    lib.mlp2_intermediate.argtypes = [P]
+    lib.mlp2_set_option.restype = ctypes.c_int
+    lib.mlp2_set_option.argtypes = [P, ctypes.c_int, ctypes.c_int64]
+    _lib = lib
+    return lib
+
+
+def strerror(code: int) -> str:
+    return load().mlp2_strerror(int(code)).decode()
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _check_tensor(t, name, numel, device):
+    import torch
+
+    if t.dtype != torch.bfloat16:
+        raise TypeError(f"{name} must be bfloat16")
+    if not t.is_cuda or t.device != device:
+        raise ValueError(f"{name} must live on {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() != numel:
+        raise ValueError(f"{name} must hold {numel} elements, has {t.numel()}")
+
+
+class Plan:
+    """A plan for ``Y[M,H] = act(X[M,H] @ W1) @ W2`` on the current device."""
+
+    def __init__(self, M: int, H: int, F: int, act: int, tuning: dict | None = None):
+        import torch
+
+        self.lib = load()
+        self.M, self.H, self.F, self.act = int(M), int(H), int(F), int(act)
+        self.device = torch.device("cuda", torch.cuda.current_device())
+        if tuning:
+            t = Tuning()
+            for k, v in tuning.items():
+                setattr(t, k, int(v))
+            h = self.lib.mlp2_plan_ex(self.M, self.H, self.F, self.act, DTYPE_BF16, ctypes.byref(t))
+        else:
+            h = self.lib.mlp2_plan(self.M, self.H, self.F, self.act, DTYPE_BF16)
+        if not h:
+            raise Mlp2Error(self.lib.mlp2_last_error(), "mlp2_plan")
+        self.handle = ctypes.c_void_p(h)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.mlp2_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):  # pragma: no cover - best effort
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def run(self, X, W1, W2, Y, mode, stream=None) -> None:
+        """Enqueue one evaluation on ``stream`` (default: torch's current stream)."""
+        import torch
+
+        n1 = 2 if self.act == ACT_SWIGLU else 1
+        _check_tensor(X, "X", self.M * self.H, self.device)
+        _check_tensor(W1, "W1", n1 * self.H * self.F, self.device)
+        _check_tensor(W2, "W2", self.F * self.H, self.device)
+        _check_tensor(Y, "Y", self.M * self.H, self.device)
+        mode = MODES.get(mode, mode)
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device)
+        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        rc = self.lib.mlp2_run(self.handle, _ptr(X), _ptr(W1), _ptr(W2), _ptr(Y), sp, int(mode))
+        if rc != OK:
+            raise Mlp2Error(rc, "mlp2_run")
+
+    def run_raw(self, X: int, W1: int, W2: int, Y: int, stream: int, mode: int) -> int:
+        """The C call with raw integers (no checks here), returning its status."""
+        return self.lib.mlp2_run(self.handle, X, W1, W2, Y, stream, mode)
+
+    def check(self) -> int:
+        return self.lib.mlp2_check(self.handle)
+
+    def info(self) -> dict:
+        i = Info()
+        rc = self.lib.mlp2_plan_info(self.handle, ctypes.byref(i))
+        if rc != OK:
+            raise Mlp2Error(rc, "mlp2_plan_info")
+        return {f: getattr(i, f) for f, _ in Info._fields_ if f != "reserved"}
+
+    def set_option(self, key: int, value: int) -> None:
+        rc = self.lib.mlp2_set_option(self.handle, int(key), int(value))
+        if rc != OK:
+            raise Mlp2Error(rc, "mlp2_set_option")
+
+    def intermediate_ptr(self) -> int:
+        return int(self.lib.mlp2_intermediate(self.handle) or 0)
+
+    def intermediate(self):
+        """A copy of the plan's bf16 Z as a torch tensor [row_blocks*bm, F] (synchronises)."""
+        import torch
+
+        info = self.info()
+        rows = info["row_blocks"] * info["bm"]
+        out = torch.empty(rows, self.F, dtype=torch.bfloat16, device=self.device)
+        torch.cuda.synchronize(self.device)
+        _hip_memcpy_d2d(out.data_ptr(), self.intermediate_ptr(), rows * self.F * 2)
+        return out
+
+
+_hip = None
+
+
+def _hip_memcpy_d2d(dst: int, src: int, nbytes: int) -> None:
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipMemcpy.restype = ctypes.c_int
+        _hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+    rc = _hip.hipMemcpy(dst, src, nbytes, 3)  # hipMemcpyDeviceToDevice
+    if rc != 0:
+        raise RuntimeError(f"hipMemcpy failed ({rc})")

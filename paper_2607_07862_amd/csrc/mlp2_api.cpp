@@ -1,0 +1,389 @@
+// C ABI of the tile-pipelined two-layer MLP: planning, validation, launch.
+//
+// The plan fixes everything that does not change between runs (tile sizes,
+// split-K factors, the GEMM1 order table, the persistent grid, the workspace)
+// so that mlp2_run only validates pointers and enqueues kernels: no
+// allocation, no host synchronisation, no memset (graph-capture safe).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <numeric>
+#include <random>
+#include <string>
+#include <vector>
+
+#include "../../include/mlp2.h"
+#include "mlp2_launch.h"
+
+using mlp2::Args;
+using mlp2::KernelConfig;
+
+struct mlp2_plan_s {
+  int64_t M = 0, H = 0, F = 0;
+  int act = 0;
+  int device = -1;
+  KernelConfig kc{};
+  int Mb = 0, Nb1 = 0, Nb2 = 0;
+  int S1 = 1, S2 = 1, kc1 = 0, kc2 = 0;
+  int items1 = 0, items2 = 0;
+  int grid = 0, occupancy = 0, num_cus = 0;
+  int order = MLP2_ORDER_COLUMN_FIRST;
+  uint32_t spin_limit = 1u << 20;
+  int drop_signal = -1;
+  // workspace
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  uint16_t* Z = nullptr;
+  float* part1 = nullptr;
+  float* part2 = nullptr;
+  uint32_t* cnt1 = nullptr;
+  uint32_t* cnt2 = nullptr;
+  uint32_t* ready = nullptr;
+  uint32_t* ctrl = nullptr;
+  uint32_t* order1 = nullptr;
+  size_t counters_off = 0, counters_bytes = 0;
+};
+
+namespace {
+
+thread_local int g_last_error = MLP2_OK;
+
+int fail(int code) {
+  g_last_error = code;
+  return code;
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+// Split K into S ranges of kc (a multiple of the stage depth) so that the
+// tile count times S reaches `want` items, keeping every range at least
+// `min_k` deep.  Returns S and sets *kc.
+int choose_split(int64_t K, int tiles, int want, int min_k, int* kc) {
+  int S = std::max(1, ceil_div(want, tiles));
+  S = std::min<int64_t>(S, std::max<int64_t>(1, K / min_k));
+  int64_t k = align_up((size_t)ceil_div(K, S), mlp2::kBK);
+  *kc = (int)k;
+  return ceil_div(K, k);
+}
+
+void build_order(mlp2_plan_s* p, std::vector<uint32_t>& out) {
+  // Item ids: id = tile * S1 + s with tile = nb * Mb + mb.
+  const int n = p->items1;
+  out.resize(n);
+  std::iota(out.begin(), out.end(), 0u);  // column-block-first
+  switch (p->order) {
+    case MLP2_ORDER_ROW_FIRST: {
+      std::vector<uint32_t> v;
+      v.reserve(n);
+      for (int mb = 0; mb < p->Mb; ++mb)
+        for (int nb = 0; nb < p->Nb1; ++nb)
+          for (int s = 0; s < p->S1; ++s) v.push_back((uint32_t)((nb * p->Mb + mb) * p->S1 + s));
+      out.swap(v);
+      break;
+    }
+    case MLP2_ORDER_REVERSED: {
+      std::vector<uint32_t> v;
+      v.reserve(n);
+      for (int nb = p->Nb1 - 1; nb >= 0; --nb)
+        for (int mb = 0; mb < p->Mb; ++mb)
+          for (int s = 0; s < p->S1; ++s) v.push_back((uint32_t)((nb * p->Mb + mb) * p->S1 + s));
+      out.swap(v);
+      break;
+    }
+    case MLP2_ORDER_SHUFFLED: {
+      std::mt19937 rng(12345u);
+      std::shuffle(out.begin(), out.end(), rng);
+      break;
+    }
+    default:
+      break;
+  }
+}
+
+bool is_gfx950(int dev) {
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return false;
+  return std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+int upload_order(mlp2_plan_s* p) {
+  std::vector<uint32_t> ord;
+  build_order(p, ord);
+  if (hipMemcpy(p->order1, ord.data(), ord.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess)
+    return MLP2_ERR_HIP;
+  return MLP2_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mlp2_last_error(void) { return g_last_error; }
+
+const char* mlp2_strerror(int code) {
+  switch (code) {
+    case MLP2_OK: return "ok";
+    case MLP2_ERR_INVALID_ARG: return "invalid argument";
+    case MLP2_ERR_UNSUPPORTED: return "unsupported size or tuning";
+    case MLP2_ERR_ALIGNMENT: return "pointer not 16-byte aligned";
+    case MLP2_ERR_HIP: return "HIP runtime call failed";
+    case MLP2_ERR_TIMEOUT: return "device flag wait timed out";
+    case MLP2_ERR_DEVICE: return "no usable gfx950 device for this plan";
+    default: return "unknown status code";
+  }
+}
+
+mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, const mlp2_tuning_t* t) {
+  g_last_error = MLP2_OK;
+  if (M < 1 || H < 1 || F < 1) { fail(MLP2_ERR_INVALID_ARG); return nullptr; }
+  if (act < MLP2_ACT_IDENTITY || act > MLP2_ACT_SWIGLU) { fail(MLP2_ERR_INVALID_ARG); return nullptr; }
+  if (dtype != MLP2_DTYPE_BF16) { fail(MLP2_ERR_INVALID_ARG); return nullptr; }
+  if (M > (1 << 20) || H % 64 || F % 64 || H > (1 << 18) || F > (1 << 18)) {
+    fail(MLP2_ERR_UNSUPPORTED);
+    return nullptr;
+  }
+  const int nb = act == MLP2_ACT_SWIGLU ? 2 : 1;
+  mlp2_tuning_t tz;
+  std::memset(&tz, 0, sizeof(tz));
+  if (t) tz = *t;
+  if (tz.bm < 0 || tz.bn1 < 0 || tz.bn2 < 0 || tz.splitk1 < 0 || tz.splitk2 < 0 || tz.grid < 0 || tz.order < 0 ||
+      tz.order > MLP2_ORDER_SHUFFLED) {
+    fail(MLP2_ERR_UNSUPPORTED);
+    return nullptr;
+  }
+
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || !is_gfx950(dev)) { fail(MLP2_ERR_DEVICE); return nullptr; }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) { fail(MLP2_ERR_HIP); return nullptr; }
+
+  auto* p = new mlp2_plan_s();
+  p->M = M; p->H = H; p->F = F; p->act = act; p->device = dev;
+  p->num_cus = prop.multiProcessorCount;
+
+  // ---- tile choice: rows per block by regime, widest column blocks that divide
+  int bm = tz.bm ? tz.bm : (M <= 32 ? 32 : M <= 64 ? 64 : 128);
+  int bn1 = tz.bn1 ? tz.bn1 : ((nb == 1 && F % 128 == 0) ? 128 : 64);
+  int bn2 = tz.bn2 ? tz.bn2 : (H % 128 == 0 ? 128 : 64);
+  p->kc = KernelConfig{bm, bn1, bn2, nb};
+  if (F % bn1 || H % bn2 || !mlp2::config_supported(p->kc)) {
+    delete p;
+    fail(MLP2_ERR_UNSUPPORTED);
+    return nullptr;
+  }
+  p->Mb = ceil_div(M, bm);
+  p->Nb1 = (int)(F / bn1);
+  p->Nb2 = (int)(H / bn2);
+  const int tiles1 = p->Mb * p->Nb1, tiles2 = p->Mb * p->Nb2;
+  const int want = p->num_cus;  // enough items to give every CU one
+  if (tz.splitk1) {
+    p->kc1 = (int)align_up((size_t)ceil_div(H, tz.splitk1), mlp2::kBK);
+    p->S1 = ceil_div(H, p->kc1);
+  } else {
+    p->S1 = choose_split(H, tiles1, want, 256, &p->kc1);
+  }
+  if (tz.splitk2) {
+    p->kc2 = (int)align_up((size_t)ceil_div(F, tz.splitk2), mlp2::kBK);
+    p->S2 = ceil_div(F, p->kc2);
+  } else {
+    p->S2 = choose_split(F, tiles2, want, 256, &p->kc2);
+  }
+  p->items1 = tiles1 * p->S1;
+  p->items2 = tiles2 * p->S2;
+  p->order = tz.order;
+
+  int occ = 0;
+  if (mlp2::pipelined_occupancy(p->kc, &occ) != hipSuccess || occ < 1) {
+    delete p;
+    fail(MLP2_ERR_HIP);
+    return nullptr;
+  }
+  p->occupancy = occ;
+  p->grid = tz.grid ? tz.grid : std::min(occ * p->num_cus, p->items1 + p->items2);
+
+  // ---- workspace: Z, partials, counters, order table
+  const int64_t Mpad = (int64_t)p->Mb * bm;
+  size_t off = 0;
+  const size_t z_off = off;
+  off = align_up(off + (size_t)Mpad * F * 2, 256);
+  const size_t p1_off = off;
+  if (p->S1 > 1) off = align_up(off + (size_t)p->items1 * nb * bm * bn1 * 4, 256);
+  const size_t p2_off = off;
+  if (p->S2 > 1) off = align_up(off + (size_t)p->items2 * bm * bn2 * 4, 256);
+  const size_t cnt_off = off;
+  const size_t c1_off = off;
+  off = align_up(off + (size_t)tiles1 * 4, 256);
+  const size_t c2_off = off;
+  off = align_up(off + (size_t)tiles2 * 4, 256);
+  const size_t r_off = off;
+  off = align_up(off + (size_t)tiles1 * 4, 256);
+  const size_t ctrl_off = off;
+  off = align_up(off + mlp2::CTRL_WORDS * 4, 256);
+  const size_t cnt_end = off;
+  const size_t ord_off = off;
+  off = align_up(off + (size_t)p->items1 * 4, 256);
+  p->ws_bytes = off;
+  if (hipMalloc(&p->ws, p->ws_bytes) != hipSuccess) {
+    delete p;
+    fail(MLP2_ERR_HIP);
+    return nullptr;
+  }
+  char* b = (char*)p->ws;
+  p->Z = (uint16_t*)(b + z_off);
+  p->part1 = p->S1 > 1 ? (float*)(b + p1_off) : nullptr;
+  p->part2 = p->S2 > 1 ? (float*)(b + p2_off) : nullptr;
+  p->cnt1 = (uint32_t*)(b + c1_off);
+  p->cnt2 = (uint32_t*)(b + c2_off);
+  p->ready = (uint32_t*)(b + r_off);
+  p->ctrl = (uint32_t*)(b + ctrl_off);
+  p->order1 = (uint32_t*)(b + ord_off);
+  p->counters_off = cnt_off;
+  p->counters_bytes = cnt_end - cnt_off;
+  if (hipMemset(b + cnt_off, 0, cnt_end - cnt_off) != hipSuccess || hipMemset(p->Z, 0, (size_t)Mpad * F * 2) != hipSuccess ||
+      upload_order(p) != MLP2_OK || hipDeviceSynchronize() != hipSuccess) {
+    (void)hipFree(p->ws);
+    delete p;
+    fail(MLP2_ERR_HIP);
+    return nullptr;
+  }
+  return p;
+}
+
+mlp2_plan_t mlp2_plan(int64_t M, int64_t H, int64_t F, int act, int dtype) {
+  return mlp2_plan_ex(M, H, F, act, dtype, nullptr);
+}
+
+int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void* Y, void* stream, int mode) {
+  if (!p || !X || !W1 || !W2 || !Y) return fail(MLP2_ERR_INVALID_ARG);
+  if (mode != MLP2_MODE_SEQUENTIAL && mode != MLP2_MODE_TILE_PIPELINED) return fail(MLP2_ERR_INVALID_ARG);
+  if (((uintptr_t)X | (uintptr_t)W1 | (uintptr_t)W2 | (uintptr_t)Y) & 15u) return fail(MLP2_ERR_ALIGNMENT);
+  const int nb = p->act == MLP2_ACT_SWIGLU ? 2 : 1;
+  const size_t xb = (size_t)p->M * p->H * 2, w1b = (size_t)nb * p->H * p->F * 2, w2b = (size_t)p->F * p->H * 2;
+  if (overlaps(Y, xb, X, xb) || overlaps(Y, xb, W1, w1b) || overlaps(Y, xb, W2, w2b)) return fail(MLP2_ERR_INVALID_ARG);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != p->device) return fail(MLP2_ERR_DEVICE);
+
+  Args a;
+  a.X = (const uint16_t*)X;
+  a.W1 = (const uint16_t*)W1;
+  a.W2 = (const uint16_t*)W2;
+  a.Y = (uint16_t*)Y;
+  a.Z = p->Z;
+  a.part1 = p->part1;
+  a.part2 = p->part2;
+  a.cnt1 = p->cnt1;
+  a.cnt2 = p->cnt2;
+  a.ready = p->ready;
+  a.ctrl = p->ctrl;
+  a.order1 = p->order1;
+  a.M = (int)p->M;
+  a.H = (int)p->H;
+  a.F = (int)p->F;
+  a.act = p->act;
+  a.Mb = p->Mb;
+  a.Nb1 = p->Nb1;
+  a.Nb2 = p->Nb2;
+  a.S1 = p->S1;
+  a.S2 = p->S2;
+  a.kc1 = p->kc1;
+  a.kc2 = p->kc2;
+  a.items1 = p->items1;
+  a.items2 = p->items2;
+  a.bn1 = p->kc.bn1;
+  a.spin_limit = p->spin_limit;
+  a.drop_signal = p->drop_signal;
+
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t err = mode == MLP2_MODE_SEQUENTIAL ? mlp2::launch_sequential(p->kc, a, s)
+                                                : mlp2::launch_pipelined(p->kc, a, p->grid, s);
+  if (err != hipSuccess) return fail(MLP2_ERR_HIP);
+  return MLP2_OK;
+}
+
+void mlp2_destroy(mlp2_plan_t p) {
+  if (!p) return;
+  int cur = -1;
+  (void)hipGetDevice(&cur);
+  if (cur != p->device) (void)hipSetDevice(p->device);
+  (void)hipDeviceSynchronize();
+  (void)hipFree(p->ws);
+  if (cur != p->device && cur >= 0) (void)hipSetDevice(cur);
+  delete p;
+}
+
+int mlp2_check(mlp2_plan_t p) {
+  if (!p) return fail(MLP2_ERR_INVALID_ARG);
+  uint32_t ctrl[mlp2::CTRL_WORDS];
+  if (hipMemcpy(ctrl, p->ctrl, sizeof(ctrl), hipMemcpyDeviceToHost) != hipSuccess) return fail(MLP2_ERR_HIP);
+  if (ctrl[mlp2::CTRL_ERROR] == 0) return MLP2_OK;
+  // Recover: counters and epoch back to zero (the stream is idle by contract).
+  if (hipMemset((char*)p->ws + p->counters_off, 0, p->counters_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+    return fail(MLP2_ERR_HIP);
+  return fail(MLP2_ERR_TIMEOUT);
+}
+
+int mlp2_plan_info(mlp2_plan_t p, mlp2_info_t* out) {
+  if (!p || !out) return fail(MLP2_ERR_INVALID_ARG);
+  std::memset(out, 0, sizeof(*out));
+  out->M = p->M;
+  out->H = p->H;
+  out->F = p->F;
+  out->act = p->act;
+  out->bm = p->kc.bm;
+  out->bn1 = p->kc.bn1;
+  out->splitk1 = p->S1;
+  out->bn2 = p->kc.bn2;
+  out->splitk2 = p->S2;
+  out->bk = mlp2::kBK;
+  out->row_blocks = p->Mb;
+  out->col_blocks1 = p->Nb1;
+  out->col_blocks2 = p->Nb2;
+  out->items1 = p->items1;
+  out->items2 = p->items2;
+  out->grid_pipelined = p->grid;
+  out->occupancy = p->occupancy;
+  out->num_cus = p->num_cus;
+  out->order = p->order;
+  out->workspace_bytes = (int64_t)p->ws_bytes;
+  out->spin_limit = p->spin_limit;
+  return MLP2_OK;
+}
+
+const void* mlp2_intermediate(mlp2_plan_t p) { return p ? p->Z : nullptr; }
+
+int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
+  if (!p) return fail(MLP2_ERR_INVALID_ARG);
+  switch (key) {
+    case MLP2_OPT_SPIN_LIMIT:
+      if (value < 1 || value > 0xFFFFFFFFLL) return fail(MLP2_ERR_INVALID_ARG);
+      p->spin_limit = (uint32_t)value;
+      return MLP2_OK;
+    case MLP2_OPT_DROP_SIGNAL:
+      if (value < -1 || value >= (int64_t)p->Mb * p->Nb1) return fail(MLP2_ERR_INVALID_ARG);
+      p->drop_signal = (int)value;
+      return MLP2_OK;
+    case MLP2_OPT_ORDER:
+      if (value < MLP2_ORDER_COLUMN_FIRST || value > MLP2_ORDER_SHUFFLED) return fail(MLP2_ERR_INVALID_ARG);
+      p->order = (int)value;
+      if (hipDeviceSynchronize() != hipSuccess || upload_order(p) != MLP2_OK) return fail(MLP2_ERR_HIP);
+      return MLP2_OK;
+    case MLP2_OPT_GRID:
+      if (value < 1 || value > (1 << 20)) return fail(MLP2_ERR_INVALID_ARG);
+      p->grid = (int)value;
+      return MLP2_OK;
+    default:
+      return fail(MLP2_ERR_INVALID_ARG);
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,129 @@
+"""Parity of the HIP path with the fp64 oracle, through the C ABI.
+
+* every case runs both modes; Y must be within the elementwise bound
+  |Y - Y_ref| <= 2e-2 max|Y_ref| + 1e-3 and within the relative-RMS bar, and
+  the two modes must agree bit for bit on Y and on the intermediate Z;
+* small shapes span several tiles and a ragged row tail and are compared
+  element by element against the full oracle;
+* the five MLP workloads run at full size in the launch configuration the
+  bench times, compared on a seeded sample of rows the oracle computes one
+  by one (max|Y_ref| taken over the sample, which is stricter);
+* structural cases (identity and zero weights) must be bit-exact.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import mlp2_oracle as O
+from paper_2607_07862_amd import binding as B
+from paper_2607_07862_amd import inputs as I
+
+from _gpu import assert_bit_equal, assert_matches_oracle, both_modes, bits_of, device_inputs, run
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [
+    # M, H, F, act, tuning
+    (1, 64, 64, 0, None),
+    (7, 128, 192, 1, None),
+    (33, 192, 320, 2, None),
+    (100, 256, 384, 1, {"bm": 32}),
+    (255, 128, 256, 0, None),
+    (64, 512, 2048, 0, None),
+    (130, 256, 512, 1, {"bm": 128, "splitk1": 2, "splitk2": 3}),
+    (70, 320, 640, 2, {"bm": 64, "splitk1": 3, "splitk2": 2}),
+    (16, 1024, 1024, 1, {"splitk1": 4, "splitk2": 4, "bn1": 64, "bn2": 64}),
+    (200, 640, 1280, 1, {"bm": 128, "bn1": 128, "bn2": 128}),
+    (129, 256, 384, 2, {"bm": 128, "splitk1": 2}),
+]
+
+
+@pytest.mark.parametrize("M,H,F,act,tuning", SMALL, ids=[f"{c[0]}x{c[1]}x{c[2]}-a{c[3]}-{c[4]}" for c in SMALL])
+def test_small_shapes_against_full_oracle(lib, M, H, F, act, tuning):
+    d = I.make_inputs(M, H, F, act, seed=M * 7 + H + F)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, tuning)
+    Ys, Zs, Yp, Zp = both_modes(plan, g)
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
+    assert_matches_oracle(Yp, ref, "pipelined Y")
+    assert_matches_oracle(Ys, ref, "sequential Y")
+    assert_bit_equal(Ys, Yp, "Y sequential vs pipelined")
+    assert_bit_equal(Zs, Zp, "Z sequential vs pipelined")
+    zref = O.intermediate(I.bits(d["X"]), I.bits(d["W1"]), M, H, F, act)
+    assert_matches_oracle(Zp[:M], zref, "Z")
+    plan.close()
+
+
+def _workload_params():
+    return [pytest.param(k, id=k) for k in I.WORKLOAD_ORDER]
+
+
+_cache = {}
+
+
+@pytest.mark.parametrize("key", _workload_params())
+def test_workloads_full_size_sampled_rows(lib, key):
+    w = I.WORKLOADS[key]
+    print(f"\n[parity] workload {w.name} seed {w.seed}", flush=True)
+    d = I.workload_inputs(w)
+    g = device_inputs(d)
+    plan = B.Plan(w.M, w.H, w.F, w.act)
+    Ys, Zs, Yp, Zp = both_modes(plan, g)
+    assert_bit_equal(Ys, Yp, "Y sequential vs pipelined")
+    assert_bit_equal(Zs, Zp, "Z sequential vs pipelined")
+    rows = I.sample_rows(w.M, 24, w.seed)
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), w.M, w.H, w.F, w.act, rows=rows)
+    r = assert_matches_oracle(Yp[torch.as_tensor(rows, device="cuda")], ref, f"{w.name} sampled rows")
+    print(f"[parity] {w.name}: max_abs_err={r['max_abs_err']:.4g} bound={r['bound']:.4g} rel_rms={r['rel_rms']:.3g}")
+    zref = O.intermediate(I.bits(d["X"]), I.bits(d["W1"]), w.M, w.H, w.F, w.act, rows=rows)
+    assert_matches_oracle(Zp[torch.as_tensor(rows, device="cuda")], zref, f"{w.name} Z sampled rows")
+    plan.close()
+
+
+@pytest.mark.parametrize("act", [0, 1])
+@pytest.mark.parametrize("M", [37, 128])
+def test_identity_weights(lib, M, act):
+    """W1 = W2 = I: Y = X bit for bit (identity act); Y = bf16(gelu(X)) within the bound (GELU)."""
+    H = 256
+    d = I.make_inputs(M, H, H, act, seed=5)
+    eye = torch.eye(H, dtype=torch.bfloat16)
+    g = device_inputs({"X": d["X"], "W1": eye, "W2": eye.clone()})
+    plan = B.Plan(M, H, H, act, {"splitk1": 2, "splitk2": 2})
+    Ys, Zs, Yp, Zp = both_modes(plan, g)
+    assert_bit_equal(Ys, Yp, "Y modes")
+    if act == 0:
+        assert_bit_equal(Yp, g["X"], "Y vs X")
+    else:
+        ref = O.gelu_tanh(O.bf16_bits_to_f64(I.bits(d["X"])))
+        assert_matches_oracle(Yp, ref, "gelu(X)")
+    plan.close()
+
+
+@pytest.mark.parametrize("act", [0, 1, 2])
+def test_zero_weights_give_exact_zero(lib, act):
+    M, H, F = 50, 128, 256
+    d = I.make_inputs(M, H, F, act, seed=6)
+    n1 = 2 if act == 2 else 1
+    g = device_inputs({"X": d["X"], "W1": torch.zeros(n1, H, F, dtype=torch.bfloat16).reshape(d["W1"].shape),
+                       "W2": torch.zeros(F, H, dtype=torch.bfloat16)})
+    plan = B.Plan(M, H, F, act)
+    Ys, _, Yp, _ = both_modes(plan, g)
+    assert np.all(bits_of(Yp) == 0) and np.all(bits_of(Ys) == 0)
+    plan.close()
+
+
+def test_runs_on_a_side_stream(lib):
+    M, H, F, act = 96, 256, 512, 1
+    d = I.make_inputs(M, H, F, act, seed=8)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        Yp = run(plan, g, B.MODE_TILE_PIPELINED, stream=s)
+        Ys = run(plan, g, B.MODE_SEQUENTIAL, stream=s)
+    s.synchronize()
+    assert_bit_equal(Ys, Yp, "Y modes on a side stream")
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
+    assert_matches_oracle(Yp, ref, "side stream")
+    plan.close()

@@ -1,0 +1,117 @@
+"""The pipelining protocol on the GPU: ordering, counter lifetime, failure.
+
+* any GEMM1 tile order and any persistent grid size give the sequential
+  mode's bits (the consumer waits for exactly the producer tiles it reads;
+  Sec. III-A: a consumer runs once all its producers are complete);
+* runs that alternate inputs and modes never read a stale intermediate and
+  never see a counter from an earlier run (the ready counters, split-K
+  counters and the epoch carry over from run to run without host resets);
+* a dropped producer signal (failure injection from the host) makes the
+  bounded wait give up, every kernel still exits, mlp2_check reports the
+  timeout and the plan recovers.
+"""
+import pytest
+import torch
+
+from oracle import mlp2_oracle as O
+from paper_2607_07862_amd import binding as B
+from paper_2607_07862_amd import inputs as I
+
+from _gpu import assert_bit_equal, assert_matches_oracle, bits_of, device_inputs, run
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("order", [B.ORDER_ROW_FIRST, B.ORDER_REVERSED, B.ORDER_SHUFFLED, B.ORDER_COLUMN_FIRST])
+@pytest.mark.parametrize("grid", [1, 3, 17, 0])
+def test_orders_and_grids_match_sequential_bits(lib, order, grid):
+    M, H, F, act = 160, 256, 768, 1
+    d = I.make_inputs(M, H, F, act, seed=40 + order)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, {"bm": 64, "splitk1": 2, "splitk2": 3})
+    Ys = run(plan, g, B.MODE_SEQUENTIAL)
+    plan.set_option(B.OPT_ORDER, order)
+    if grid:
+        plan.set_option(B.OPT_GRID, grid)
+    Yp = run(plan, g, B.MODE_TILE_PIPELINED)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    assert_bit_equal(Ys, Yp, f"order {order} grid {grid}")
+    plan.close()
+
+
+@pytest.mark.parametrize("act", [0, 1, 2])
+def test_alternating_inputs_and_modes(lib, act):
+    M, H, F = 96, 256, 512
+    sets = [device_inputs(I.make_inputs(M, H, F, act, seed=60 + i)) for i in range(3)]
+    plan = B.Plan(M, H, F, act, {"bm": 32, "splitk1": 2, "splitk2": 2})
+    refs = []
+    for gi in sets:
+        refs.append(run(plan, gi, B.MODE_SEQUENTIAL).clone())
+    torch.cuda.synchronize()
+    outs = []
+    seq = [0, 1, 2, 2, 0, 1, 0, 0, 2, 1] * 3
+    for n, i in enumerate(seq):
+        mode = B.MODE_TILE_PIPELINED if n % 3 else B.MODE_SEQUENTIAL
+        outs.append((i, run(plan, sets[i], mode)))
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    for n, (i, y) in enumerate(outs):
+        assert_bit_equal(y, refs[i], f"run {n} (inputs {i})")
+    plan.close()
+
+
+def test_repeated_pipelined_runs_are_bit_stable(lib):
+    w = I.WORKLOADS["tiny"]
+    g = device_inputs(I.workload_inputs(w))
+    plan = B.Plan(w.M, w.H, w.F, w.act)
+    first = run(plan, g, B.MODE_TILE_PIPELINED).clone()
+    ys = [run(plan, g, B.MODE_TILE_PIPELINED) for _ in range(200)]
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    ref = bits_of(first)
+    for n, y in enumerate(ys):
+        assert (bits_of(y) == ref).all(), f"run {n}"
+    plan.close()
+
+
+def test_dropped_signal_times_out_and_recovers(lib):
+    M, H, F, act = 64, 128, 256, 1
+    d = I.make_inputs(M, H, F, act, seed=70)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act)
+    plan.set_option(B.OPT_SPIN_LIMIT, 2000)
+    plan.set_option(B.OPT_DROP_SIGNAL, 0)
+    run(plan, g, B.MODE_TILE_PIPELINED)
+    torch.cuda.synchronize()
+    assert plan.check() == B.ERR_TIMEOUT
+    # recovered: counters reset, the next runs are correct in both modes
+    plan.set_option(B.OPT_DROP_SIGNAL, -1)
+    plan.set_option(B.OPT_SPIN_LIMIT, 1 << 20)
+    Yp = run(plan, g, B.MODE_TILE_PIPELINED)
+    Ys = run(plan, g, B.MODE_SEQUENTIAL)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    assert_bit_equal(Ys, Yp, "after recovery")
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
+    assert_matches_oracle(Yp, ref, "after recovery")
+    plan.close()
+
+
+def test_run_argument_errors(lib):
+    M, H, F = 32, 64, 128
+    g = device_inputs(I.make_inputs(M, H, F, 0, seed=1))
+    plan = B.Plan(M, H, F, 0)
+    Y = torch.empty(M, H, dtype=torch.bfloat16, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    X, W1, W2, y = (t.data_ptr() for t in (g["X"], g["W1"], g["W2"], Y))
+    assert plan.run_raw(X, W1, W2, y, s, 2) == B.ERR_INVALID_ARG
+    assert plan.run_raw(X + 2, W1, W2, y, s, 0) == B.ERR_ALIGNMENT
+    assert plan.run_raw(X, W1, W2, X, s, 0) == B.ERR_INVALID_ARG  # Y aliases X
+    assert plan.run_raw(0, W1, W2, y, s, 0) == B.ERR_INVALID_ARG
+    with pytest.raises(ValueError):
+        plan.run(g["X"], g["W1"], g["W2"], torch.empty(M, H + 1, dtype=torch.bfloat16, device="cuda"), 0)
+    info = plan.info()
+    assert info["items1"] == info["row_blocks"] * info["col_blocks1"] * info["splitk1"]
+    assert info["grid_pipelined"] >= 1 and info["occupancy"] >= 1
+    plan.close()
