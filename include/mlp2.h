@@ -83,9 +83,10 @@ typedef struct mlp2_tuning {
   int splitk1;   /* GEMM1 split-K factor (>= 1)                                           */
   int bn2;       /* GEMM2 column-block width: 64 or 128                                   */
   int splitk2;   /* GEMM2 split-K factor (>= 1)                                           */
-  int grid;      /* persistent grid of the pipelined launch (work-groups)                 */
+  int grid;      /* persistent grid of every launch (>= max(splitk1, splitk2))            */
   int order;     /* enum mlp2_order                                                       */
-  int reserved[7];
+  int stages;    /* LDS ring depth of the tile mainloop (2, 3 or 4)                       */
+  int reserved[6];
 } mlp2_tuning_t;
 
 /* What a plan chose, for reports and tests. */
@@ -96,14 +97,17 @@ typedef struct mlp2_info {
   int row_blocks;        /* ceil(M / bm)                                    */
   int col_blocks1;       /* F / bn1                                         */
   int col_blocks2;       /* H / bn2                                         */
-  int items1, items2;    /* GEMM1 work items (tiles x splitk1), GEMM2 items */
+  int items1, items2;    /* GEMM1 / GEMM2 split items (tiles x splitk)       */
   int grid_pipelined;    /* persistent work-groups of the pipelined launch  */
   int occupancy;         /* resident work-groups per CU of that kernel      */
   int num_cus;
   int order;
   int64_t workspace_bytes;
   uint32_t spin_limit;
-  int reserved[8];
+  int stages;            /* LDS ring depth                                  */
+  int grid_gemm1;        /* persistent work-groups of the GEMM1 launch      */
+  int grid_gemm2;        /* persistent work-groups of the GEMM2 launch      */
+  int reserved[5];
 } mlp2_info_t;
 
 /* Create a plan for Y[M,H] = act(X[M,H] . W1) . W2 on the current HIP device.
@@ -151,7 +155,9 @@ const void* mlp2_intermediate(mlp2_plan_t plan);
  *   MLP2_OPT_SPIN_LIMIT   polls before a flag wait gives up (default ~1 s of polling)
  *   MLP2_OPT_DROP_SIGNAL  GEMM1 tile index whose ready signal is skipped (-1 = none)
  *   MLP2_OPT_ORDER        enum mlp2_order (rebuilds the order table)
- *   MLP2_OPT_GRID         persistent grid size of the pipelined launch (>= 1)
+ *   MLP2_OPT_GRID         persistent grid of every launch (0 = automatic; else at
+ *                         least max(splitk1, splitk2), since split-K parts wait
+ *                         for their siblings)
  * Returns MLP2_OK or MLP2_ERR_INVALID_ARG. */
 enum mlp2_option { MLP2_OPT_SPIN_LIMIT = 1, MLP2_OPT_DROP_SIGNAL = 2, MLP2_OPT_ORDER = 3, MLP2_OPT_GRID = 4 };
 int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);

@@ -46,7 +46,8 @@ class Tuning(ctypes.Structure):
         ("splitk2", ctypes.c_int),
         ("grid", ctypes.c_int),
         ("order", ctypes.c_int),
-        ("reserved", ctypes.c_int * 7),
+        ("stages", ctypes.c_int),
+        ("reserved", ctypes.c_int * 6),
     ]
 
 
@@ -73,7 +74,10 @@ class Info(ctypes.Structure):
         ("order", ctypes.c_int),
         ("workspace_bytes", ctypes.c_int64),
         ("spin_limit", ctypes.c_uint32),
-        ("reserved", ctypes.c_int * 8),
+        ("stages", ctypes.c_int),
+        ("grid_gemm1", ctypes.c_int),
+        ("grid_gemm2", ctypes.c_int),
+        ("reserved", ctypes.c_int * 5),
     ]
 
 

@@ -29,7 +29,8 @@ struct mlp2_plan_s {
   int Mb = 0, Nb1 = 0, Nb2 = 0;
   int S1 = 1, S2 = 1, kc1 = 0, kc2 = 0;
   int items1 = 0, items2 = 0;
-  int grid = 0, occupancy = 0, num_cus = 0;
+  int grid = 0, grid1 = 0, grid2 = 0, occupancy = 0, num_cus = 0;
+  int grid_override = 0;
   int order = MLP2_ORDER_COLUMN_FIRST;
   uint32_t spin_limit = 1u << 20;
   int drop_signal = -1;
@@ -71,38 +72,35 @@ int choose_split(int64_t K, int tiles, int want, int min_k, int* kc) {
   return ceil_div(K, k);
 }
 
+// GEMM1 item order of the pipelined launch.  Items are id = tile * S1 + s with
+// tile = nb * Mb + mb.  Every policy orders *tiles* and keeps the S1 parts of
+// a tile adjacent: split-K parts wait for their siblings, and adjacency (with
+// a grid of at least S1 work-groups) is what keeps the launch deadlock-free.
 void build_order(mlp2_plan_s* p, std::vector<uint32_t>& out) {
-  // Item ids: id = tile * S1 + s with tile = nb * Mb + mb.
-  const int n = p->items1;
-  out.resize(n);
-  std::iota(out.begin(), out.end(), 0u);  // column-block-first
+  std::vector<uint32_t> tiles;
+  tiles.reserve((size_t)p->Mb * p->Nb1);
   switch (p->order) {
-    case MLP2_ORDER_ROW_FIRST: {
-      std::vector<uint32_t> v;
-      v.reserve(n);
+    case MLP2_ORDER_ROW_FIRST:
       for (int mb = 0; mb < p->Mb; ++mb)
-        for (int nb = 0; nb < p->Nb1; ++nb)
-          for (int s = 0; s < p->S1; ++s) v.push_back((uint32_t)((nb * p->Mb + mb) * p->S1 + s));
-      out.swap(v);
+        for (int nb = 0; nb < p->Nb1; ++nb) tiles.push_back((uint32_t)(nb * p->Mb + mb));
       break;
-    }
-    case MLP2_ORDER_REVERSED: {
-      std::vector<uint32_t> v;
-      v.reserve(n);
+    case MLP2_ORDER_REVERSED:
       for (int nb = p->Nb1 - 1; nb >= 0; --nb)
-        for (int mb = 0; mb < p->Mb; ++mb)
-          for (int s = 0; s < p->S1; ++s) v.push_back((uint32_t)((nb * p->Mb + mb) * p->S1 + s));
-      out.swap(v);
+        for (int mb = 0; mb < p->Mb; ++mb) tiles.push_back((uint32_t)(nb * p->Mb + mb));
       break;
-    }
-    case MLP2_ORDER_SHUFFLED: {
-      std::mt19937 rng(12345u);
-      std::shuffle(out.begin(), out.end(), rng);
-      break;
-    }
-    default:
+    default:  // column-block-first (also the base of the shuffled order)
+      for (int nb = 0; nb < p->Nb1; ++nb)
+        for (int mb = 0; mb < p->Mb; ++mb) tiles.push_back((uint32_t)(nb * p->Mb + mb));
+      if (p->order == MLP2_ORDER_SHUFFLED) {
+        std::mt19937 rng(12345u);
+        std::shuffle(tiles.begin(), tiles.end(), rng);
+      }
       break;
   }
+  out.clear();
+  out.reserve(tiles.size() * p->S1);
+  for (uint32_t t : tiles)
+    for (int s = 0; s < p->S1; ++s) out.push_back(t * (uint32_t)p->S1 + (uint32_t)s);
 }
 
 bool is_gfx950(int dev) {
@@ -156,7 +154,7 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   mlp2_tuning_t tz;
   std::memset(&tz, 0, sizeof(tz));
   if (t) tz = *t;
-  if (tz.bm < 0 || tz.bn1 < 0 || tz.bn2 < 0 || tz.splitk1 < 0 || tz.splitk2 < 0 || tz.grid < 0 || tz.order < 0 ||
+  if (tz.bm < 0 || tz.bn1 < 0 || tz.bn2 < 0 || tz.splitk1 < 0 || tz.splitk2 < 0 || tz.grid < 0 || tz.order < 0 || tz.stages < 0 ||
       tz.order > MLP2_ORDER_SHUFFLED) {
     fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
@@ -175,7 +173,8 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   int bm = tz.bm ? tz.bm : (M <= 32 ? 32 : M <= 64 ? 64 : 128);
   int bn1 = tz.bn1 ? tz.bn1 : ((nb == 1 && F % 128 == 0) ? 128 : 64);
   int bn2 = tz.bn2 ? tz.bn2 : (H % 128 == 0 ? 128 : 64);
-  p->kc = KernelConfig{bm, bn1, bn2, nb};
+  const int ns = tz.stages ? tz.stages : 4;
+  p->kc = KernelConfig{bm, bn1, bn2, nb, ns};
   if (F % bn1 || H % bn2 || !mlp2::config_supported(p->kc)) {
     delete p;
     fail(MLP2_ERR_UNSUPPORTED);
@@ -198,18 +197,30 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   } else {
     p->S2 = choose_split(F, tiles2, want, 256, &p->kc2);
   }
+  p->order = tz.order;
   p->items1 = tiles1 * p->S1;
   p->items2 = tiles2 * p->S2;
-  p->order = tz.order;
-
-  int occ = 0;
-  if (mlp2::pipelined_occupancy(p->kc, &occ) != hipSuccess || occ < 1) {
+  // split-K parts wait for their siblings: every launch needs >= max(S1, S2) work-groups
+  const int min_grid = std::max(p->S1, p->S2);
+  if (tz.grid && tz.grid < min_grid) {
     delete p;
-    fail(MLP2_ERR_HIP);
+    fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
   }
-  p->occupancy = occ;
-  p->grid = tz.grid ? tz.grid : std::min(occ * p->num_cus, p->items1 + p->items2);
+
+  int occ[3] = {0, 0, 0};
+  for (int w = 0; w < 3; ++w) {
+    if (mlp2::occupancy(p->kc, w, &occ[w]) != hipSuccess || occ[w] < 1) {
+      delete p;
+      fail(MLP2_ERR_HIP);
+      return nullptr;
+    }
+  }
+  p->occupancy = occ[2];
+  p->grid_override = tz.grid;
+  p->grid1 = std::max(min_grid, std::min(occ[0] * p->num_cus, p->items1));
+  p->grid2 = std::max(min_grid, std::min(occ[1] * p->num_cus, p->items2));
+  p->grid = std::max(min_grid, std::min(occ[2] * p->num_cus, p->items1 + p->items2));
 
   // ---- workspace: Z, partials, counters, order table
   const int64_t Mpad = (int64_t)p->Mb * bm;
@@ -304,8 +315,10 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   a.drop_signal = p->drop_signal;
 
   hipStream_t s = (hipStream_t)stream;
-  hipError_t err = mode == MLP2_MODE_SEQUENTIAL ? mlp2::launch_sequential(p->kc, a, s)
-                                                : mlp2::launch_pipelined(p->kc, a, p->grid, s);
+  const int go = p->grid_override;
+  const int grids[2] = {go ? go : p->grid1, go ? go : p->grid2};
+  hipError_t err = mode == MLP2_MODE_SEQUENTIAL ? mlp2::launch_sequential(p->kc, a, grids, s)
+                                                : mlp2::launch_pipelined(p->kc, a, go ? go : p->grid, s);
   if (err != hipSuccess) return fail(MLP2_ERR_HIP);
   return MLP2_OK;
 }
@@ -345,12 +358,15 @@ int mlp2_plan_info(mlp2_plan_t p, mlp2_info_t* out) {
   out->bn2 = p->kc.bn2;
   out->splitk2 = p->S2;
   out->bk = mlp2::kBK;
+  out->stages = p->kc.ns;
   out->row_blocks = p->Mb;
   out->col_blocks1 = p->Nb1;
   out->col_blocks2 = p->Nb2;
   out->items1 = p->items1;
   out->items2 = p->items2;
-  out->grid_pipelined = p->grid;
+  out->grid_pipelined = p->grid_override ? p->grid_override : p->grid;
+  out->grid_gemm1 = p->grid_override ? p->grid_override : p->grid1;
+  out->grid_gemm2 = p->grid_override ? p->grid_override : p->grid2;
   out->occupancy = p->occupancy;
   out->num_cus = p->num_cus;
   out->order = p->order;
@@ -378,8 +394,10 @@ int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
       if (hipDeviceSynchronize() != hipSuccess || upload_order(p) != MLP2_OK) return fail(MLP2_ERR_HIP);
       return MLP2_OK;
     case MLP2_OPT_GRID:
-      if (value < 1 || value > (1 << 20)) return fail(MLP2_ERR_INVALID_ARG);
-      p->grid = (int)value;
+      // 0 = automatic; otherwise at least one work-group per split-K part of a tile
+      if (value < 0 || value > (1 << 20) || (value > 0 && value < std::max(p->S1, p->S2)))
+        return fail(MLP2_ERR_INVALID_ARG);
+      p->grid_override = (int)value;
       return MLP2_OK;
     default:
       return fail(MLP2_ERR_INVALID_ARG);

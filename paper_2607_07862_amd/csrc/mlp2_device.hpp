@@ -53,7 +53,7 @@ struct Args {
   int Mb, Nb1, Nb2;        // row blocks; GEMM1 / GEMM2 column blocks
   int S1, S2;              // split-K factors
   int kc1, kc2;            // K per split (multiples of kBK)
-  int items1, items2;
+  int items1, items2;      // GEMM1 / GEMM2 work items (tiles x split-K parts)
   int bn1;                 // GEMM1 column-block width (ready-counter granularity along GEMM2's K)
   uint32_t spin_limit;
   int drop_signal;         // GEMM1 tile whose signal is skipped (failure injection), -1 = none
@@ -103,34 +103,69 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 // ------------------------------------------------------------------ tile geometry
 
 // A work-group tile of BM rows (the M side: X or Z rows) by BN columns (the N
-// side: W columns).  Four waves in a WM x WN grid; each wave owns a
-// (BM/WM) x (BN/WN) sub-tile made of 16x16 MFMA blocks.
+// side: W columns), staged through an NS-deep ring of LDS buffers of kBK rows
+// of K each.  Four waves in a WM x WN grid; each wave owns a (BM/WM) x
+// (BN/WN) sub-tile made of 16x16 MFMA blocks.
 //
 // The MFMA is issued with the *weight* fragment as its A operand and the
 // activation fragment as its B operand, so each lane ends up holding output
 // row (lane % 16) and, for a pair of adjacent blocks, 8 consecutive output
 // columns: the epilogue stores 16 contiguous bytes per lane.
-template <int BM_, int BN_, int WM_, int WN_>
+//
+// LDS stage layout (bytes), both parts unpadded and XOR-swizzled in 16-byte
+// chunks, because the direct-to-LDS loads write each wave's 1 KB contiguously
+// (lane i -> bytes 16 i):
+//   activation tile [BM][kBK] bf16, rows of 128 B: chunk c of row r sits at
+//     position c ^ ((r >> 1) & 7), so the 16 rows read by one ds_read_b128
+//     group land in 16 distinct 4-bank groups;
+//   weight tile [kBK][BN] bf16 per operand: chunk c of row k at c ^ swzB(k),
+//     which puts the 4 rows read by one ds_read_b64_tr_b16 group in
+//     different banks.
+template <int BM_, int BN_, int WM_, int WN_, int NS_>
 struct Tile {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NS = NS_;
   static_assert(WM * WN == 4, "four waves");
+  static_assert(BN == 64 || BN == 128 || BN == 256, "weight tile width");
+  static_assert(NS >= 2, "at least double buffered");
   static constexpr int MW = BM / WM;  // rows per wave
   static constexpr int NW = BN / WN;  // columns per wave
   static constexpr int TM = MW / 16;
   static constexpr int TN = NW / 16;
   static_assert(TM >= 1 && TN >= 2 && TN % 2 == 0, "wave tile shape");
-  static constexpr int A_STRIDE = kBK + 8;  // LDS row of the activation tile [BM][kBK], padded
-  static constexpr int B_STRIDE = BN + 16;  // LDS row of the weight tile [kBK][BN], padded
-  static constexpr int A_ELEMS = BM * A_STRIDE;
-  static constexpr int B_ELEMS = kBK * B_STRIDE;
-  static constexpr int A_CHUNKS = BM * kBK / 8 / kThreads;  // 16-byte loads per thread
-  static constexpr int B_CHUNKS = kBK * BN / 8 / kThreads;
-  static_assert(A_CHUNKS >= 1 && B_CHUNKS >= 1, "tile too small for 256 threads");
+  static constexpr int A_BYTES = BM * kBK * 2;
+  static constexpr int B_BYTES = kBK * BN * 2;
+  static constexpr int A_DMA = A_BYTES / 1024 / 4;  // 1 KB wave loads per wave and stage
+  static constexpr int B_DMA = B_BYTES / 1024 / 4;
+  static_assert(A_DMA >= 1 && B_DMA >= 1, "tile too small for four waves");
   template <int NB>
-  static constexpr int stage_elems() { return A_ELEMS + NB * B_ELEMS; }
+  static constexpr int stage_bytes() { return A_BYTES + NB * B_BYTES; }
   template <int NB>
-  static constexpr int lds_elems() { return 2 * stage_elems<NB>(); }
+  static constexpr int lds_bytes() { return NS * stage_bytes<NB>(); }
+  template <int NB>
+  static constexpr int dma_per_stage() { return A_DMA + NB * B_DMA; }
 };
+
+__device__ __forceinline__ int swz_a(int row) { return (row >> 1) & 7; }
+template <int BN>
+__device__ __forceinline__ int swz_b(int k) {
+  return BN >= 128 ? 4 * (k & 3) : 4 * ((k >> 1) & 1);
+}
+
+// One 16-byte-per-lane direct-to-LDS load: lane i reads 16 bytes at
+// base + voff and writes them to LDS at lds_addr + 16 i.  Issued through
+// inline assembly so that the compiler does not serialise every LDS read
+// behind it (it cannot tell the ring's stages apart); completion is tracked
+// explicitly with s_waitcnt vmcnt.  M0 carries the LDS address; the kernels
+// use M0 for nothing else.
+__device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base) : "memory");
+}
+
+// Wait until at most n of this wave's vector-memory operations are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 // ------------------------------------------------------------------ mainloop
 
@@ -138,14 +173,20 @@ struct NoWait {
   __device__ __forceinline__ void operator()(int) {}
 };
 
-// acc[b][tn][tm] += sum over k in [kbeg, kend) of W_b[k][n] * A[m][k] for the
+// acc[b][tn][tm] = sum over k in [kbeg, kend) of W_b[k][n] * A[m][k] for the
 // tile at (m0, n0).  A rows past `mlast` are clamped to `mlast` (their results
-// are never stored).  `wait(k)` runs before the activation operand of the
-// stage starting at k is loaded (after its weight loads were issued).
+// are never stored).  `wait(k)` runs, in every wave, before the activation
+// operand of the stage starting at k is requested (after its weight loads).
+//
+// Pipeline: stages k0, k0 + kBK, ... are loaded NS - 1 ahead of use.  At
+// iteration it a wave waits for its own loads of stage it, a barrier makes
+// every wave's loads of stage it visible and retires every wave's reads of
+// stage it - 1, then the loads of stage it + NS - 1 go into that freed buffer
+// and stage it is multiplied.
 template <class T, int NB, class Wait>
 __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long lda, int m0, int mlast,
                                          const uint16_t* const (&Bp)[NB], long ldb, int n0, int kbeg, int kend,
-                                         f32x4 (&acc)[NB][T::TN][T::TM], uint16_t* lds, Wait& wait) {
+                                         f32x4 (&acc)[NB][T::TN][T::TM], char* lds, Wait& wait) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -162,79 +203,81 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   const int nk = (kend - kbeg) / kBK;
   if (nk <= 0) return;
 
-  // global -> register staging
-  u32x4 ra[T::A_CHUNKS];
-  u32x4 rb[NB][T::B_CHUNKS];
-  const uint16_t* a_src[T::A_CHUNKS];
-  int a_lds[T::A_CHUNKS];
+  const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
+  constexpr int SB = T::template stage_bytes<NB>();
+  constexpr int PER_STAGE = T::template dma_per_stage<NB>();
+
+  // DMA source offsets (bytes, relative to the tensor bases) at k = 0.
+  uint32_t a_off[T::A_DMA];
 #pragma unroll
-  for (int i = 0; i < T::A_CHUNKS; ++i) {
-    const int q = tid + kThreads * i;
-    const int row = q >> 3, c8 = q & 7;
+  for (int j = 0; j < T::A_DMA; ++j) {
+    const int ch = wave + 4 * j;  // 1 KB chunk = 8 rows of 128 B
+    const int row = 8 * ch + (lane >> 3);
+    const int lc = (lane & 7) ^ swz_a(row);
     int gr = m0 + row;
     gr = gr > mlast ? mlast : gr;
-    a_src[i] = A + (long)gr * lda + c8 * 8;
-    a_lds[i] = row * T::A_STRIDE + c8 * 8;
+    a_off[j] = (uint32_t)(((long)gr * lda + 8 * lc) * 2);
   }
-  constexpr int BC = T::BN / 8;  // 16-byte chunks per weight row
-  long b_off[T::B_CHUNKS];
-  int b_lds[T::B_CHUNKS];
+  constexpr int CPR = T::BN / 8;      // 16-byte chunks per weight row
+  constexpr int RPC = 64 / CPR;       // weight rows per 1 KB chunk
+  uint32_t b_off[T::B_DMA];
 #pragma unroll
-  for (int i = 0; i < T::B_CHUNKS; ++i) {
-    const int q = tid + kThreads * i;
-    const int row = q / BC, c8 = q % BC;
-    b_off[i] = (long)row * ldb + n0 + c8 * 8;
-    b_lds[i] = row * T::B_STRIDE + c8 * 8;
+  for (int j = 0; j < T::B_DMA; ++j) {
+    const int ch = wave + 4 * j;
+    const int row = RPC * ch + lane / CPR;
+    const int lc = (lane % CPR) ^ swz_b<T::BN>(row);
+    b_off[j] = (uint32_t)(((long)row * ldb + n0 + 8 * lc) * 2);
   }
 
-  auto gload = [&](int k) {
+  auto issue = [&](int st) {
+    const int k = kbeg + st * kBK;
+    const uint32_t sbase = lds_base + (uint32_t)((st % T::NS) * SB);
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int i = 0; i < T::B_CHUNKS; ++i)
-        rb[b][i] = *reinterpret_cast<const u32x4*>(Bp[b] + (long)k * ldb + b_off[i]);
+      for (int j = 0; j < T::B_DMA; ++j)
+        dma16(Bp[b], b_off[j] + (uint32_t)((long)k * ldb * 2),
+              uniform(sbase + (uint32_t)(T::A_BYTES + b * T::B_BYTES + (wave + 4 * j) * 1024)));
     wait(k);
 #pragma unroll
-    for (int i = 0; i < T::A_CHUNKS; ++i) ra[i] = *reinterpret_cast<const u32x4*>(a_src[i] + k);
-  };
-  auto sstore = [&](int s) {
-    uint16_t* base = lds + s * T::template stage_elems<NB>();
-#pragma unroll
-    for (int i = 0; i < T::A_CHUNKS; ++i) *reinterpret_cast<u32x4*>(base + a_lds[i]) = ra[i];
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int i = 0; i < T::B_CHUNKS; ++i)
-        *reinterpret_cast<u32x4*>(base + T::A_ELEMS + b * T::B_ELEMS + b_lds[i]) = rb[b][i];
+    for (int j = 0; j < T::A_DMA; ++j)
+      dma16(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + 4 * j) * 1024)));
   };
 
-  // Fragment addressing inside a stage.
+  // Fragment addressing (bytes inside a stage).
   //   activation (MFMA B operand): lane holds A[row = l%16][k = 8(l/16) .. +7]  -> ds_read_b128
   //   weight (MFMA A operand): ds_read_b64_tr_b16 over 4 rows x 4 chunks per 16-lane group;
   //     lane 4r+c of group g addresses row 8g+r (+4 for the upper half), columns 8c + 4*t2 .. +3,
   //     and receives column (8*(i/4) + 4*t2 + i%4) of those 4 rows, i = lane % 16.
-  const int a_frag = (wm * T::MW + (lane & 15)) * T::A_STRIDE + 8 * (lane >> 4);
+  const int arow = wm * T::MW + (lane & 15);
+  const int a_frag0 = arow * 128 + (((lane >> 4) ^ swz_a(arow)) << 4);          // ks = 0
+  const int a_frag1 = arow * 128 + (((4 + (lane >> 4)) ^ swz_a(arow)) << 4);    // ks = 1
   const int g = lane >> 4, r4 = (lane & 15) >> 2, c4 = lane & 3;
-  const int b_frag = (8 * g + r4) * T::B_STRIDE + wn * T::NW + 8 * c4;
+  const int brow = 8 * g + r4;
+  int b_frag[T::TN / 2];
+#pragma unroll
+  for (int tp = 0; tp < T::TN / 2; ++tp) {
+    const int q = ((wn * T::NW + 32 * tp) >> 3) + c4;
+    b_frag[tp] = T::A_BYTES + brow * (2 * T::BN) + ((q ^ swz_b<T::BN>(brow)) << 4);
+  }
 
-  auto compute = [&](int s) {
-    const uint16_t* base = lds + s * T::template stage_elems<NB>();
+  auto compute = [&](int st) {
+    const char* base = lds + (st % T::NS) * SB;
 #pragma unroll
     for (int ks = 0; ks < kBK / 32; ++ks) {
       bf16x8 xf[T::TM];
 #pragma unroll
       for (int tm = 0; tm < T::TM; ++tm)
-        xf[tm] = *reinterpret_cast<const bf16x8*>(base + a_frag + tm * 16 * T::A_STRIDE + ks * 32);
+        xf[tm] = *reinterpret_cast<const bf16x8*>(base + (ks ? a_frag1 : a_frag0) + tm * 16 * 128);
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        const uint16_t* bb = base + T::A_ELEMS + b * T::B_ELEMS + b_frag + ks * 32 * T::B_STRIDE;
 #pragma unroll
         for (int tp = 0; tp < T::TN / 2; ++tp) {
 #pragma unroll
           for (int t2 = 0; t2 < 2; ++t2) {
-            const uint16_t* p = bb + tp * 32 + t2 * 4;
+            const char* p = base + b * T::B_BYTES + b_frag[tp] + ks * 32 * (2 * T::BN) + t2 * 8;
             bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p));
-            bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p + 4 * T::B_STRIDE));
+            bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p + 4 * (2 * T::BN)));
             bf16x8 wf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
             for (int tm = 0; tm < T::TM; ++tm)
@@ -245,16 +288,29 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     }
   };
 
-  gload(kbeg);
-  sstore(0);
-  __syncthreads();
+  // Prologue: NS - 1 stages in flight.
+#pragma unroll
+  for (int st = 0; st < T::NS - 1; ++st)
+    if (st < nk) issue(st);
+
   for (int it = 0; it < nk; ++it) {
-    const int s = it & 1;
-    if (it + 1 < nk) gload(kbeg + (it + 1) * kBK);
-    compute(s);
-    if (it + 1 < nk) sstore(s ^ 1);
+    // Own loads of stage `it` complete: the stages issued after it may stay in flight.
+    const int after = min(T::NS - 2, nk - 1 - it);
+    if constexpr (T::NS >= 4) {
+      if (after >= 2) wait_vm<2 * PER_STAGE>();
+      else if (after == 1) wait_vm<PER_STAGE>();
+      else wait_vm<0>();
+    } else if constexpr (T::NS == 3) {
+      if (after >= 1) wait_vm<PER_STAGE>();
+      else wait_vm<0>();
+    } else {
+      wait_vm<0>();
+    }
     __syncthreads();
+    if (it + T::NS - 1 < nk) issue(it + T::NS - 1);
+    compute(it);
   }
+  __syncthreads();  // every wave is done reading the ring before it is reused
 }
 
 // ------------------------------------------------------------------ fragment <-> tile coordinates
@@ -283,24 +339,30 @@ __device__ __forceinline__ void pair_values(const f32x4 (&a)[T::TN][T::TM], int 
 
 // ------------------------------------------------------------------ split-K partials
 //
-// Partials are stored fragment-native: for work item (tile, split s) each
-// wave writes its accumulators as contiguous 1 KB runs (64 lanes x 16 bytes),
-// so the writes and the reducer's reads are fully coalesced.  The reducer of a
-// tile has the same lane <-> element mapping as every split.
+// With split-K, a tile's K range is cut into S parts computed by separate
+// work items.  Each part stores its fp32 accumulators "fragment-native": lane
+// l of wave w writes its f32x4 of block i at ((tile*S + s)*PER_ITEM +
+// (w*PER_WAVE + i)*64 + l), so writes and reads are fully coalesced 1 KB runs.
+// The reduction is spread over the S parts themselves, in "units" (a wave's
+// pair of adjacent 16x16 blocks in one row block, for every weight operand):
+// once all S parts have arrived each part adds up its share of the units in
+// the fixed order s = 0, 1, ..., S-1 and runs their epilogue.  The order of
+// the adds never depends on which part finished last.
 
 template <class T, int NB>
 struct Partial {
-  static constexpr int PER_WAVE = NB * T::TN * T::TM;            // f32x4 per lane
-  static constexpr long PER_ITEM = 4L * PER_WAVE * 64;            // f32x4 per (tile, split)
-  __device__ static f32x4* at(float* base, long tile, int S, int s) {
-    return reinterpret_cast<f32x4*>(base) + (tile * S + s) * PER_ITEM + (long)(threadIdx.x >> 6) * PER_WAVE * 64 +
-           (threadIdx.x & 63);
+  static constexpr int PER_WAVE = NB * T::TN * T::TM;  // f32x4 per lane
+  static constexpr long PER_ITEM = 4L * PER_WAVE * 64;  // f32x4 per (tile, split)
+  static constexpr int UNITS = 4 * T::TM * (T::TN / 2); // (wave, tm, tp) triples per tile
+  __device__ static long block_index(long tile, int S, int s, int w, int b, int tn, int tm) {
+    return (tile * S + s) * PER_ITEM + ((long)w * PER_WAVE + ((b * T::TN + tn) * T::TM + tm)) * 64;
   }
 };
 
 template <class T, int NB>
 __device__ __forceinline__ void store_partial(float* base, long tile, int S, int s, const f32x4 (&acc)[NB][T::TN][T::TM]) {
-  f32x4* p = Partial<T, NB>::at(base, tile, S, s);
+  f32x4* p = reinterpret_cast<f32x4*>(base) + Partial<T, NB>::block_index(tile, S, s, threadIdx.x >> 6, 0, 0, 0) +
+             (threadIdx.x & 63);
   int i = 0;
 #pragma unroll
   for (int b = 0; b < NB; ++b)
@@ -310,88 +372,163 @@ __device__ __forceinline__ void store_partial(float* base, long tile, int S, int
       for (int tm = 0; tm < T::TM; ++tm, ++i) p[i * 64] = acc[b][tn][tm];
 }
 
-// acc = sum over s = 0 .. S-1 of partial s, in that order (fixed, so the result
-// does not depend on which split arrived last).
+// A reduction unit: wave w's blocks (2 tp, tm) and (2 tp + 1, tm).
+template <class T>
+struct Unit {
+  int w, tm, tp;
+  __device__ explicit Unit(int u) {
+    constexpr int per_wave = T::TM * (T::TN / 2);
+    w = u / per_wave;
+    const int r = u - w * per_wave;
+    tm = r / (T::TN / 2);
+    tp = r - tm * (T::TN / 2);
+  }
+  // Output row and first of the 8 consecutive columns held by `lane` of this unit.
+  __device__ int row(int m0, int lane) const { return m0 + (w % T::WM) * T::MW + 16 * tm + (lane & 15); }
+  __device__ int col(int n0, int lane) const { return n0 + (w / T::WM) * T::NW + 32 * tp + 8 * (lane >> 4); }
+};
+
+// v[b][0..7] = sum over s = 0 .. S-1 (in that order) of the unit's 8 values for
+// weight operand b, as held by `lane` (the same layout pair_values produces).
 template <class T, int NB>
-__device__ __forceinline__ void reduce_partials(const float* base, long tile, int S, f32x4 (&acc)[NB][T::TN][T::TM]) {
+__device__ __forceinline__ void reduce_unit(const float* base, long tile, int S, const Unit<T>& u, int lane,
+                                            float (&v)[NB][8]) {
+  const f32x4* p = reinterpret_cast<const f32x4*>(base);
 #pragma unroll
   for (int b = 0; b < NB; ++b)
 #pragma unroll
-    for (int tn = 0; tn < T::TN; ++tn)
+    for (int i = 0; i < 8; ++i) v[b][i] = 0.f;
+  int s = 0;
+  // two parts per round: their loads are in flight together
+  for (; s + 2 <= S; s += 2) {
+    f32x4 q[2][NB][2];
 #pragma unroll
-      for (int tm = 0; tm < T::TM; ++tm) acc[b][tn][tm] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < S; ++s) {
-    const f32x4* p = Partial<T, NB>::at(const_cast<float*>(base), tile, S, s);
-    int i = 0;
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
+      for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int tn = 0; tn < T::TN; ++tn)
+        for (int t2 = 0; t2 < 2; ++t2)
+          q[h][b][t2] = p[Partial<T, NB>::block_index(tile, S, s + h, u.w, b, 2 * u.tp + t2, u.tm) + lane];
 #pragma unroll
-        for (int tm = 0; tm < T::TM; ++tm, ++i) acc[b][tn][tm] += p[i * 64];
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[b][r] += q[h][b][0][r];
+          v[b][4 + r] += q[h][b][1][r];
+        }
+  }
+  if (s < S) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const f32x4 q0 = p[Partial<T, NB>::block_index(tile, S, s, u.w, b, 2 * u.tp, u.tm) + lane];
+      const f32x4 q1 = p[Partial<T, NB>::block_index(tile, S, s, u.w, b, 2 * u.tp + 1, u.tm) + lane];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[b][r] += q0[r];
+        v[b][4 + r] += q1[r];
+      }
+    }
   }
 }
 
-// Split-K arrival: all waves' partial stores complete, then one lane bumps the
-// tile's counter (acq_rel, agent scope).  Returns true in every thread of the
-// work-group that arrived last; that work-group then owns the reduction.
-// The counter advances by S per run and is never reset: the last arriver is
-// the one whose previous value is epoch * S + S - 1 (unsigned, wrap-safe).
-__device__ __forceinline__ bool arrive_last(uint32_t* cnt, uint32_t epoch, int S, int* s_flag) {
+// Release-increment of a counter after every wave's stores are complete
+// (used for split-K arrivals and for the producer's ready signal).
+__device__ __forceinline__ void release_add(uint32_t* cnt) {
   wait_all_mem();
   __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    *s_flag = (old - epoch * (uint32_t)S) == (uint32_t)(S - 1);
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wait until *cnt has reached `target` (wrap-safe), then acquire at agent
+// scope.  Wave 0 polls and sleeps between polls; after spin_limit polls it
+// gives up and latches CTRL_ERROR.  A barrier carries the outcome (through
+// *s_slot) and the ordering to every wave.  Returns false on a timeout or if
+// an earlier wait of this run already timed out.
+__device__ __forceinline__ bool wait_count(const uint32_t* cnt, uint32_t target, uint32_t spin_limit, uint32_t* err,
+                                           int* s_slot) {
+  if (uniform((int)(threadIdx.x >> 6)) == 0) {
+    bool ok = false;
+    if (uniform(ld_relaxed(err)) == 0u) {
+      // scalar loop: every exit condition is wave-uniform
+      for (uint32_t polls = 0;; ++polls) {
+        ok = (int32_t)(uniform(ld_relaxed(cnt)) - target) >= 0;
+        if (ok || polls >= spin_limit) break;
+        __builtin_amdgcn_s_sleep(2);
+      }
+      if (!ok && (threadIdx.x & 63) == 0) __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (ok) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if ((threadIdx.x & 63) == 0) *s_slot = ok;
   }
   __syncthreads();
-  const bool last = uniform(*s_flag) != 0;
-  __syncthreads();  // s_flag may be rewritten by the next arrival
-  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  return last;
+  const bool ok = uniform(*s_slot) != 0;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  __syncthreads();  // *s_slot may be rewritten by the next wait
+  return ok;
 }
 
 // ------------------------------------------------------------------ ready flags
 
-// Producer side: every wave's Z stores are complete, then one lane performs
-// an agent-scope release increment of the tile's ready counter.
-__device__ __forceinline__ void signal_ready(uint32_t* flag) {
-  wait_all_mem();
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(flag, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
+// Producer side (Sec. III-A: the producer fences its output, then signals):
+// every wave's Z stores are complete, then one lane performs an agent-scope
+// release increment of the tile's ready counter.
+__device__ __forceinline__ void signal_ready(uint32_t* flag) { release_add(flag); }
 
-// Consumer side: before loading Z columns [k, k + kBK) of row block mb, wait
-// until the GEMM1 tile (mb, k / bn1) has signalled in this run, i.e. until its
-// counter reaches epoch + 1 (compared wrap-safe).  Each wave polls for itself
-// (uniform address, one request per poll), sleeps between polls, gives up after
-// spin_limit polls (latching CTRL_ERROR), then performs an agent-scope acquire.
+// Consumer side: before loading Z columns [k, k + kBK) of row block mb, the
+// GEMM1 tile (mb, k / bn1) must have signalled every time it does in a run
+// (once per split-K part), i.e. its counter must have reached
+// (epoch + 1) * S1 (compared wrap-safe).
+//
+// Wave 0 reads up to 64 consecutive counters of the item's K range in one
+// vector load and takes the longest ready prefix (a ballot), so that one
+// agent-scope acquire covers every K-slice that is already available; an
+// acquire invalidates the L2 of the XCD, so it is issued once per newly ready
+// prefix, not once per slice and wave.  Between polls the wave sleeps; after
+// spin_limit polls it gives up, latches CTRL_ERROR and stops waiting for the
+// rest of the run.  The result reaches the other waves through LDS and a
+// work-group barrier.  Every call is made by all waves with the same k.
 struct ReadyWait {
   const uint32_t* ready;
   uint32_t* err;  // CTRL_ERROR word
   int mb, Mb, bn1;
+  int kb_last;    // last column block of this item's K range
   uint32_t target;
   uint32_t spin_limit;
-  int known;  // highest column block already acquired by this wave
+  int* s_known;   // LDS broadcast slot
+  int known;      // highest column block acquired by this work-group (uniform)
   __device__ __forceinline__ void operator()(int k) {
     const int kb = k / bn1;
     if (kb <= known) return;
-    const uint32_t* f = ready + (long)kb * Mb + mb;
-    // Once any wait of this run has given up, no wave waits again: the run
-    // finishes promptly and the error is reported by the host.
-    if ((int32_t)(uniform(ld_relaxed(f)) - target) < 0 && uniform(ld_relaxed(err)) == 0u) {
-      for (uint32_t polls = 0;; ++polls) {
-        if (polls >= spin_limit) {
-          if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          known = 0x7fffffff;
-          return;
+    if (uniform((int)(threadIdx.x >> 6)) == 0) {  // wave 0, as a scalar branch
+      const int lane = threadIdx.x & 63;
+      const int j = kb + lane;
+      const uint32_t* f = ready + (long)(j <= kb_last ? j : kb_last) * Mb + mb;
+      int hi = -1;
+      if (uniform(ld_relaxed(err)) == 0u) {
+        // scalar loop: every exit condition is wave-uniform
+        uint64_t m = 0;
+        for (uint32_t polls = 0;; ++polls) {
+          const uint32_t v = ld_relaxed(f);  // every lane loads (address clamped in range)
+          m = __builtin_amdgcn_ballot_w64((j <= kb_last) & ((int32_t)(v - target) >= 0));
+          if ((m & 1u) || polls >= spin_limit) break;
+          __builtin_amdgcn_s_sleep(2);
         }
-        __builtin_amdgcn_s_sleep(2);
-        if ((int32_t)(uniform(ld_relaxed(f)) - target) >= 0) break;
+        if (m & 1u)
+          hi = kb + (int)__builtin_ctzll(~m) - 1;
+        else if (lane == 0)
+          __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
+      if (hi >= 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      if (lane == 0) *s_known = hi >= 0 ? hi : 0x7fffffff;
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    known = kb;
+    __syncthreads();
+    known = uniform(*s_known);
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    // Every wave has read *s_known before wave 0 may write it again: the
+    // pipeline prologue calls this back to back, with no other barrier between.
+    __syncthreads();
   }
 };
 

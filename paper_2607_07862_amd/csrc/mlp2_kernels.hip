@@ -22,12 +22,55 @@
 
 namespace mlp2 {
 
-// ------------------------------------------------------------------ work items
+// ------------------------------------------------------------------ epilogues
 
+// GEMM1 epilogue for one lane: activation in fp32 on the 8 consecutive values
+// of row `row` from column `col`, round to bf16, one 16-byte store into Z.
+template <int NB>
+__device__ __forceinline__ void store_z(const Args& a, long row, int col, const float (&v)[NB][8]) {
+  float z[8];
+  if constexpr (NB == 2) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[i] = silu(v[0][i]) * v[1][i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[i] = v[0][i];
+    if (a.act == ACT_GELU_TANH) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) z[i] = gelu_tanh(z[i]);
+    }
+  }
+  *reinterpret_cast<u32x4*>(a.Z + row * a.F + col) = pack_bf16x8(z);
+}
+
+__device__ __forceinline__ void store_y(const Args& a, int row, int col, const float (&v)[8]) {
+  if (row < a.M) *reinterpret_cast<u32x4*>(a.Y + (long)row * a.H + col) = pack_bf16x8(v);
+}
+
+// Claims the next ticket early: thread 0 issues the atomic and parks the value
+// in *s_next; it is read after the item's closing barrier.  Called once per
+// item, after the item's last wait, so that an item never holds a claim it
+// might itself be waiting for.
+__device__ __forceinline__ void claim_next(const Args& a, int* s_next) {
+  if (threadIdx.x == 0)
+    *s_next = (int)__hip_atomic_fetch_add(a.ctrl + CTRL_TICKET, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ------------------------------------------------------------------ work items
+//
+// Split-K epilogue, shared by both GEMMs: each part stores its partial and
+// release-increments the tile's arrival counter, waits until all S parts have
+// arrived, then sums (in the fixed order s = 0..S-1) and finishes its own
+// share of the tile's units: units [s*U/S, (s+1)*U/S), one unit per wave at a
+// time.  Every part therefore reads about one tile's worth of partials, and
+// the tile's reduction runs on S work-groups at once.
+
+// GEMM1 item id = tile * S1 + s, tile = nb * Mb + mb.
 template <class T, int NB>
-__device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t epoch, uint16_t* lds, int* s_flag) {
+__device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t epoch, char* lds, int* s_slot,
+                                           int* s_next) {
   const int id = uniform(id_in);
-  const int tile = id / a.S1, s = id - (id / a.S1) * a.S1;
+  const int tile = id / a.S1, s = id - tile * a.S1;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
   const int m0 = mb * T::BM, n0 = nb * T::BN;
   const int kbeg = s * a.kc1;
@@ -40,54 +83,45 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
   NoWait nowait;
   mainloop<T, NB>(a.X, a.H, m0, a.M - 1, Bp, a.F, n0, kbeg, kend, acc, lds, nowait);
 
-  if (a.S1 > 1) {
-    store_partial<T, NB>(a.part1, tile, a.S1, s, acc);
-    const bool last = arrive_last(a.cnt1 + tile, epoch, a.S1, s_flag);
-    if (!last) return;  // uniform; no barrier follows in this item
-    reduce_partials<T, NB>(a.part1, tile, a.S1, acc);
-  }
-
-  // Fused epilogue: activation in fp32, round to bf16, 16-byte stores of Z.
-  FragPos<T> fp(m0, n0);
+  if (a.S1 == 1) {
+    claim_next(a, s_next);
+    FragPos<T> fp(m0, n0);
 #pragma unroll
-  for (int tm = 0; tm < T::TM; ++tm) {
+    for (int tm = 0; tm < T::TM; ++tm)
 #pragma unroll
-    for (int tp = 0; tp < T::TN / 2; ++tp) {
-      float v[8];
-      if constexpr (NB == 2) {
-        float gt[8], up[8];
-        pair_values<T>(acc[0], tp, tm, gt);
-        pair_values<T>(acc[1], tp, tm, up);
+      for (int tp = 0; tp < T::TN / 2; ++tp) {
+        float v[NB][8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = silu(gt[i]) * up[i];
-      } else {
-        pair_values<T>(acc[0], tp, tm, v);
-        if (a.act == ACT_GELU_TANH) {
-#pragma unroll
-          for (int i = 0; i < 8; ++i) v[i] = gelu_tanh(v[i]);
-        }
+        for (int b = 0; b < NB; ++b) pair_values<T>(acc[b], tp, tm, v[b]);
+        store_z<NB>(a, fp.row0 + 16 * tm, fp.col0 + 32 * tp, v);
       }
-      const long row = fp.row0 + 16 * tm;
-      const int col = fp.col0 + 32 * tp;
-      *reinterpret_cast<u32x4*>(a.Z + row * a.F + col) = pack_bf16x8(v);
+  } else {
+    store_partial<T, NB>(a.part1, tile, a.S1, s, acc);
+    release_add(a.cnt1 + tile);
+    wait_count(a.cnt1 + tile, (epoch + 1u) * (uint32_t)a.S1, a.spin_limit, a.ctrl + CTRL_ERROR, s_slot);
+    claim_next(a, s_next);
+    constexpr int U = Partial<T, NB>::UNITS;
+    const int u0 = s * U / a.S1, u1 = (s + 1) * U / a.S1;
+    const int lane = threadIdx.x & 63;
+    for (int ui = u0 + uniform((int)(threadIdx.x >> 6)); ui < u1; ui += 4) {
+      const Unit<T> u(ui);
+      float v[NB][8];
+      reduce_unit<T, NB>(a.part1, tile, a.S1, u, lane, v);
+      store_z<NB>(a, u.row(m0, lane), u.col(n0, lane), v);
     }
   }
-  // Producer signal: Z tile complete and released, then ready[tile] += 1.
-  if (tile != a.drop_signal) {
-    signal_ready(a.ready + tile);
-  } else {
-    wait_all_mem();
-    __syncthreads();
-  }
+  // Producer signal (one per part and run): Z rows of this part released, ready[tile] += 1.
+  if (!(tile == a.drop_signal && s == 0)) signal_ready(a.ready + tile);
 }
 
-// GEMM2 item p: split s = p / tiles2 (lower splits first: they read the
-// column blocks of Z that complete first), tile = p % tiles2.
+// GEMM2 item p = tile * S2 + s (the parts of a tile are adjacent tickets,
+// see the kernels' deadlock argument).  WAIT: each K-slice of Z is consumed
+// only after its GEMM1 tile has signalled.
 template <class T, bool WAIT>
-__device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epoch, uint16_t* lds, int* s_flag) {
+__device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epoch, char* lds, int* s_slot,
+                                           int* s_next) {
   const int p = uniform(p_in);
-  const int tiles2 = a.Mb * a.Nb2;
-  const int s = p / tiles2, tile = p - s * tiles2;
+  const int tile = p / a.S2, s = p - (p / a.S2) * a.S2;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
   const int m0 = mb * T::BM, n0 = nb * T::BN;
   const int kbeg = s * a.kc2;
@@ -97,151 +131,185 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
   const uint16_t* Bp[1] = {a.W2};
   const int zlast = a.Mb * T::BM - 1;
   if constexpr (WAIT) {
-    ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, epoch + 1u, a.spin_limit, -1};
+    ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1,
+                (epoch + 1u) * (uint32_t)a.S1, a.spin_limit, s_slot, -1};
     mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, w);
   } else {
     NoWait nowait;
     mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, nowait);
   }
 
-  if (a.S2 > 1) {
-    store_partial<T, 1>(a.part2, tile, a.S2, s, acc);
-    const bool last = arrive_last(a.cnt2 + tile, epoch, a.S2, s_flag);
-    if (!last) return;  // uniform; no barrier follows in this item
-    reduce_partials<T, 1>(a.part2, tile, a.S2, acc);
-  }
-
-  FragPos<T> fp(m0, n0);
+  if (a.S2 == 1) {
+    claim_next(a, s_next);
+    FragPos<T> fp(m0, n0);
 #pragma unroll
-  for (int tm = 0; tm < T::TM; ++tm) {
-    const int row = fp.row0 + 16 * tm;
-    if (row < a.M) {
+    for (int tm = 0; tm < T::TM; ++tm)
 #pragma unroll
       for (int tp = 0; tp < T::TN / 2; ++tp) {
         float v[8];
         pair_values<T>(acc[0], tp, tm, v);
-        *reinterpret_cast<u32x4*>(a.Y + (long)row * a.H + fp.col0 + 32 * tp) = pack_bf16x8(v);
+        store_y(a, fp.row0 + 16 * tm, fp.col0 + 32 * tp, v);
       }
+  } else {
+    store_partial<T, 1>(a.part2, tile, a.S2, s, acc);
+    release_add(a.cnt2 + tile);
+    wait_count(a.cnt2 + tile, (epoch + 1u) * (uint32_t)a.S2, a.spin_limit, a.ctrl + CTRL_ERROR, s_slot);
+    claim_next(a, s_next);
+    constexpr int U = Partial<T, 1>::UNITS;
+    const int u0 = s * U / a.S2, u1 = (s + 1) * U / a.S2;
+    const int lane = threadIdx.x & 63;
+    for (int ui = u0 + uniform((int)(threadIdx.x >> 6)); ui < u1; ui += 4) {
+      const Unit<T> u(ui);
+      float v[1][8];
+      reduce_unit<T, 1>(a.part2, tile, a.S2, u, lane, v);
+      store_y(a, u.row(m0, lane), u.col(n0, lane), v[0]);
     }
   }
 }
 
-// The last work-group of a run's final kernel resets the ticket and the done
-// count and advances the epoch (all stream-ordered before the next run).
-__device__ __forceinline__ void finish_run(const Args& a, uint32_t epoch) {
+// The last work-group of a kernel resets the ticket and the done count; the
+// run's final kernel also advances the epoch (all stream-ordered before the
+// next kernel of the plan).
+__device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, bool end_of_run) {
   __syncthreads();
   if (threadIdx.x == 0) {
     const uint32_t old = __hip_atomic_fetch_add(a.ctrl + CTRL_DONE, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     if (old == gridDim.x - 1) {
       __hip_atomic_store(a.ctrl + CTRL_TICKET, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(a.ctrl + CTRL_DONE, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(a.ctrl + CTRL_EPOCH, epoch + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      if (end_of_run) __hip_atomic_store(a.ctrl + CTRL_EPOCH, epoch + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
 
 // ------------------------------------------------------------------ kernels
+//
+// Every kernel is persistent: a work-group takes tickets from CTRL_TICKET
+// until the kernel's item list is exhausted.  Item lists (in ticket order):
+//   PHASE_GEMM1:     GEMM1 items in the order table's order
+//   PHASE_GEMM2:     GEMM2 items
+//   PHASE_PIPELINED: both lists back to back; GEMM2 items wait per K-slice.
+// Waits: a split-K part waits for its sibling parts (adjacent tickets: the
+// parts of a tile are consecutive in every item list), a GEMM2 item for GEMM1
+// tiles (earlier tickets).  A work-group claims its next ticket only after the
+// last wait of its current item.  Let q be the first unclaimed ticket: every
+// tile whose parts all lie below q is held by work-groups that will finish it
+// (GEMM1 tiles first, then GEMM2 tiles, whose waits on GEMM1 therefore end);
+// only the tile containing q can have parts waiting for unclaimed siblings, at
+// most S - 1 of them.  So with a grid of at least max(S1, S2) work-groups some
+// work-group always gets to claim q: no launch deadlocks, whatever the
+// residency.  The host enforces that grid bound.
+
+enum { PHASE_GEMM1 = 0, PHASE_GEMM2 = 1, PHASE_PIPELINED = 2 };
 
 template <int A, int B>
 struct MaxI {
   static constexpr int value = A > B ? A : B;
 };
 
-template <class T1, int NB, class T2>
-__global__ __launch_bounds__(kThreads) void k_gemm1(Args a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[T1::template lds_elems<NB>()];
-  __shared__ int s_flag;
-  const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
-  gemm1_item<T1, NB>(a, (int)a.order1[blockIdx.x], epoch, lds, &s_flag);
+template <class T1, int NB, class T2, int PHASE>
+constexpr int kernel_lds() {
+  return PHASE == PHASE_GEMM1   ? T1::template lds_bytes<NB>()
+         : PHASE == PHASE_GEMM2 ? T2::template lds_bytes<1>()
+                                : MaxI<T1::template lds_bytes<NB>(), T2::template lds_bytes<1>()>::value;
 }
 
-template <class T1, int NB, class T2>
-__global__ __launch_bounds__(kThreads) void k_gemm2(Args a) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[T2::template lds_elems<1>()];
-  __shared__ int s_flag;
-  const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
-  gemm2_item<T2, false>(a, blockIdx.x, epoch, lds, &s_flag);
-  finish_run(a, epoch);
+// Work-groups per CU the register budget must allow: two whenever two rings fit in LDS.
+template <class T1, int NB, class T2, int PHASE>
+constexpr int min_blocks() {
+  return kernel_lds<T1, NB, T2, PHASE>() <= 80 * 1024 ? 2 : 1;
 }
 
-template <class T1, int NB, class T2>
-__global__ __launch_bounds__(kThreads) void k_pipelined(Args a) {
-  constexpr int kLds = MaxI<T1::template lds_elems<NB>(), T2::template lds_elems<1>()>::value;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[kLds];
-  __shared__ int s_item, s_flag;
+template <class T1, int NB, class T2, int PHASE>
+__global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, PHASE>())) void k_mlp2(Args a) {
+  constexpr int kLds = kernel_lds<T1, NB, T2, PHASE>();
+  __shared__ __attribute__((aligned(1024))) char lds[kLds];
+  __shared__ int s_item, s_slot;
   const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
-  const int total = a.items1 + a.items2;
+  const int g1 = PHASE == PHASE_GEMM2 ? 0 : a.items1;
+  const int g2 = PHASE == PHASE_GEMM1 ? 0 : a.items2;
+  const int total = g1 + g2;
+  claim_next(a, &s_item);
   for (;;) {
-    if (threadIdx.x == 0)
-      s_item = (int)__hip_atomic_fetch_add(a.ctrl + CTRL_TICKET, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    const int p = uniform(s_item);
-    __syncthreads();  // s_item is rewritten at the next ticket
+    int p = uniform(s_item);
+    __syncthreads();  // s_item is rewritten by the item's claim_next
     if (p >= total) break;
-    if (p < a.items1)
-      gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_flag);
+    if (p < g1)
+      gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_slot, &s_item);
     else
-      gemm2_item<T2, true>(a, p - a.items1, epoch, lds, &s_flag);
-    __syncthreads();  // the item's last LDS reads complete before the next item's writes
+      gemm2_item<T2, PHASE == PHASE_PIPELINED>(a, p - g1, epoch, lds, &s_slot, &s_item);
   }
-  finish_run(a, epoch);
+  finish_kernel(a, epoch, PHASE != PHASE_GEMM1);
 }
 
 // ------------------------------------------------------------------ dispatch table
 
-template <int BM, int BN>
+// Tile shapes by (rows, columns, ring depth).
+template <int BM, int BN, int NS>
 struct TileFor;
-template <> struct TileFor<32, 64> { using type = Tile<32, 64, 2, 2>; };
-template <> struct TileFor<32, 128> { using type = Tile<32, 128, 1, 4>; };
-template <> struct TileFor<64, 64> { using type = Tile<64, 64, 2, 2>; };
-template <> struct TileFor<64, 128> { using type = Tile<64, 128, 2, 2>; };
-template <> struct TileFor<128, 64> { using type = Tile<128, 64, 2, 2>; };
-template <> struct TileFor<128, 128> { using type = Tile<128, 128, 2, 2>; };
+template <int NS> struct TileFor<32, 64, NS> { using type = Tile<32, 64, 2, 2, NS>; };
+template <int NS> struct TileFor<32, 128, NS> { using type = Tile<32, 128, 1, 4, NS>; };
+template <int NS> struct TileFor<64, 64, NS> { using type = Tile<64, 64, 2, 2, NS>; };
+template <int NS> struct TileFor<64, 128, NS> { using type = Tile<64, 128, 2, 2, NS>; };
+template <int NS> struct TileFor<128, 64, NS> { using type = Tile<128, 64, 2, 2, NS>; };
+template <int NS> struct TileFor<128, 128, NS> { using type = Tile<128, 128, 2, 2, NS>; };
+template <int NS> struct TileFor<128, 256, NS> { using type = Tile<128, 256, 2, 2, NS>; };
+template <int NS> struct TileFor<64, 256, NS> { using type = Tile<64, 256, 1, 4, NS>; };
+template <int NS> struct TileFor<32, 256, NS> { using type = Tile<32, 256, 1, 4, NS>; };
 
 struct Entry {
-  int bm, bn1, bn2, nb;
+  int bm, bn1, bn2, nb, ns;
   const void* seq1;
   const void* seq2;
   const void* pipe;
 };
 
-#define MLP2_ENTRY(BM, BN1, BN2, NB)                                                                    \
-  Entry {                                                                                               \
-    BM, BN1, BN2, NB,                                                                                   \
-        (const void*)&k_gemm1<typename TileFor<BM, BN1>::type, NB, typename TileFor<BM, BN2>::type>,    \
-        (const void*)&k_gemm2<typename TileFor<BM, BN1>::type, NB, typename TileFor<BM, BN2>::type>,    \
-        (const void*)&k_pipelined<typename TileFor<BM, BN1>::type, NB, typename TileFor<BM, BN2>::type> \
+#define MLP2_K(BM, BN1, BN2, NB, NS, PH) \
+  (const void*)&k_mlp2<typename TileFor<BM, BN1, NS>::type, NB, typename TileFor<BM, BN2, NS>::type, PH>
+#define MLP2_ENTRY(BM, BN1, BN2, NB, NS)                                                             \
+  Entry {                                                                                           \
+    BM, BN1, BN2, NB, NS, MLP2_K(BM, BN1, BN2, NB, NS, PHASE_GEMM1),                               \
+        MLP2_K(BM, BN1, BN2, NB, NS, PHASE_GEMM2),                                                  \
+        MLP2_K(BM, BN1, BN2, NB, NS, PHASE_PIPELINED)                                               \
   }
 
 static const Entry kEntries[] = {
-    MLP2_ENTRY(32, 128, 128, 1), MLP2_ENTRY(32, 128, 64, 1), MLP2_ENTRY(32, 64, 128, 1), MLP2_ENTRY(32, 64, 64, 1),
-    MLP2_ENTRY(64, 128, 128, 1), MLP2_ENTRY(64, 128, 64, 1), MLP2_ENTRY(64, 64, 128, 1), MLP2_ENTRY(64, 64, 64, 1),
-    MLP2_ENTRY(128, 128, 128, 1), MLP2_ENTRY(128, 128, 64, 1), MLP2_ENTRY(128, 64, 128, 1), MLP2_ENTRY(128, 64, 64, 1),
-    MLP2_ENTRY(32, 64, 128, 2), MLP2_ENTRY(32, 64, 64, 2), MLP2_ENTRY(64, 64, 128, 2), MLP2_ENTRY(64, 64, 64, 2),
-    MLP2_ENTRY(128, 64, 128, 2), MLP2_ENTRY(128, 64, 64, 2),
+    MLP2_ENTRY(32, 128, 128, 1, 4), MLP2_ENTRY(32, 128, 64, 1, 4), MLP2_ENTRY(32, 64, 128, 1, 4), MLP2_ENTRY(32, 64, 64, 1, 4),
+    MLP2_ENTRY(64, 128, 128, 1, 4), MLP2_ENTRY(64, 128, 64, 1, 4), MLP2_ENTRY(64, 64, 128, 1, 4), MLP2_ENTRY(64, 64, 64, 1, 4),
+    MLP2_ENTRY(128, 128, 128, 1, 4), MLP2_ENTRY(128, 128, 64, 1, 4), MLP2_ENTRY(128, 64, 128, 1, 4), MLP2_ENTRY(128, 64, 64, 1, 4),
+    MLP2_ENTRY(32, 64, 128, 2, 4), MLP2_ENTRY(32, 64, 64, 2, 4), MLP2_ENTRY(64, 64, 128, 2, 4), MLP2_ENTRY(64, 64, 64, 2, 4),
+    MLP2_ENTRY(128, 64, 128, 2, 4), MLP2_ENTRY(128, 64, 64, 2, 4),
+    // shallower rings: two work-groups per CU
+    MLP2_ENTRY(128, 128, 128, 1, 2), MLP2_ENTRY(128, 128, 128, 1, 3), MLP2_ENTRY(128, 64, 64, 1, 3),
+    MLP2_ENTRY(64, 128, 128, 1, 3), MLP2_ENTRY(128, 64, 128, 2, 2), MLP2_ENTRY(32, 128, 128, 1, 3),
+    // wide weight tiles: half the activation traffic per weight byte
+    MLP2_ENTRY(128, 256, 256, 1, 3), MLP2_ENTRY(128, 256, 128, 1, 3), MLP2_ENTRY(128, 128, 256, 1, 3),
+    MLP2_ENTRY(128, 256, 256, 1, 2), MLP2_ENTRY(32, 256, 256, 1, 4), MLP2_ENTRY(64, 256, 256, 1, 3),
 };
 
 static const Entry* find_entry(const KernelConfig& c) {
   for (const Entry& e : kEntries)
-    if (e.bm == c.bm && e.bn1 == c.bn1 && e.bn2 == c.bn2 && e.nb == c.nb) return &e;
+    if (e.bm == c.bm && e.bn1 == c.bn1 && e.bn2 == c.bn2 && e.nb == c.nb && e.ns == c.ns) return &e;
   return nullptr;
 }
 
 bool config_supported(const KernelConfig& c) { return find_entry(c) != nullptr; }
 
-hipError_t pipelined_occupancy(const KernelConfig& c, int* blocks_per_cu) {
+hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu) {
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, e->pipe, kThreads, 0);
+  const void* k = which == 0 ? e->seq1 : which == 1 ? e->seq2 : e->pipe;
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, kThreads, 0);
 }
 
-hipError_t launch_sequential(const KernelConfig& c, const Args& a, hipStream_t stream) {
+hipError_t launch_sequential(const KernelConfig& c, const Args& a, const int grids[2], hipStream_t stream) {
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
   void* args[] = {const_cast<Args*>(&a)};
-  hipError_t err = hipLaunchKernel(e->seq1, dim3(a.items1), dim3(kThreads), args, 0, stream);
+  hipError_t err = hipLaunchKernel(e->seq1, dim3(grids[0]), dim3(kThreads), args, 0, stream);
   if (err != hipSuccess) return err;
-  return hipLaunchKernel(e->seq2, dim3(a.items2), dim3(kThreads), args, 0, stream);
+  return hipLaunchKernel(e->seq2, dim3(grids[1]), dim3(kThreads), args, 0, stream);
 }
 
 hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipStream_t stream) {

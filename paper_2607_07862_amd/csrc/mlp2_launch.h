@@ -7,15 +7,16 @@
 
 namespace mlp2 {
 
-// A compiled kernel family: row block, GEMM1 / GEMM2 column-block widths and
-// the number of GEMM1 weight operands (2 for SwiGLU).
+// A compiled kernel family: row block, GEMM1 / GEMM2 column-block widths, the
+// number of GEMM1 weight operands (2 for SwiGLU) and the LDS ring depth.
 struct KernelConfig {
-  int bm, bn1, bn2, nb;
+  int bm, bn1, bn2, nb, ns;
 };
 
 bool config_supported(const KernelConfig& c);
-hipError_t pipelined_occupancy(const KernelConfig& c, int* blocks_per_cu);
-hipError_t launch_sequential(const KernelConfig& c, const Args& a, hipStream_t stream);
+// Resident work-groups per CU of a kernel: which = 0 (GEMM1 phase), 1 (GEMM2 phase), 2 (pipelined).
+hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu);
+hipError_t launch_sequential(const KernelConfig& c, const Args& a, const int grids[2], hipStream_t stream);
 hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
 
 }  // namespace mlp2

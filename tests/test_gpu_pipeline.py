@@ -23,7 +23,7 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("order", [B.ORDER_ROW_FIRST, B.ORDER_REVERSED, B.ORDER_SHUFFLED, B.ORDER_COLUMN_FIRST])
-@pytest.mark.parametrize("grid", [1, 3, 17, 0])
+@pytest.mark.parametrize("grid", [3, 4, 17, 0])
 def test_orders_and_grids_match_sequential_bits(lib, order, grid):
     M, H, F, act = 160, 256, 768, 1
     d = I.make_inputs(M, H, F, act, seed=40 + order)
@@ -113,5 +113,33 @@ def test_run_argument_errors(lib):
         plan.run(g["X"], g["W1"], g["W2"], torch.empty(M, H + 1, dtype=torch.bfloat16, device="cuda"), 0)
     info = plan.info()
     assert info["items1"] == info["row_blocks"] * info["col_blocks1"] * info["splitk1"]
+    # split-K parts wait for their siblings: a grid below max(S1, S2) is refused
+    smax = max(info["splitk1"], info["splitk2"])
+    if smax > 1:
+        with pytest.raises(B.Mlp2Error):
+            plan.set_option(B.OPT_GRID, smax - 1)
+    plan.set_option(B.OPT_GRID, 0)
     assert info["grid_pipelined"] >= 1 and info["occupancy"] >= 1
+    plan.close()
+
+
+@pytest.mark.parametrize("order", [B.ORDER_REVERSED, B.ORDER_SHUFFLED, B.ORDER_COLUMN_FIRST])
+def test_consecutive_slice_waits_stay_in_step(lib, order):
+    """bn1 = 64 makes every 64-deep stage of GEMM2 a new column block of Z, so
+    the pipeline prologue waits several times in a row; with a reversed or
+    shuffled GEMM1 order those waits see short ready prefixes.  Every run must
+    give the sequential mode's bits."""
+    M, H, F, act = 256, 1024, 4096, 2
+    d = I.make_inputs(M, H, F, act, seed=80 + order)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, {"bm": 128, "bn1": 64, "bn2": 128, "splitk2": 2})
+    Ys = run(plan, g, B.MODE_SEQUENTIAL).clone()
+    plan.set_option(B.OPT_ORDER, order)
+    outs = [run(plan, g, B.MODE_TILE_PIPELINED) for _ in range(20)]
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    for n, y in enumerate(outs):
+        assert_bit_equal(Ys, y, f"run {n}")
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
+    assert_matches_oracle(Ys, ref, "sequential")
     plan.close()

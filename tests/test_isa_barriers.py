@@ -35,42 +35,139 @@ def asm(tmp_path_factory):
 
 def kernels(text):
     out = {}
-    for m in re.finditer(r"^(_Z\w*k_(?:gemm1|gemm2|pipelined)\w*):", text, re.M):
+    for m in re.finditer(r"^(_Z\w*k_mlp2\w*):", text, re.M):
         body = text[m.end():]
-        end = body.find("s_endpgm")
+        end = body.find(".Lfunc_end")
         out[m.group(1)] = body[:end]
     return out
 
 
-def violations(body):
-    bad = []
-    stack = []
-    seen_labels = set()
-    for ln, line in enumerate(body.splitlines()):
-        s = line.split(";")[0].strip()
-        if not s:
+def loop_headers(body):
+    """Labels the compiler annotates as loop headers."""
+    heads = set()
+    lines = body.splitlines()
+    for i, line in enumerate(lines):
+        m = re.match(r"^(\.LBB\w+):", line)
+        if m and any("Loop Header" in l for l in lines[i : i + 4]):
+            heads.add(m.group(1))
+    return heads
+
+
+def parse_blocks(body):
+    """Basic blocks of a kernel: list of (label, [instructions]) in layout order."""
+    blocks = [["<entry>", []]]
+    for line in body.splitlines():
+        code = line.split(";")[0].strip()
+        if not code:
             continue
-        if re.match(r"^\.LBB\w+:$", s):
-            seen_labels.add(s[:-1])
-            continue
-        m = re.match(r"s_(?:and|or)_saveexec_b64\s+(s\[\d+:\d+\])", s)
+        m = re.match(r"^(\.LBB\w+):$", code)
         if m:
-            stack.append(m.group(1))
+            blocks.append([m.group(1), []])
             continue
-        m = re.match(r"s_or_b64\s+exec,\s*exec,\s*(s\[\d+:\d+\])", s)
-        if m and m.group(1) in stack:
-            del stack[len(stack) - 1 - stack[::-1].index(m.group(1)):]
+        if code.startswith(".") or code.startswith("#"):
             continue
-        if s.startswith("s_barrier") and stack:
-            bad.append(f"line {ln}: s_barrier inside exec region(s) {stack}")
-        # a loop continued through the exec mask: a backward exec-conditional branch,
-        # or lanes retired from exec inside a loop
-        m = re.match(r"s_cbranch_exec(?:nz|z)\s+(\.LBB\w+)", s)
-        if m and m.group(1) in seen_labels:
-            bad.append(f"line {ln}: backward exec-masked branch '{s}'")
-        if re.match(r"s_andn2_b64\s+exec,\s*exec", s):
-            bad.append(f"line {ln}: lanes retired from exec '{s}'")
+        blocks[-1][1].append(code)
+        if re.match(r"s_(c?branch|endpgm)", code):
+            blocks.append([f"<after{len(blocks)}>", []])
+    return [(l, ins) for l, ins in blocks if ins or l.startswith(".LBB")]
+
+
+def successors(blocks, i):
+    ins = blocks[i][1]
+    last = ins[-1] if ins else ""
+    nxt = [i + 1] if i + 1 < len(blocks) else []
+    index = {l: j for j, (l, _) in enumerate(blocks)}
+    m = re.match(r"s_branch\s+(\.LBB\w+)", last)
+    if m:
+        return [index[m.group(1)]]
+    m = re.match(r"s_cbranch_\w+\s+(\.LBB\w+)", last)
+    if m:
+        return [index[m.group(1)]] + nxt
+    if last.startswith("s_endpgm"):
+        return []
+    return nxt
+
+
+def violations(body):
+    """Barriers reached with an open exec-masked region, found by dataflow over the CFG.
+
+    State: the stack of SGPR pairs saved by s_and_saveexec / s_or_saveexec that
+    have not yet been restored by s_or_b64 exec, exec, <pair>.
+    """
+    blocks = parse_blocks(body)
+    heads = loop_headers(body)
+    bad = []
+    entry = {0: ((), ())}
+    work = [0]
+    seen_state = {}
+    while work:
+        i = work.pop()
+        state = list(entry[i][0])
+        alias = dict(entry[i][1])  # complement masks from s_xor, mapped to their region
+
+        def region_of(reg):
+            return alias.get(reg, reg)
+
+        for ins in blocks[i][1]:
+            # else entry: s_or_saveexec / s_andn2_saveexec on a region's own mask
+            m = re.match(r"s_(?:or|andn2)_saveexec_b64\s+(s\[\d+:\d+\]),\s*(s\[\d+:\d+\])", ins)
+            if m and region_of(m.group(2)) in state:
+                r = region_of(m.group(2))
+                del state[len(state) - 1 - state[::-1].index(r):]
+                state.append(m.group(1))
+                continue
+            m = re.match(r"s_(?:and|or)_saveexec_b64\s+(s\[\d+:\d+\])", ins)
+            if m:
+                state.append(m.group(1))
+                continue
+            m = re.match(r"s_xor_b64\s+(s\[\d+:\d+\]),\s*(?:exec,\s*(s\[\d+:\d+\])|(s\[\d+:\d+\]),\s*exec)", ins)
+            if m:
+                src = m.group(2) or m.group(3)
+                if region_of(src) in state:
+                    alias[m.group(1)] = region_of(src)
+                continue
+            m = re.match(r"s_or_b64\s+exec,\s*exec,\s*(s\[\d+:\d+\])", ins)
+            if m and region_of(m.group(1)) in state:
+                r = region_of(m.group(1))
+                del state[len(state) - 1 - state[::-1].index(r):]
+                continue
+            if ins.startswith("s_barrier") and state:
+                bad.append(f"{blocks[i][0]}: s_barrier inside exec region(s) {state}")
+            m = re.match(r"s_cbranch_exec(?:nz|z)\s+(\.LBB\w+)", ins)
+            if m and m.group(1) in heads:
+                bad.append(f"{blocks[i][0]}: exec-masked loop back-edge '{ins}'")
+            if re.match(r"s_andn2_b64\s+exec,\s*exec", ins):
+                bad.append(f"{blocks[i][0]}: lanes retired from exec '{ins}'")
+        out = (tuple(state), tuple(sorted(alias.items())))
+        for j in successors(blocks, i):
+            if j in entry:
+                if entry[j][0] != out[0] and (j, out[0]) not in seen_state:
+                    seen_state[(j, out[0])] = True
+                    bad.append(f"{blocks[j][0]}: reached with exec regions {entry[j][0]} and {out[0]}")
+                continue
+            entry[j] = out
+            work.append(j)
+    return sorted(set(bad))
+
+
+def m0_misuse(body):
+    """M0 is written only to address a direct-to-LDS load, immediately before it."""
+    bad = []
+    lines = [l.split(";")[0].strip() for l in body.splitlines()]
+    lines = [l for l in lines if l and not l.startswith(".") and not l.startswith("#")]
+    for i, s in enumerate(lines):
+        if re.match(r"s_\w+\s+m0\b", s):
+            nxt = lines[i + 1] if i + 1 < len(lines) else ""
+            if not nxt.startswith("global_load_lds"):
+                bad.append(f"m0 written by '{s}' not followed by a direct-to-LDS load")
+        if re.search(r"\bm0\b", s) and not re.match(r"s_mov_b32\s+m0,", s):
+            bad.append(f"m0 used by '{s}'")
     return bad
+
+
+def test_m0_only_feeds_direct_to_lds_loads(asm):
+    problems = {n: m0_misuse(b)[:3] for n, b in kernels(asm).items() if m0_misuse(b)}
+    assert not problems, problems
 
 
 def test_every_kernel_keeps_barriers_in_uniform_control_flow(asm):
