@@ -162,6 +162,23 @@ const void* mlp2_intermediate(mlp2_plan_t plan);
 enum mlp2_option { MLP2_OPT_SPIN_LIMIT = 1, MLP2_OPT_DROP_SIGNAL = 2, MLP2_OPT_ORDER = 3, MLP2_OPT_GRID = 4 };
 int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
 
+/* Per-item timing trace (diagnostics).  Only a library built with the
+ * MLP2_TRACE macro records; an ordinary build returns MLP2_ERR_UNSUPPORTED
+ * and its kernels carry no trace code.  `buffer` is caller-owned device
+ * memory (8-byte aligned, NULL detaches) that later runs of the plan fill:
+ * for section s (0 = the GEMM1 kernel or the pipelined kernel, 1 = the GEMM2
+ * kernel of the sequential mode) and work-group g of that launch, the block
+ * at uint64 offset (s * G + g) * (1 + 6 * records_per_group) holds the
+ * item count, then one record per item of 6 uint64: ticket, start, mainloop
+ * end, end (100 MHz device real-time counter), ticks waiting for the tile
+ * loads of the work-group's own ring, ticks waiting for ready counters and
+ * split-K siblings.  Items beyond records_per_group are counted, not stored.
+ * G is the largest of the plan's grids (grid_pipelined, grid_gemm1,
+ * grid_gemm2 of mlp2_plan_info); the buffer must hold
+ * 2 * G * (1 + 6 * records_per_group) words.  Returns MLP2_OK, MLP2_ERR_INVALID_ARG
+ * or MLP2_ERR_UNSUPPORTED. */
+int mlp2_trace_attach(mlp2_plan_t plan, void* buffer, int records_per_group);
+
 #ifdef __cplusplus
 }
 #endif

@@ -11,6 +11,7 @@ import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libmlp2.so")
+TRACE_LIB_PATH = os.path.join(PKG, "libmlp2_trace.so")
 
 ACT_IDENTITY, ACT_GELU_TANH, ACT_SWIGLU = 0, 1, 2
 DTYPE_BF16 = 0
@@ -34,6 +35,7 @@ EXPORTS = (
     "mlp2_plan_info",
     "mlp2_intermediate",
     "mlp2_set_option",
+    "mlp2_trace_attach",
 )
 
 
@@ -90,11 +92,17 @@ class Mlp2Error(RuntimeError):
 _lib = None
 
 
-def load(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load the compiled library (raises if it was not built)."""
+def load(path: str | None = None) -> ctypes.CDLL:
+    """Load the compiled library (raises if it was not built).
+
+    ``MLP2_TRACE=1`` in the environment selects the timing-trace build
+    ``libmlp2_trace.so`` (``python -m paper_2607_07862_amd.build --trace``).
+    """
     global _lib
     if _lib is not None:
         return _lib
+    if path is None:
+        path = TRACE_LIB_PATH if os.environ.get("MLP2_TRACE") == "1" else LIB_PATH
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with `python -m paper_2607_07862_amd.build`")
     lib = ctypes.CDLL(path)
@@ -119,6 +127,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mlp2_intermediate.argtypes = [P]
     lib.mlp2_set_option.restype = ctypes.c_int
     lib.mlp2_set_option.argtypes = [P, ctypes.c_int, ctypes.c_int64]
+    lib.mlp2_trace_attach.restype = ctypes.c_int
+    lib.mlp2_trace_attach.argtypes = [P, P, ctypes.c_int]
     _lib = lib
     return lib
 
@@ -210,6 +220,12 @@ class Plan:
         rc = self.lib.mlp2_set_option(self.handle, int(key), int(value))
         if rc != OK:
             raise Mlp2Error(rc, "mlp2_set_option")
+
+    def attach_trace(self, buffer, records_per_group: int) -> None:
+        """Attach a device uint64/int64 tensor as the timing-trace buffer (trace builds only)."""
+        rc = self.lib.mlp2_trace_attach(self.handle, _ptr(buffer), int(records_per_group))
+        if rc != OK:
+            raise Mlp2Error(rc, "mlp2_trace_attach")
 
     def intermediate_ptr(self) -> int:
         return int(self.lib.mlp2_intermediate(self.handle) or 0)

@@ -22,21 +22,23 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, trace: bool = False) -> str:
+    """Compile the library; ``trace=True`` builds ``libmlp2_trace.so`` with per-item timing records."""
     objs = []
-    build_dir = os.path.join(PKG, "_build")
+    build_dir = os.path.join(PKG, "_build_trace" if trace else "_build")
+    lib_path = os.path.join(PKG, "libmlp2_trace.so") if trace else LIB_PATH
     os.makedirs(build_dir, exist_ok=True)
     common = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
-              "-I" + os.path.join(ROOT, "include"), "-I" + CSRC] + DEVICE_FLAGS
+              "-I" + os.path.join(ROOT, "include"), "-I" + CSRC] + DEVICE_FLAGS + (["-DMLP2_TRACE"] if trace else [])
     for src in SOURCES:
         obj = os.path.join(build_dir, src + ".o")
         cmd = common + (["-x", "hip"] if src.endswith(".cpp") else []) + ["-c", os.path.join(CSRC, src), "-o", obj]
         _run(cmd, verbose)
         objs.append(obj)
-    tmp = LIB_PATH + ".tmp"
+    tmp = lib_path + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs, verbose)
-    os.replace(tmp, LIB_PATH)
-    return LIB_PATH
+    os.replace(tmp, lib_path)
+    return lib_path
 
 
 def _run(cmd, verbose):
@@ -51,4 +53,4 @@ def _run(cmd, verbose):
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, trace="--trace" in sys.argv))

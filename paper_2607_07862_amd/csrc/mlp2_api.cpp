@@ -34,6 +34,8 @@ struct mlp2_plan_s {
   int order = MLP2_ORDER_COLUMN_FIRST;
   uint32_t spin_limit = 1u << 20;
   int drop_signal = -1;
+  uint64_t* trace = nullptr;  // caller-owned timing buffer (trace builds)
+  int trace_cap = 0;
   // workspace
   void* ws = nullptr;
   size_t ws_bytes = 0;
@@ -313,10 +315,13 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   a.bn1 = p->kc.bn1;
   a.spin_limit = p->spin_limit;
   a.drop_signal = p->drop_signal;
+  a.trace = p->trace;
+  a.trace_cap = p->trace_cap;
 
   hipStream_t s = (hipStream_t)stream;
   const int go = p->grid_override;
   const int grids[2] = {go ? go : p->grid1, go ? go : p->grid2};
+  a.trace_groups = std::max(std::max(grids[0], grids[1]), go ? go : p->grid);
   hipError_t err = mode == MLP2_MODE_SEQUENTIAL ? mlp2::launch_sequential(p->kc, a, grids, s)
                                                 : mlp2::launch_pipelined(p->kc, a, go ? go : p->grid, s);
   if (err != hipSuccess) return fail(MLP2_ERR_HIP);
@@ -402,6 +407,14 @@ int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
     default:
       return fail(MLP2_ERR_INVALID_ARG);
   }
+}
+
+int mlp2_trace_attach(mlp2_plan_t p, void* buffer, int records_per_group) {
+  if (!p || (buffer && records_per_group < 1) || ((uintptr_t)buffer & 7u)) return fail(MLP2_ERR_INVALID_ARG);
+  if (!mlp2::kTrace) return fail(MLP2_ERR_UNSUPPORTED);
+  p->trace = (uint64_t*)buffer;
+  p->trace_cap = buffer ? records_per_group : 0;
+  return MLP2_OK;
 }
 
 }  // extern "C"

@@ -57,7 +57,33 @@ struct Args {
   int bn1;                 // GEMM1 column-block width (ready-counter granularity along GEMM2's K)
   uint32_t spin_limit;
   int drop_signal;         // GEMM1 tile whose signal is skipped (failure injection), -1 = none
+  uint64_t* trace;         // per-work-group timing records (trace builds only), or null
+  int trace_cap;           // records per work-group
+  int trace_groups;        // work-groups per trace section (the largest grid of the plan)
 };
+
+// ------------------------------------------------------------------ optional timing trace
+//
+// Built with -DMLP2_TRACE, thread 0 of every work-group records per item:
+// {ticket, start, mainloop end, end, ring-wait ticks, flag-wait ticks} on the
+// 100 MHz real-time counter.  Ring waits are the mainloop's waits for its own
+// loads plus the stage barrier; flag waits are ready-counter and sibling waits.
+// Without the macro every hook compiles to nothing.
+#ifdef MLP2_TRACE
+constexpr bool kTrace = true;
+#else
+constexpr bool kTrace = false;
+#endif
+constexpr int kTraceWords = 6;
+
+struct TraceAcc {
+  uint64_t ring = 0, flag = 0, t_main = 0;
+};
+
+__device__ __forceinline__ uint64_t trace_now() {
+  if constexpr (kTrace) return __builtin_amdgcn_s_memrealtime();
+  return 0;
+}
 
 // ------------------------------------------------------------------ scalars
 
@@ -186,7 +212,7 @@ struct NoWait {
 template <class T, int NB, class Wait>
 __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long lda, int m0, int mlast,
                                          const uint16_t* const (&Bp)[NB], long ldb, int n0, int kbeg, int kend,
-                                         f32x4 (&acc)[NB][T::TN][T::TM], char* lds, Wait& wait) {
+                                         f32x4 (&acc)[NB][T::TN][T::TM], char* lds, Wait& wait, TraceAcc& tr) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
@@ -294,6 +320,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     if (st < nk) issue(st);
 
   for (int it = 0; it < nk; ++it) {
+    const uint64_t t0 = trace_now();
     // Own loads of stage `it` complete: the stages issued after it may stay in flight.
     const int after = min(T::NS - 2, nk - 1 - it);
     if constexpr (T::NS >= 4) {
@@ -307,6 +334,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
       wait_vm<0>();
     }
     __syncthreads();
+    if constexpr (kTrace) tr.ring += trace_now() - t0;
     if (it + T::NS - 1 < nk) issue(it + T::NS - 1);
     compute(it);
   }
@@ -447,7 +475,8 @@ __device__ __forceinline__ void release_add(uint32_t* cnt) {
 // *s_slot) and the ordering to every wave.  Returns false on a timeout or if
 // an earlier wait of this run already timed out.
 __device__ __forceinline__ bool wait_count(const uint32_t* cnt, uint32_t target, uint32_t spin_limit, uint32_t* err,
-                                           int* s_slot) {
+                                           int* s_slot, TraceAcc& tr) {
+  const uint64_t t0 = trace_now();
   if (uniform((int)(threadIdx.x >> 6)) == 0) {
     bool ok = false;
     if (uniform(ld_relaxed(err)) == 0u) {
@@ -466,6 +495,7 @@ __device__ __forceinline__ bool wait_count(const uint32_t* cnt, uint32_t target,
   const bool ok = uniform(*s_slot) != 0;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
   __syncthreads();  // *s_slot may be rewritten by the next wait
+  if constexpr (kTrace) tr.flag += trace_now() - t0;
   return ok;
 }
 
@@ -498,9 +528,11 @@ struct ReadyWait {
   uint32_t spin_limit;
   int* s_known;   // LDS broadcast slot
   int known;      // highest column block acquired by this work-group (uniform)
+  TraceAcc* tr;
   __device__ __forceinline__ void operator()(int k) {
     const int kb = k / bn1;
     if (kb <= known) return;
+    const uint64_t t0 = trace_now();
     if (uniform((int)(threadIdx.x >> 6)) == 0) {  // wave 0, as a scalar branch
       const int lane = threadIdx.x & 63;
       const int j = kb + lane;
@@ -529,6 +561,7 @@ struct ReadyWait {
     // Every wave has read *s_known before wave 0 may write it again: the
     // pipeline prologue calls this back to back, with no other barrier between.
     __syncthreads();
+    if constexpr (kTrace) tr->flag += trace_now() - t0;
   }
 };
 

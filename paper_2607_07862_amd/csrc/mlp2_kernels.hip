@@ -56,6 +56,31 @@ __device__ __forceinline__ void claim_next(const Args& a, int* s_next) {
     *s_next = (int)__hip_atomic_fetch_add(a.ctrl + CTRL_TICKET, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ------------------------------------------------------------------ trace records (MLP2_TRACE builds)
+
+// Layout of the trace buffer: per kernel section (0 = GEMM1 or pipelined
+// kernel, 1 = GEMM2 kernel of the sequential mode; trace_groups work-groups
+// per section) and work-group, one word
+// with the item count, then trace_cap records of kTraceWords words: ticket,
+// start, mainloop end, end, ring-wait ticks, flag-wait ticks.  Records past
+// trace_cap are counted, not stored.  Written by thread 0 with plain stores.
+__device__ __forceinline__ void tr_mark_mainloop(TraceAcc& tr) { tr.t_main = trace_now(); }
+
+__device__ __forceinline__ void tr_record(const Args& a, int section, int n, int ticket, uint64_t t_start,
+                                          const TraceAcc& tr) {
+  if (a.trace == nullptr || threadIdx.x != 0) return;
+  uint64_t* slot = a.trace + ((long)section * a.trace_groups + blockIdx.x) * (1 + (long)a.trace_cap * kTraceWords);
+  slot[0] = (uint64_t)(n + 1);
+  if (n >= a.trace_cap) return;
+  uint64_t* r = slot + 1 + (long)n * kTraceWords;
+  r[0] = (uint64_t)ticket;
+  r[1] = t_start;
+  r[2] = tr.t_main;
+  r[3] = trace_now();
+  r[4] = tr.ring;
+  r[5] = tr.flag;
+}
+
 // ------------------------------------------------------------------ work items
 //
 // Split-K epilogue, shared by both GEMMs: each part stores its partial and
@@ -68,7 +93,7 @@ __device__ __forceinline__ void claim_next(const Args& a, int* s_next) {
 // GEMM1 item id = tile * S1 + s, tile = nb * Mb + mb.
 template <class T, int NB>
 __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t epoch, char* lds, int* s_slot,
-                                           int* s_next) {
+                                           int* s_next, TraceAcc& tr) {
   const int id = uniform(id_in);
   const int tile = id / a.S1, s = id - tile * a.S1;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
@@ -81,7 +106,8 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
   Bp[0] = a.W1;
   if constexpr (NB == 2) Bp[1] = a.W1 + (long)a.H * a.F;
   NoWait nowait;
-  mainloop<T, NB>(a.X, a.H, m0, a.M - 1, Bp, a.F, n0, kbeg, kend, acc, lds, nowait);
+  mainloop<T, NB>(a.X, a.H, m0, a.M - 1, Bp, a.F, n0, kbeg, kend, acc, lds, nowait, tr);
+  if constexpr (kTrace) tr_mark_mainloop(tr);
 
   if (a.S1 == 1) {
     claim_next(a, s_next);
@@ -98,7 +124,7 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
   } else {
     store_partial<T, NB>(a.part1, tile, a.S1, s, acc);
     release_add(a.cnt1 + tile);
-    wait_count(a.cnt1 + tile, (epoch + 1u) * (uint32_t)a.S1, a.spin_limit, a.ctrl + CTRL_ERROR, s_slot);
+    wait_count(a.cnt1 + tile, (epoch + 1u) * (uint32_t)a.S1, a.spin_limit, a.ctrl + CTRL_ERROR, s_slot, tr);
     claim_next(a, s_next);
     constexpr int U = Partial<T, NB>::UNITS;
     const int u0 = s * U / a.S1, u1 = (s + 1) * U / a.S1;
@@ -119,7 +145,7 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
 // only after its GEMM1 tile has signalled.
 template <class T, bool WAIT>
 __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epoch, char* lds, int* s_slot,
-                                           int* s_next) {
+                                           int* s_next, TraceAcc& tr) {
   const int p = uniform(p_in);
   const int tile = p / a.S2, s = p - (p / a.S2) * a.S2;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
@@ -132,12 +158,13 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
   const int zlast = a.Mb * T::BM - 1;
   if constexpr (WAIT) {
     ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1,
-                (epoch + 1u) * (uint32_t)a.S1, a.spin_limit, s_slot, -1};
-    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, w);
+                (epoch + 1u) * (uint32_t)a.S1, a.spin_limit, s_slot, -1, &tr};
+    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, w, tr);
   } else {
     NoWait nowait;
-    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, nowait);
+    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, nowait, tr);
   }
+  if constexpr (kTrace) tr_mark_mainloop(tr);
 
   if (a.S2 == 1) {
     claim_next(a, s_next);
@@ -153,7 +180,7 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
   } else {
     store_partial<T, 1>(a.part2, tile, a.S2, s, acc);
     release_add(a.cnt2 + tile);
-    wait_count(a.cnt2 + tile, (epoch + 1u) * (uint32_t)a.S2, a.spin_limit, a.ctrl + CTRL_ERROR, s_slot);
+    wait_count(a.cnt2 + tile, (epoch + 1u) * (uint32_t)a.S2, a.spin_limit, a.ctrl + CTRL_ERROR, s_slot, tr);
     claim_next(a, s_next);
     constexpr int U = Partial<T, 1>::UNITS;
     const int u0 = s * U / a.S2, u1 = (s + 1) * U / a.S2;
@@ -230,15 +257,19 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, PHASE>())) void k
   const int g2 = PHASE == PHASE_GEMM1 ? 0 : a.items2;
   const int total = g1 + g2;
   claim_next(a, &s_item);
+  int n_items = 0;
   for (;;) {
     __syncthreads();
     int p = uniform(s_item);
     __syncthreads();  // s_item is rewritten by the item's claim_next
     if (p >= total) break;
+    TraceAcc tr;
+    const uint64_t t_start = trace_now();
     if (p < g1)
-      gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_slot, &s_item);
+      gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_slot, &s_item, tr);
     else
-      gemm2_item<T2, PHASE == PHASE_PIPELINED>(a, p - g1, epoch, lds, &s_slot, &s_item);
+      gemm2_item<T2, PHASE == PHASE_PIPELINED>(a, p - g1, epoch, lds, &s_slot, &s_item, tr);
+    if constexpr (kTrace) tr_record(a, PHASE == PHASE_GEMM2 ? 1 : 0, n_items++, p, t_start, tr);
   }
   finish_kernel(a, epoch, PHASE != PHASE_GEMM1);
 }
