@@ -83,7 +83,8 @@ typedef struct mlp2_tuning {
   int splitk1;   /* GEMM1 split-K factor (>= 1)                                           */
   int bn2;       /* GEMM2 column-block width: 64 or 128                                   */
   int splitk2;   /* GEMM2 split-K factor (>= 1)                                           */
-  int grid;      /* persistent grid of every launch (>= max(splitk1, splitk2))            */
+  int grid;      /* persistent grid of every launch (no more work-groups than fit the
+                    device at once)                                                      */
   int order;     /* enum mlp2_order                                                       */
   int stages;    /* LDS ring depth of the tile mainloop (2, 3 or 4)                       */
   int reserved[6];
@@ -155,9 +156,8 @@ const void* mlp2_intermediate(mlp2_plan_t plan);
  *   MLP2_OPT_SPIN_LIMIT   polls before a flag wait gives up (default ~1 s of polling)
  *   MLP2_OPT_DROP_SIGNAL  GEMM1 tile index whose ready signal is skipped (-1 = none)
  *   MLP2_OPT_ORDER        enum mlp2_order (rebuilds the order table)
- *   MLP2_OPT_GRID         persistent grid of every launch (0 = automatic; else at
- *                         least max(splitk1, splitk2), since split-K parts wait
- *                         for their siblings)
+ *   MLP2_OPT_GRID         persistent grid of every launch (0 = automatic; else
+ *                         at most the work-groups that fit the device at once)
  * Returns MLP2_OK or MLP2_ERR_INVALID_ARG. */
 enum mlp2_option { MLP2_OPT_SPIN_LIMIT = 1, MLP2_OPT_DROP_SIGNAL = 2, MLP2_OPT_ORDER = 3, MLP2_OPT_GRID = 4 };
 int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
@@ -168,14 +168,15 @@ int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
  * memory (8-byte aligned, NULL detaches) that later runs of the plan fill:
  * for section s (0 = the GEMM1 kernel or the pipelined kernel, 1 = the GEMM2
  * kernel of the sequential mode) and work-group g of that launch, the block
- * at uint64 offset (s * G + g) * (1 + 6 * records_per_group) holds the
- * item count, then one record per item of 6 uint64: ticket, start, mainloop
- * end, end (100 MHz device real-time counter), ticks waiting for the tile
- * loads of the work-group's own ring, ticks waiting for ready counters and
- * split-K siblings.  Items beyond records_per_group are counted, not stored.
+ * at uint64 offset (s * G + g) * (1 + 8 * records_per_group) holds the
+ * item count, then one record per item of 8 uint64: item rank, start,
+ * mainloop end, split-K arrival released, split-K siblings arrived (0 and 0
+ * for an item without split-K), end (times on the 100 MHz device real-time
+ * counter), ticks waiting for the tile loads of the work-group's own ring,
+ * ticks waiting for ready counters and split-K siblings.  Items beyond records_per_group are counted, not stored.
  * G is the largest of the plan's grids (grid_pipelined, grid_gemm1,
  * grid_gemm2 of mlp2_plan_info); the buffer must hold
- * 2 * G * (1 + 6 * records_per_group) words.  Returns MLP2_OK, MLP2_ERR_INVALID_ARG
+ * 2 * G * (1 + 8 * records_per_group) words.  Returns MLP2_OK, MLP2_ERR_INVALID_ARG
  * or MLP2_ERR_UNSUPPORTED. */
 int mlp2_trace_attach(mlp2_plan_t plan, void* buffer, int records_per_group);
 

@@ -31,6 +31,7 @@ struct mlp2_plan_s {
   int items1 = 0, items2 = 0;
   int grid = 0, grid1 = 0, grid2 = 0, occupancy = 0, num_cus = 0;
   int grid_override = 0;
+  int max_grid = 0;  // work-groups of every kernel of the plan that fit the device at once
   int order = MLP2_ORDER_COLUMN_FIRST;
   uint32_t spin_limit = 1u << 20;
   int drop_signal = -1;
@@ -63,11 +64,15 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
-// Split K into S ranges of kc (a multiple of the stage depth) so that the
-// tile count times S reaches `want` items, keeping every range at least
-// `min_k` deep.  Returns S and sets *kc.
+// Claim lists of a launch: one per XCD (8), or one per work-group for grids
+// below 8, so that every list has a work-group.
+int claim_lists(int grid) { return std::min(8, std::max(1, grid)); }
+
+// Split K into S ranges of kc (a multiple of the stage depth): as many parts
+// as keep the tile count times S within `want` items (one round of the
+// persistent grid), each range at least `min_k` deep.  Returns S and sets *kc.
 int choose_split(int64_t K, int tiles, int want, int min_k, int* kc) {
-  int S = std::max(1, ceil_div(want, tiles));
+  int S = std::max(1, want / std::max(1, tiles));
   S = std::min<int64_t>(S, std::max<int64_t>(1, K / min_k));
   int64_t k = align_up((size_t)ceil_div(K, S), mlp2::kBK);
   *kc = (int)k;
@@ -171,45 +176,39 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   p->M = M; p->H = H; p->F = F; p->act = act; p->device = dev;
   p->num_cus = prop.multiProcessorCount;
 
-  // ---- tile choice: rows per block by regime, widest column blocks that divide
-  int bm = tz.bm ? tz.bm : (M <= 32 ? 32 : M <= 64 ? 64 : 128);
-  int bn1 = tz.bn1 ? tz.bn1 : ((nb == 1 && F % 128 == 0) ? 128 : 64);
-  int bn2 = tz.bn2 ? tz.bn2 : (H % 128 == 0 ? 128 : 64);
-  const int ns = tz.stages ? tz.stages : 4;
-  p->kc = KernelConfig{bm, bn1, bn2, nb, ns};
-  if (F % bn1 || H % bn2 || !mlp2::config_supported(p->kc)) {
+  // ---- tile choice by regime.  Up to 256 rows (weight streaming): one row
+  // block holds every row, so each weight byte is read once; 128-wide weight
+  // tiles except at 128 rows, where the activation tile is the larger operand
+  // and 64-wide tiles give enough items with little or no split-K.  Beyond
+  // 256 rows (MFMA-bound): 128 x 128 tiles, two work-groups per CU.
+  const bool big = M > 256;
+  const int bm0 = M <= 32 ? 32 : M <= 64 ? 64 : M <= 128 ? 128 : M <= 256 ? 256 : 128;
+  const int wide = (bm0 != 128 || big) ? 128 : 64;
+  const int pref[4] = {bm0, nb == 1 ? wide : 64, bm0 == 128 && !big ? 64 : 128, big ? 2 : bm0 == 256 ? 3 : 4};
+  // Fallbacks when the preferred tiles do not divide F / H or are not built.
+  const int cand[][4] = {
+      {pref[0], pref[1], pref[2], pref[3]}, {pref[0], pref[1], 64, pref[3]}, {pref[0], 64, 64, pref[3]},
+      {pref[0], pref[1], pref[2], 4},       {pref[0], pref[1], 64, 4},       {pref[0], 64, 64, 4},
+      {128, 64, 64, 4},                     {64, 64, 64, 4},                 {32, 64, 64, 4},
+  };
+  bool found = false;
+  for (const auto& c : cand) {
+    KernelConfig k{tz.bm ? tz.bm : c[0], tz.bn1 ? tz.bn1 : c[1], tz.bn2 ? tz.bn2 : c[2], nb, tz.stages ? tz.stages : c[3]};
+    if (F % k.bn1 == 0 && H % k.bn2 == 0 && mlp2::config_supported(k)) {
+      p->kc = k;
+      found = true;
+      break;
+    }
+  }
+  if (!found) {
     delete p;
     fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
   }
+  const int bm = p->kc.bm, bn1 = p->kc.bn1, bn2 = p->kc.bn2;
   p->Mb = ceil_div(M, bm);
   p->Nb1 = (int)(F / bn1);
   p->Nb2 = (int)(H / bn2);
-  const int tiles1 = p->Mb * p->Nb1, tiles2 = p->Mb * p->Nb2;
-  const int want = p->num_cus;  // enough items to give every CU one
-  if (tz.splitk1) {
-    p->kc1 = (int)align_up((size_t)ceil_div(H, tz.splitk1), mlp2::kBK);
-    p->S1 = ceil_div(H, p->kc1);
-  } else {
-    p->S1 = choose_split(H, tiles1, want, 256, &p->kc1);
-  }
-  if (tz.splitk2) {
-    p->kc2 = (int)align_up((size_t)ceil_div(F, tz.splitk2), mlp2::kBK);
-    p->S2 = ceil_div(F, p->kc2);
-  } else {
-    p->S2 = choose_split(F, tiles2, want, 256, &p->kc2);
-  }
-  p->order = tz.order;
-  p->items1 = tiles1 * p->S1;
-  p->items2 = tiles2 * p->S2;
-  // split-K parts wait for their siblings: every launch needs >= max(S1, S2) work-groups
-  const int min_grid = std::max(p->S1, p->S2);
-  if (tz.grid && tz.grid < min_grid) {
-    delete p;
-    fail(MLP2_ERR_UNSUPPORTED);
-    return nullptr;
-  }
-
   int occ[3] = {0, 0, 0};
   for (int w = 0; w < 3; ++w) {
     if (mlp2::occupancy(p->kc, w, &occ[w]) != hipSuccess || occ[w] < 1) {
@@ -218,11 +217,34 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
       return nullptr;
     }
   }
+  const int tiles1 = p->Mb * p->Nb1, tiles2 = p->Mb * p->Nb2;
+  if (tz.splitk1) {
+    p->kc1 = (int)align_up((size_t)ceil_div(H, tz.splitk1), mlp2::kBK);
+    p->S1 = ceil_div(H, p->kc1);
+  } else {
+    p->S1 = choose_split(H, tiles1, occ[0] * p->num_cus, 256, &p->kc1);
+  }
+  if (tz.splitk2) {
+    p->kc2 = (int)align_up((size_t)ceil_div(F, tz.splitk2), mlp2::kBK);
+    p->S2 = ceil_div(F, p->kc2);
+  } else {
+    p->S2 = choose_split(F, tiles2, occ[1] * p->num_cus, 256, &p->kc2);
+  }
+  p->order = tz.order;
+  p->items1 = tiles1 * p->S1;
+  p->items2 = tiles2 * p->S2;
+
   p->occupancy = occ[2];
+  p->max_grid = std::min(std::min(occ[0], occ[1]), occ[2]) * p->num_cus;
+  if (tz.grid > p->max_grid) {
+    delete p;
+    fail(MLP2_ERR_UNSUPPORTED);
+    return nullptr;
+  }
   p->grid_override = tz.grid;
-  p->grid1 = std::max(min_grid, std::min(occ[0] * p->num_cus, p->items1));
-  p->grid2 = std::max(min_grid, std::min(occ[1] * p->num_cus, p->items2));
-  p->grid = std::max(min_grid, std::min(occ[2] * p->num_cus, p->items1 + p->items2));
+  p->grid1 = std::min(occ[0] * p->num_cus, p->items1);
+  p->grid2 = std::min(occ[1] * p->num_cus, p->items2);
+  p->grid = std::min(occ[2] * p->num_cus, p->items1 + p->items2);
 
   // ---- workspace: Z, partials, counters, order table
   const int64_t Mpad = (int64_t)p->Mb * bm;
@@ -321,9 +343,18 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   hipStream_t s = (hipStream_t)stream;
   const int go = p->grid_override;
   const int grids[2] = {go ? go : p->grid1, go ? go : p->grid2};
-  a.trace_groups = std::max(std::max(grids[0], grids[1]), go ? go : p->grid);
-  hipError_t err = mode == MLP2_MODE_SEQUENTIAL ? mlp2::launch_sequential(p->kc, a, grids, s)
-                                                : mlp2::launch_pipelined(p->kc, a, go ? go : p->grid, s);
+  const int gridp = go ? go : p->grid;
+  a.trace_groups = std::max(std::max(grids[0], grids[1]), gridp);
+  hipError_t err;
+  if (mode == MLP2_MODE_SEQUENTIAL) {
+    a.lists = claim_lists(grids[0]);
+    Args a2 = a;
+    a2.lists = claim_lists(grids[1]);
+    err = mlp2::launch_sequential(p->kc, a, a2, grids, s);
+  } else {
+    a.lists = claim_lists(gridp);
+    err = mlp2::launch_pipelined(p->kc, a, gridp, s);
+  }
   if (err != hipSuccess) return fail(MLP2_ERR_HIP);
   return MLP2_OK;
 }
@@ -399,8 +430,8 @@ int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
       if (hipDeviceSynchronize() != hipSuccess || upload_order(p) != MLP2_OK) return fail(MLP2_ERR_HIP);
       return MLP2_OK;
     case MLP2_OPT_GRID:
-      // 0 = automatic; otherwise at least one work-group per split-K part of a tile
-      if (value < 0 || value > (1 << 20) || (value > 0 && value < std::max(p->S1, p->S2)))
+      // 0 = automatic; otherwise 1 .. the work-groups that fit the device at once
+      if (value < 0 || value > p->max_grid)
         return fail(MLP2_ERR_INVALID_ARG);
       p->grid_override = (int)value;
       return MLP2_OK;

@@ -28,9 +28,9 @@ constexpr int kBK = 64;        // K depth of one LDS stage
 // Control words of a plan (device memory, zero at plan creation).
 enum {
   CTRL_EPOCH = 0,   // runs completed; read at kernel start, bumped by the run's last work-group
-  CTRL_TICKET = 1,  // next work item of the pipelined launch
-  CTRL_DONE = 2,    // work-groups of the run's final kernel that have finished
+  CTRL_DONE = 2,    // work-groups of the current kernel that have finished
   CTRL_ERROR = 3,   // nonzero once a bounded flag wait gave up
+  CTRL_TICKET = 8,  // CTRL_TICKET + l: next ticket of claim list l (up to 8 lists)
   CTRL_WORDS = 16
 };
 
@@ -60,13 +60,14 @@ struct Args {
   uint64_t* trace;         // per-work-group timing records (trace builds only), or null
   int trace_cap;           // records per work-group
   int trace_groups;        // work-groups per trace section (the largest grid of the plan)
+  int lists;               // claim lists of the launch (1 or 8; work-group g claims from list g % lists)
 };
 
 // ------------------------------------------------------------------ optional timing trace
 //
 // Built with -DMLP2_TRACE, thread 0 of every work-group records per item:
-// {ticket, start, mainloop end, end, ring-wait ticks, flag-wait ticks} on the
-// 100 MHz real-time counter.  Ring waits are the mainloop's waits for its own
+// {rank, start, mainloop end, split-K arrival released, siblings arrived, end,
+// ring-wait ticks, flag-wait ticks} on the 100 MHz real-time counter.  Ring waits are the mainloop's waits for its own
 // loads plus the stage barrier; flag waits are ready-counter and sibling waits.
 // Without the macro every hook compiles to nothing.
 #ifdef MLP2_TRACE
@@ -74,10 +75,10 @@ constexpr bool kTrace = true;
 #else
 constexpr bool kTrace = false;
 #endif
-constexpr int kTraceWords = 6;
+constexpr int kTraceWords = 8;
 
 struct TraceAcc {
-  uint64_t ring = 0, flag = 0, t_main = 0;
+  uint64_t ring = 0, flag = 0, t_main = 0, t_rel = 0, t_wait = 0;
 };
 
 __device__ __forceinline__ uint64_t trace_now() {
@@ -371,11 +372,13 @@ __device__ __forceinline__ void pair_values(const f32x4 (&a)[T::TN][T::TM], int 
 // work items.  Each part stores its fp32 accumulators "fragment-native": lane
 // l of wave w writes its f32x4 of block i at ((tile*S + s)*PER_ITEM +
 // (w*PER_WAVE + i)*64 + l), so writes and reads are fully coalesced 1 KB runs.
-// The reduction is spread over the S parts themselves, in "units" (a wave's
-// pair of adjacent 16x16 blocks in one row block, for every weight operand):
-// once all S parts have arrived each part adds up its share of the units in
-// the fixed order s = 0, 1, ..., S-1 and runs their epilogue.  The order of
-// the adds never depends on which part finished last.
+// Each part then counts its arrival on the tile's counter; the part that
+// arrives last (it reads the count just below the run's target) adds up the
+// tile in "units" (a wave's pair of adjacent 16x16 blocks in one row block,
+// for every weight operand) in the fixed order s = 0, 1, ..., S-1 and runs the
+// tile's epilogue; the other parts go straight on to their next item.  No part
+// ever waits for a sibling, and the order of the adds never depends on which
+// part finished last, so every run and mode gives the same bits.
 
 template <class T, int NB>
 struct Partial {
@@ -404,6 +407,7 @@ __device__ __forceinline__ void store_partial(float* base, long tile, int S, int
 template <class T>
 struct Unit {
   int w, tm, tp;
+  __device__ Unit() = default;
   __device__ explicit Unit(int u) {
     constexpr int per_wave = T::TM * (T::TN / 2);
     w = u / per_wave;
@@ -416,47 +420,47 @@ struct Unit {
   __device__ int col(int n0, int lane) const { return n0 + (w / T::WM) * T::NW + 32 * tp + 8 * (lane >> 4); }
 };
 
-// v[b][0..7] = sum over s = 0 .. S-1 (in that order) of the unit's 8 values for
-// weight operand b, as held by `lane` (the same layout pair_values produces).
-template <class T, int NB>
-__device__ __forceinline__ void reduce_unit(const float* base, long tile, int S, const Unit<T>& u, int lane,
-                                            float (&v)[NB][8]) {
+// v[g][b][0..7] = sum over s = 0 .. S-1 (in that order) of the 8 values of
+// unit ug[g] for weight operand b, as held by `lane` (the layout pair_values
+// produces).  G units at a time and R parts per round keep 2*G*NB*R loads of
+// one wave in flight together; slots past the last part load part S - 1
+// again (in bounds) and are not added.
+template <class T, int NB, int G>
+__device__ __forceinline__ void reduce_units(const float* base, long tile, int S, const Unit<T> (&ug)[G], int lane,
+                                             float (&v)[G][NB][8]) {
   const f32x4* p = reinterpret_cast<const f32x4*>(base);
 #pragma unroll
-  for (int b = 0; b < NB; ++b)
+  for (int g = 0; g < G; ++g)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) v[b][i] = 0.f;
-  int s = 0;
-  // two parts per round: their loads are in flight together
-  for (; s + 2 <= S; s += 2) {
-    f32x4 q[2][NB][2];
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+      for (int i = 0; i < 8; ++i) v[g][b][i] = 0.f;
+  constexpr int R = 8;
+  for (int s = 0; s < S; s += R) {
+    f32x4 q[R][G][NB][2];
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
+    for (int h = 0; h < R; ++h) {
+      const int sh = min(s + h, S - 1);
 #pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2)
-          q[h][b][t2] = p[Partial<T, NB>::block_index(tile, S, s + h, u.w, b, 2 * u.tp + t2, u.tm) + lane];
+      for (int g = 0; g < G; ++g)
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
+          for (int t2 = 0; t2 < 2; ++t2)
+            q[h][g][b][t2] = p[Partial<T, NB>::block_index(tile, S, sh, ug[g].w, b, 2 * ug[g].tp + t2, ug[g].tm) + lane];
+    }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          v[b][r] += q[h][b][0][r];
-          v[b][4 + r] += q[h][b][1][r];
-        }
-  }
-  if (s < S) {
+    for (int h = 0; h < R; ++h) {
+      if (s + h >= S) break;  // uniform
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const f32x4 q0 = p[Partial<T, NB>::block_index(tile, S, s, u.w, b, 2 * u.tp, u.tm) + lane];
-      const f32x4 q1 = p[Partial<T, NB>::block_index(tile, S, s, u.w, b, 2 * u.tp + 1, u.tm) + lane];
+      for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        v[b][r] += q0[r];
-        v[b][4 + r] += q1[r];
-      }
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            v[g][b][r] += q[h][g][b][0][r];
+            v[g][b][4 + r] += q[h][g][b][1][r];
+          }
     }
   }
 }
@@ -469,34 +473,27 @@ __device__ __forceinline__ void release_add(uint32_t* cnt) {
   if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Wait until *cnt has reached `target` (wrap-safe), then acquire at agent
-// scope.  Wave 0 polls and sleeps between polls; after spin_limit polls it
-// gives up and latches CTRL_ERROR.  A barrier carries the outcome (through
-// *s_slot) and the ordering to every wave.  Returns false on a timeout or if
-// an earlier wait of this run already timed out.
-__device__ __forceinline__ bool wait_count(const uint32_t* cnt, uint32_t target, uint32_t spin_limit, uint32_t* err,
-                                           int* s_slot, TraceAcc& tr) {
-  const uint64_t t0 = trace_now();
-  if (uniform((int)(threadIdx.x >> 6)) == 0) {
-    bool ok = false;
-    if (uniform(ld_relaxed(err)) == 0u) {
-      // scalar loop: every exit condition is wave-uniform
-      for (uint32_t polls = 0;; ++polls) {
-        ok = (int32_t)(uniform(ld_relaxed(cnt)) - target) >= 0;
-        if (ok || polls >= spin_limit) break;
-        __builtin_amdgcn_s_sleep(2);
-      }
-      if (!ok && (threadIdx.x & 63) == 0) __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    if (ok) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    if ((threadIdx.x & 63) == 0) *s_slot = ok;
+// A split-K part's arrival: store the partial, then one acquire-release
+// increment of the tile's counter (after every wave's stores are complete).
+// Returns true (uniformly) on the part that arrives last in this run, i.e.
+// that reads `target - 1`; that part has also acquired the others' partials
+// (agent-scope acquire by the incrementing thread, then a barrier and a
+// work-group acquire for the other waves).
+template <class T, int NB>
+__device__ __forceinline__ bool arrive_split(float* part, uint32_t* cnt, long tile, int S, int s, uint32_t target,
+                                             const f32x4 (&acc)[NB][T::TN][T::TM], int* s_slot) {
+  store_partial<T, NB>(part, tile, S, s, acc);
+  wait_all_mem();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    *s_slot = old == target - 1u;
   }
   __syncthreads();
-  const bool ok = uniform(*s_slot) != 0;
+  const bool last = uniform(*s_slot) != 0;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-  __syncthreads();  // *s_slot may be rewritten by the next wait
-  if constexpr (kTrace) tr.flag += trace_now() - t0;
-  return ok;
+  __syncthreads();  // *s_slot may be rewritten
+  return last;
 }
 
 // ------------------------------------------------------------------ ready flags
@@ -507,9 +504,8 @@ __device__ __forceinline__ bool wait_count(const uint32_t* cnt, uint32_t target,
 __device__ __forceinline__ void signal_ready(uint32_t* flag) { release_add(flag); }
 
 // Consumer side: before loading Z columns [k, k + kBK) of row block mb, the
-// GEMM1 tile (mb, k / bn1) must have signalled every time it does in a run
-// (once per split-K part), i.e. its counter must have reached
-// (epoch + 1) * S1 (compared wrap-safe).
+// GEMM1 tile (mb, k / bn1) must have signalled in this run (once per tile and
+// run), i.e. its counter must have reached epoch + 1 (compared wrap-safe).
 //
 // Wave 0 reads up to 64 consecutive counters of the item's K range in one
 // vector load and takes the longest ready prefix (a ballot), so that one

@@ -47,13 +47,20 @@ __device__ __forceinline__ void store_y(const Args& a, int row, int col, const f
   if (row < a.M) *reinterpret_cast<u32x4*>(a.Y + (long)row * a.H + col) = pack_bf16x8(v);
 }
 
-// Claims the next ticket early: thread 0 issues the atomic and parks the value
-// in *s_next; it is read after the item's closing barrier.  Called once per
-// item, after the item's last wait, so that an item never holds a claim it
-// might itself be waiting for.
+// Claims the next item early: thread 0 takes a ticket t of its claim list
+// l = blockIdx.x % lists and parks the item rank l + t * lists in *s_next; it
+// is read after the item's closing barrier.  Called once per item, after the
+// item's last wait, so that an item never holds a claim it might itself be
+// waiting for.  Work-groups are placed on the XCDs round-robin by index, so
+// with 8 lists every XCD takes every 8th item of the rank order: the same
+// number of weight-streaming items per XCD (and per L2 and fabric link),
+// while the chip as a whole still works through the ranks in order.
 __device__ __forceinline__ void claim_next(const Args& a, int* s_next) {
-  if (threadIdx.x == 0)
-    *s_next = (int)__hip_atomic_fetch_add(a.ctrl + CTRL_TICKET, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x == 0) {
+    const int l = (int)(blockIdx.x % (unsigned)a.lists);
+    const uint32_t t = __hip_atomic_fetch_add(a.ctrl + CTRL_TICKET + l, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *s_next = l + (int)t * a.lists;
+  }
 }
 
 // ------------------------------------------------------------------ trace records (MLP2_TRACE builds)
@@ -61,8 +68,9 @@ __device__ __forceinline__ void claim_next(const Args& a, int* s_next) {
 // Layout of the trace buffer: per kernel section (0 = GEMM1 or pipelined
 // kernel, 1 = GEMM2 kernel of the sequential mode; trace_groups work-groups
 // per section) and work-group, one word
-// with the item count, then trace_cap records of kTraceWords words: ticket,
-// start, mainloop end, end, ring-wait ticks, flag-wait ticks.  Records past
+// with the item count, then trace_cap records of kTraceWords words: rank,
+// start, mainloop end, split-K arrival released, siblings arrived (both 0
+// without split-K), end, ring-wait ticks, flag-wait ticks.  Records past
 // trace_cap are counted, not stored.  Written by thread 0 with plain stores.
 __device__ __forceinline__ void tr_mark_mainloop(TraceAcc& tr) { tr.t_main = trace_now(); }
 
@@ -76,19 +84,40 @@ __device__ __forceinline__ void tr_record(const Args& a, int section, int n, int
   r[0] = (uint64_t)ticket;
   r[1] = t_start;
   r[2] = tr.t_main;
-  r[3] = trace_now();
-  r[4] = tr.ring;
-  r[5] = tr.flag;
+  r[3] = tr.t_rel;
+  r[4] = tr.t_wait;
+  r[5] = trace_now();
+  r[6] = tr.ring;
+  r[7] = tr.flag;
+}
+
+// The completing part's reduction: every unit of the tile, G units per wave
+// at a time (two for one weight operand, one for two), handed to `epi` with
+// the unit's summed values.
+template <class T, int NB, class Epi>
+__device__ __forceinline__ void reduce_epilogue(const float* part, long tile, int S, Epi&& epi) {
+  constexpr int U = Partial<T, NB>::UNITS;
+  constexpr int G = NB == 1 ? 2 : 1;
+  static_assert(U % G == 0, "units per group");
+  const int lane = threadIdx.x & 63;
+  for (int u0 = uniform((int)(threadIdx.x >> 6)) * G; u0 < U; u0 += 4 * G) {
+    Unit<T> ug[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) ug[g] = Unit<T>(u0 + g);
+    float v[G][NB][8];
+    reduce_units<T, NB, G>(part, tile, S, ug, lane, v);
+#pragma unroll
+    for (int g = 0; g < G; ++g) epi(ug[g], lane, v[g]);
+  }
 }
 
 // ------------------------------------------------------------------ work items
 //
 // Split-K epilogue, shared by both GEMMs: each part stores its partial and
-// release-increments the tile's arrival counter, waits until all S parts have
-// arrived, then sums (in the fixed order s = 0..S-1) and finishes its own
-// share of the tile's units: units [s*U/S, (s+1)*U/S), one unit per wave at a
-// time.  Every part therefore reads about one tile's worth of partials, and
-// the tile's reduction runs on S work-groups at once.
+// counts its arrival (arrive_split); the part that completes the tile sums
+// all S partials in the fixed order s = 0..S-1 and runs the tile's epilogue,
+// the others claim their next item at once.  A GEMM1 tile signals its ready
+// counter once per run, after the tile's Z rows are stored.
 
 // GEMM1 item id = tile * S1 + s, tile = nb * Mb + mb.
 template <class T, int NB>
@@ -122,22 +151,16 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
         store_z<NB>(a, fp.row0 + 16 * tm, fp.col0 + 32 * tp, v);
       }
   } else {
-    store_partial<T, NB>(a.part1, tile, a.S1, s, acc);
-    release_add(a.cnt1 + tile);
-    wait_count(a.cnt1 + tile, (epoch + 1u) * (uint32_t)a.S1, a.spin_limit, a.ctrl + CTRL_ERROR, s_slot, tr);
+    const bool last = arrive_split<T, NB>(a.part1, a.cnt1 + tile, tile, a.S1, s, (epoch + 1u) * (uint32_t)a.S1, acc, s_slot);
+    if constexpr (kTrace) tr.t_rel = tr.t_wait = trace_now();
     claim_next(a, s_next);
-    constexpr int U = Partial<T, NB>::UNITS;
-    const int u0 = s * U / a.S1, u1 = (s + 1) * U / a.S1;
-    const int lane = threadIdx.x & 63;
-    for (int ui = u0 + uniform((int)(threadIdx.x >> 6)); ui < u1; ui += 4) {
-      const Unit<T> u(ui);
-      float v[NB][8];
-      reduce_unit<T, NB>(a.part1, tile, a.S1, u, lane, v);
+    if (!last) return;
+    reduce_epilogue<T, NB>(a.part1, tile, a.S1, [&](const Unit<T>& u, int lane, const float (&v)[NB][8]) {
       store_z<NB>(a, u.row(m0, lane), u.col(n0, lane), v);
-    }
+    });
   }
-  // Producer signal (one per part and run): Z rows of this part released, ready[tile] += 1.
-  if (!(tile == a.drop_signal && s == 0)) signal_ready(a.ready + tile);
+  // Producer signal (one per tile and run): the tile's Z rows are released, ready[tile] += 1.
+  if (tile != a.drop_signal) signal_ready(a.ready + tile);
 }
 
 // GEMM2 item p = tile * S2 + s (the parts of a tile are adjacent tickets,
@@ -157,8 +180,8 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
   const uint16_t* Bp[1] = {a.W2};
   const int zlast = a.Mb * T::BM - 1;
   if constexpr (WAIT) {
-    ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1,
-                (epoch + 1u) * (uint32_t)a.S1, a.spin_limit, s_slot, -1, &tr};
+    ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1, epoch + 1u, a.spin_limit, s_slot,
+                -1, &tr};
     mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, w, tr);
   } else {
     NoWait nowait;
@@ -178,19 +201,13 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
         store_y(a, fp.row0 + 16 * tm, fp.col0 + 32 * tp, v);
       }
   } else {
-    store_partial<T, 1>(a.part2, tile, a.S2, s, acc);
-    release_add(a.cnt2 + tile);
-    wait_count(a.cnt2 + tile, (epoch + 1u) * (uint32_t)a.S2, a.spin_limit, a.ctrl + CTRL_ERROR, s_slot, tr);
+    const bool last = arrive_split<T, 1>(a.part2, a.cnt2 + tile, tile, a.S2, s, (epoch + 1u) * (uint32_t)a.S2, acc, s_slot);
+    if constexpr (kTrace) tr.t_rel = tr.t_wait = trace_now();
     claim_next(a, s_next);
-    constexpr int U = Partial<T, 1>::UNITS;
-    const int u0 = s * U / a.S2, u1 = (s + 1) * U / a.S2;
-    const int lane = threadIdx.x & 63;
-    for (int ui = u0 + uniform((int)(threadIdx.x >> 6)); ui < u1; ui += 4) {
-      const Unit<T> u(ui);
-      float v[1][8];
-      reduce_unit<T, 1>(a.part2, tile, a.S2, u, lane, v);
+    if (!last) return;
+    reduce_epilogue<T, 1>(a.part2, tile, a.S2, [&](const Unit<T>& u, int lane, const float (&v)[1][8]) {
       store_y(a, u.row(m0, lane), u.col(n0, lane), v[0]);
-    }
+    });
   }
 }
 
@@ -202,7 +219,8 @@ __device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, boo
   if (threadIdx.x == 0) {
     const uint32_t old = __hip_atomic_fetch_add(a.ctrl + CTRL_DONE, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     if (old == gridDim.x - 1) {
-      __hip_atomic_store(a.ctrl + CTRL_TICKET, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int l = 0; l < a.lists; ++l)
+        __hip_atomic_store(a.ctrl + CTRL_TICKET + l, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __hip_atomic_store(a.ctrl + CTRL_DONE, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (end_of_run) __hip_atomic_store(a.ctrl + CTRL_EPOCH, epoch + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -211,21 +229,20 @@ __device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, boo
 
 // ------------------------------------------------------------------ kernels
 //
-// Every kernel is persistent: a work-group takes tickets from CTRL_TICKET
-// until the kernel's item list is exhausted.  Item lists (in ticket order):
+// Every kernel is persistent: a work-group claims item ranks (claim_next)
+// until the kernel's items are exhausted.  Items in rank order:
 //   PHASE_GEMM1:     GEMM1 items in the order table's order
 //   PHASE_GEMM2:     GEMM2 items
-//   PHASE_PIPELINED: both lists back to back; GEMM2 items wait per K-slice.
-// Waits: a split-K part waits for its sibling parts (adjacent tickets: the
-// parts of a tile are consecutive in every item list), a GEMM2 item for GEMM1
-// tiles (earlier tickets).  A work-group claims its next ticket only after the
-// last wait of its current item.  Let q be the first unclaimed ticket: every
-// tile whose parts all lie below q is held by work-groups that will finish it
-// (GEMM1 tiles first, then GEMM2 tiles, whose waits on GEMM1 therefore end);
-// only the tile containing q can have parts waiting for unclaimed siblings, at
-// most S - 1 of them.  So with a grid of at least max(S1, S2) work-groups some
-// work-group always gets to claim q: no launch deadlocks, whatever the
-// residency.  The host enforces that grid bound.
+//   PHASE_PIPELINED: both back to back; GEMM2 items wait per K-slice.
+// Claim list l holds the ranks congruent to l modulo `lists` and hands them
+// out in increasing order.  The only waits are a GEMM2 item's waits for GEMM1
+// tiles, which have lower ranks (split-K parts never wait for each other).  A
+// work-group claims its next item only after the last wait of its current
+// item.  Take the lowest-ranked unfinished item u: every lower rank is
+// finished, so if u is claimed its waits end and it finishes; if it is not,
+// every claimed item of its list ranks below u and is finished, so a
+// work-group of that list is free to claim it.  Hence no launch deadlocks for
+// any grid with at least one work-group per list, whatever the residency.
 
 enum { PHASE_GEMM1 = 0, PHASE_GEMM2 = 1, PHASE_PIPELINED = 2 };
 
@@ -288,6 +305,8 @@ template <int NS> struct TileFor<128, 128, NS> { using type = Tile<128, 128, 2, 
 template <int NS> struct TileFor<128, 256, NS> { using type = Tile<128, 256, 2, 2, NS>; };
 template <int NS> struct TileFor<64, 256, NS> { using type = Tile<64, 256, 1, 4, NS>; };
 template <int NS> struct TileFor<32, 256, NS> { using type = Tile<32, 256, 1, 4, NS>; };
+template <int NS> struct TileFor<256, 64, NS> { using type = Tile<256, 64, 4, 1, NS>; };
+template <int NS> struct TileFor<256, 128, NS> { using type = Tile<256, 128, 4, 1, NS>; };
 
 struct Entry {
   int bm, bn1, bn2, nb, ns;
@@ -317,6 +336,9 @@ static const Entry kEntries[] = {
     // wide weight tiles: half the activation traffic per weight byte
     MLP2_ENTRY(128, 256, 256, 1, 3), MLP2_ENTRY(128, 256, 128, 1, 3), MLP2_ENTRY(128, 128, 256, 1, 3),
     MLP2_ENTRY(128, 256, 256, 1, 2), MLP2_ENTRY(32, 256, 256, 1, 4), MLP2_ENTRY(64, 256, 256, 1, 3),
+    // 256-row blocks: the weights of a 129..256-row batch are streamed once
+    MLP2_ENTRY(256, 64, 128, 2, 3), MLP2_ENTRY(256, 64, 64, 2, 3), MLP2_ENTRY(256, 128, 128, 1, 3),
+    MLP2_ENTRY(256, 64, 64, 1, 3),
 };
 
 static const Entry* find_entry(const KernelConfig& c) {
@@ -334,13 +356,15 @@ hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu) {
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, kThreads, 0);
 }
 
-hipError_t launch_sequential(const KernelConfig& c, const Args& a, const int grids[2], hipStream_t stream) {
+hipError_t launch_sequential(const KernelConfig& c, const Args& a1, const Args& a2, const int grids[2],
+                             hipStream_t stream) {
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
-  void* args[] = {const_cast<Args*>(&a)};
-  hipError_t err = hipLaunchKernel(e->seq1, dim3(grids[0]), dim3(kThreads), args, 0, stream);
+  void* args1[] = {const_cast<Args*>(&a1)};
+  hipError_t err = hipLaunchKernel(e->seq1, dim3(grids[0]), dim3(kThreads), args1, 0, stream);
   if (err != hipSuccess) return err;
-  return hipLaunchKernel(e->seq2, dim3(grids[1]), dim3(kThreads), args, 0, stream);
+  void* args2[] = {const_cast<Args*>(&a2)};
+  return hipLaunchKernel(e->seq2, dim3(grids[1]), dim3(kThreads), args2, 0, stream);
 }
 
 hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipStream_t stream) {

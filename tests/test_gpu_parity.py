@@ -35,6 +35,8 @@ SMALL = [
     (16, 1024, 1024, 1, {"splitk1": 4, "splitk2": 4, "bn1": 64, "bn2": 64}),
     (200, 640, 1280, 1, {"bm": 128, "bn1": 128, "bn2": 128}),
     (129, 256, 384, 2, {"bm": 128, "splitk1": 2}),
+    (200, 320, 640, 2, None),
+    (140, 256, 384, 0, {"splitk1": 2, "splitk2": 3}),
 ]
 
 

@@ -23,7 +23,7 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("order", [B.ORDER_ROW_FIRST, B.ORDER_REVERSED, B.ORDER_SHUFFLED, B.ORDER_COLUMN_FIRST])
-@pytest.mark.parametrize("grid", [3, 4, 17, 0])
+@pytest.mark.parametrize("grid", [1, 2, 3, 4, 17, 0])
 def test_orders_and_grids_match_sequential_bits(lib, order, grid):
     M, H, F, act = 160, 256, 768, 1
     d = I.make_inputs(M, H, F, act, seed=40 + order)
@@ -113,11 +113,13 @@ def test_run_argument_errors(lib):
         plan.run(g["X"], g["W1"], g["W2"], torch.empty(M, H + 1, dtype=torch.bfloat16, device="cuda"), 0)
     info = plan.info()
     assert info["items1"] == info["row_blocks"] * info["col_blocks1"] * info["splitk1"]
-    # split-K parts wait for their siblings: a grid below max(S1, S2) is refused
-    smax = max(info["splitk1"], info["splitk2"])
-    if smax > 1:
-        with pytest.raises(B.Mlp2Error):
-            plan.set_option(B.OPT_GRID, smax - 1)
+    # persistent grids: any size from one work-group up to what fits the device at once
+    too_many = info["occupancy"] * info["num_cus"] + 1
+    with pytest.raises(B.Mlp2Error):
+        plan.set_option(B.OPT_GRID, too_many)
+    with pytest.raises(B.Mlp2Error):
+        plan.set_option(B.OPT_GRID, -1)
+    plan.set_option(B.OPT_GRID, 1)
     plan.set_option(B.OPT_GRID, 0)
     assert info["grid_pipelined"] >= 1 and info["occupancy"] >= 1
     plan.close()

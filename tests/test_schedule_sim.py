@@ -1,14 +1,17 @@
-"""CPU simulation of the persistent ticket scheduler (no GPU needed).
+"""CPU simulation of the persistent item scheduler (no GPU needed).
 
-The kernels hand out work items through one ticket counter: GEMM1 items (in
-the order table's order) then, in the pipelined launch, GEMM2 items.  A
-split-K part waits for its sibling parts; a GEMM2 item waits, K-slice by
-K-slice, for the GEMM1 tiles of its row block; a work-group claims its next
-ticket after the last wait of its current item.  The claim in the design is
-that every launch finishes for any grid of at least max(S1, S2) work-groups,
-because the parts of a tile are adjacent tickets.  This simulates that
-protocol with random item durations and checks it, and checks that a
-split-major numbering of the GEMM2 parts (not adjacent) can deadlock.
+The kernels hand out work items by rank: GEMM1 items (in the order table's
+order) then, in the pipelined launch, GEMM2 items.  Work-group g claims from
+list g % L, which hands out the ranks congruent to its index modulo L in
+increasing order (L = min(8, grid): one list per XCD).  Split-K parts never
+wait for each other: each counts its arrival and the last one to arrive
+finishes the tile (a GEMM1 tile then signals its ready counter).  A GEMM2 item
+waits for the GEMM1 tiles of its K range; a work-group claims its next item
+after the last wait of its current one.  The claim in the design is that
+every launch finishes for any grid of at least one work-group, because every
+wait targets a lower rank.  This simulates that protocol with random item
+durations and checks it, and checks that a rank order putting consumers
+before their producers can deadlock.
 """
 import random
 
@@ -26,44 +29,49 @@ def column_first_tiles(Mb, Nb1, order, seed=12345):
     return tiles
 
 
-def items(Mb, Nb1, Nb2, S1, S2, kslices_per_part, order, gemm2_split_major=False):
-    """Ticket-ordered items: (kind, tile, s, needs) with needs = GEMM1 column blocks a GEMM2 part reads."""
-    out = []
-    for t in column_first_tiles(Mb, Nb1, order):
-        for s in range(S1):
-            out.append(("g1", t, s, []))
-    tiles2 = Mb * Nb2
-    idx = [(tile, s) for tile in range(tiles2) for s in range(S2)]
-    if gemm2_split_major:
-        idx = [(tile, s) for s in range(S2) for tile in range(tiles2)]
-    per = (Nb1 + S2 - 1) // S2
-    for tile, s in idx:
+def items(Mb, Nb1, Nb2, S1, S2, order, consumers_first=False):
+    """Rank-ordered items: (kind, tile, s, needs) with needs = GEMM1 tiles a GEMM2 part reads."""
+    g1 = [("g1", t, s, []) for t in column_first_tiles(Mb, Nb1, order) for s in range(S1)]
+    per = -(-Nb1 // S2)
+    g2 = []
+    for tile in range(Mb * Nb2):
         mb = tile % Mb
-        kbs = [kb for kb in range(s * per, min(Nb1, (s + 1) * per))]
-        out.append(("g2", tile, s, [(kb * Mb + mb) for kb in kbs]))
-    return out
+        for s in range(S2):
+            kbs = range(s * per, min(Nb1, (s + 1) * per))
+            g2.append(("g2", tile, s, [kb * Mb + mb for kb in kbs]))
+    return g2 + g1 if consumers_first else g1 + g2
 
 
-def simulate(item_list, S1, S2, grid, seed, max_steps=200000):
+def claim_lists(grid):
+    """The host's rule: one list per XCD, fewer when the grid is smaller."""
+    return min(8, max(1, grid))
+
+
+def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000):
     """Returns True if every item completes."""
     rng = random.Random(seed)
+    lists = lists or claim_lists(grid)
     S = {"g1": S1, "g2": S2}
     arrived = {}  # (kind, tile) -> parts arrived
-    signals = {}  # GEMM1 tile -> parts signalled
+    signals = set()  # GEMM1 tiles whose last part has finished the tile
     done = 0
-    ticket = [0]
+    ticket = [0] * lists
 
-    def claim():
-        t = ticket[0]
-        ticket[0] += 1
-        return t
+    def claim(g):
+        lst = g % lists
+        t = ticket[lst]
+        ticket[lst] += 1
+        return lst + t * lists
 
-    # work-group state: [item index or None, phase, remaining time, prefetched ticket]
-    wgs = [[claim(), "main", rng.randint(1, 5), None] for _ in range(grid)]
-    for step in range(max_steps):
+    # work-group state: [item rank or None, phase, remaining time]
+    order = list(range(grid))
+    rng.shuffle(order)  # first claims in any order
+    first = {g: claim(g) for g in order}
+    wgs = [[first[g], "main", rng.randint(1, 5)] for g in range(grid)]
+    for _ in range(max_steps):
         progressed = False
-        for w in wgs:
-            p, phase, rem, nxt = w
+        for g, w in enumerate(wgs):
+            p, phase, rem = w
             if p is None:
                 continue
             if p >= len(item_list):
@@ -71,33 +79,19 @@ def simulate(item_list, S1, S2, grid, seed, max_steps=200000):
                 progressed = True
                 continue
             kind, tile, s, needs = item_list[p]
-            if phase == "main":
-                # a GEMM2 part may only run once its Z slices are complete
-                if kind == "g2" and any(signals.get(n, 0) < S1 for n in needs):
-                    continue
-                if rem > 0:
-                    w[2] -= 1
-                    progressed = True
-                    continue
-                if S[kind] > 1:
-                    arrived[(kind, tile)] = arrived.get((kind, tile), 0) + 1
-                    w[1] = "siblings"
-                else:
-                    w[1] = "epilogue"
-                    w[3] = claim()
+            if kind == "g2" and any(n not in signals for n in needs):
+                continue  # waiting for producer tiles
+            if rem > 0:
+                w[2] -= 1
                 progressed = True
-            elif phase == "siblings":
-                if arrived[(kind, tile)] < S[kind]:
-                    continue
-                w[1] = "epilogue"
-                w[3] = claim()
-                progressed = True
-            elif phase == "epilogue":
-                if kind == "g1":
-                    signals[tile] = signals.get(tile, 0) + 1
-                done += 1
-                w[0], w[1], w[2], w[3] = nxt, "main", rng.randint(1, 5), None
-                progressed = True
+                continue
+            key = (kind, tile)
+            arrived[key] = arrived.get(key, 0) + 1
+            if arrived[key] == S[kind] and kind == "g1":
+                signals.add(tile)  # the completing part reduces, stores Z and signals
+            done += 1
+            w[0], w[2] = claim(g), rng.randint(1, 5)
+            progressed = True
         if done == len(item_list):
             return True
         if not progressed:
@@ -112,22 +106,33 @@ CASES = [
     (3, 5, 2, 1, 4),
     (1, 16, 8, 4, 2),
     (2, 4, 4, 1, 1),
+    (1, 6, 2, 12, 9),
 ]
 
 
 @pytest.mark.parametrize("order", ["column", "row", "reversed", "shuffled"])
 @pytest.mark.parametrize("Mb,Nb1,Nb2,S1,S2", CASES)
-def test_pipelined_schedule_finishes_for_any_grid_from_max_s(order, Mb, Nb1, Nb2, S1, S2):
-    lst = items(Mb, Nb1, Nb2, S1, S2, 1, order)
-    for grid in range(max(S1, S2), max(S1, S2) + 6):
-        for seed in range(8):
+def test_pipelined_schedule_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
+    lst = items(Mb, Nb1, Nb2, S1, S2, order)
+    for grid in (1, 2, 3, 5, 7, 8, 9, 16, 17, 40):
+        for seed in range(6):
             assert simulate(lst, S1, S2, grid, seed), (order, grid, seed)
 
 
-def test_split_major_gemm2_parts_can_deadlock():
-    """The numbering the kernels avoid: parts of a GEMM2 tile spread over the ticket range."""
-    Mb, Nb1, Nb2, S1, S2 = 1, 4, 4, 1, 3
-    lst = items(Mb, Nb1, Nb2, S1, S2, 1, "column", gemm2_split_major=True)
-    assert not all(simulate(lst, S1, S2, 3, seed) for seed in range(8))
-    lst_ok = items(Mb, Nb1, Nb2, S1, S2, 1, "column")
-    assert all(simulate(lst_ok, S1, S2, 3, seed) for seed in range(8))
+def test_consumers_ranked_before_producers_can_deadlock():
+    """Why GEMM2 items follow every GEMM1 item in rank order."""
+    Mb, Nb1, Nb2, S1, S2 = 1, 4, 4, 1, 1
+    bad = items(Mb, Nb1, Nb2, S1, S2, "column", consumers_first=True)
+    assert not all(simulate(bad, S1, S2, 3, seed) for seed in range(6))
+    good = items(Mb, Nb1, Nb2, S1, S2, "column")
+    assert all(simulate(good, S1, S2, 3, seed) for seed in range(6))
+
+
+def test_lists_cover_every_rank_once():
+    for grid in (1, 3, 8, 13, 64):
+        L = claim_lists(grid)
+        seen = []
+        for lst in range(L):
+            seen += [lst + t * L for t in range(100) if lst + t * L < 100]
+        assert sorted(seen) == list(range(100))
+        assert L <= grid
