@@ -4,11 +4,15 @@
 A step is one ``mlp2_run`` (the whole hot path: GEMM1 + activation + ready
 signals + GEMM2) over one batch of synthetic inputs already resident in HBM.
 W warm-up steps, then exactly K back-to-back steps of the tile-pipelined mode
-timed between a synchronise on each side, then the same for the sequential
-mode.  The JSON line on stdout carries the pipelined latency as ``value``,
-the sequential latency beside it, the roofline fraction of the dominant
-kernel (HIP events on the launch stream) and the CPU oracle timed on a
-bounded sample.
+timed between a synchronise on each side; ``value`` is that block's mean
+latency per step.  Beside it the line carries the sequential mode's latency
+(same block timing), cold latencies of both modes (a 1 GiB write evicts the
+L2s and the 256 MB MALL before each timed run, modes interleaved), the
+roofline fraction of the dominant kernel (the pipelined launch, timed with HIP
+events on the stream it is launched on), HBM traffic from committed
+rocprofv3 counter summaries when they match the current kernel sources, a
+table of both modes on every MLP workload, and the fp64 CPU oracle timed on a
+bounded sample of the headline workload.
 
 Only ``--gpus 1`` is supported: the build targets a single GPU.
 """
@@ -18,6 +22,7 @@ import argparse
 import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -28,6 +33,7 @@ METRIC = "2-layer MLP latency µs (pipelined vs sequential) + % HBM BW / MFMA pe
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 KERNEL_SOURCES = ["paper_2607_07862_amd/csrc/mlp2_device.hpp", "paper_2607_07862_amd/csrc/mlp2_kernels.hip"]
+FLUSH_BYTES = 1 << 30
 
 
 def log(*a):
@@ -43,33 +49,104 @@ def kernel_source_hash() -> str:
 
 
 def measured_traffic(workload_key: str):
-    """HBM bytes per launch from the committed rocprofv3 --pmc summary, if it matches these sources."""
+    """HBM bytes per pipelined launch from the committed counter summary, if it matches these sources."""
     p = os.path.join(ROOT, "profiles", f"traffic_{workload_key}.json")
     if not os.path.exists(p):
         return None
     try:
-        d = json.load(open(p))
-    except Exception:
+        with open(p) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
         return None
     if d.get("kernel_source_hash") != kernel_source_hash():
         return None
-    return d.get("bytes_per_launch")
+    return d.get("hbm_bytes_per_launch")
 
 
-def time_block(plan, g, Y, mode, steps, stream):
+def bound_of(w) -> str:
+    return "mfma" if w.alg_flops() / w.alg_bytes() > BF16_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3 else "hbm"
+
+
+def roofline(w, us: float) -> dict:
+    if bound_of(w) == "hbm":
+        achieved = w.alg_bytes() / (us * 1e-6) / 1e9
+        r = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    else:
+        achieved = w.alg_flops() / (us * 1e-6) / 1e12
+        r = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+    r["frac"] = round(achieved / r["peak"], 4)
+    return r
+
+
+def device_random_inputs(w):
+    """Inputs of the workload's shapes and distributions drawn on the device (timing only)."""
     import torch
 
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    start.record(stream)
-    for _ in range(steps):
-        plan.run(g["X"], g["W1"], g["W2"], Y, mode, stream=stream)
-    stop.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    return start.elapsed_time(stop) * 1e3 / steps, wall  # us per step (events), wall seconds
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1000 + w.seed)
+    n1 = 2 if w.gated else 1
+    X = torch.randn(w.M, w.H, device="cuda", generator=gen).to(torch.bfloat16)
+    W1 = (torch.randn(n1 * w.H, w.F, device="cuda", generator=gen) * w.H ** -0.5).to(torch.bfloat16)
+    W2 = (torch.randn(w.F, w.H, device="cuda", generator=gen) * w.F ** -0.5).to(torch.bfloat16)
+    return {"X": X, "W1": W1, "W2": W2}
+
+
+class Runner:
+    def __init__(self, B, w, g, tuning, stream):
+        import torch
+
+        self.B, self.w, self.g, self.stream = B, w, g, stream
+        self.Y = torch.empty(w.M, w.H, dtype=torch.bfloat16, device="cuda")
+        self.plan = B.Plan(w.M, w.H, w.F, w.act, tuning)
+        self.info = self.plan.info()
+
+    def run(self, mode):
+        self.plan.run(self.g["X"], self.g["W1"], self.g["W2"], self.Y, mode, stream=self.stream)
+
+    def block(self, mode, steps):
+        """Mean µs per step of `steps` back-to-back runs (HIP events on the launch stream)."""
+        import torch
+
+        start = torch.cuda.Event(enable_timing=True)
+        stop = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(self.stream)
+        for _ in range(steps):
+            self.run(mode)
+        stop.record(self.stream)
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) * 1e3 / steps
+
+    def cold(self, modes, iters, flush):
+        """Per-run µs with the caches flushed before every run, modes interleaved."""
+        import torch
+
+        out = {m: [] for m in modes}
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters * len(modes))]
+        i = 0
+        for _ in range(iters):
+            for m in modes:
+                flush.zero_()
+                a, b = evs[i]
+                a.record(self.stream)
+                self.run(m)
+                b.record(self.stream)
+                out[m].append((a, b))
+                i += 1
+        torch.cuda.synchronize()
+        return {m: [a.elapsed_time(b) * 1e3 for a, b in v] for m, v in out.items()}
+
+    def check(self):
+        if self.plan.check() != self.B.OK:
+            raise RuntimeError(f"{self.w.name}: a device flag wait timed out")
+
+    def close(self):
+        self.plan.close()
+
+
+def pct(v, q):
+    v = sorted(v)
+    return v[min(len(v) - 1, max(0, int(round(q * (len(v) - 1)))))]
 
 
 def cpu_baseline(w, d, budget_s: float):
@@ -101,12 +178,12 @@ def cpu_baseline(w, d, budget_s: float):
             break
     per_row = sum(times) / rows_done
     return {
-        "value": per_row * w.M * 1e6,
+        "value": round(per_row * w.M * 1e6, 1),
         "unit": "us",
         "cores": int(cores),
         "kind": "oracle",
-        "sample": f"{rows_done} output rows in {len(times)} calls of {rows_per} rows (fp64 numpy, weights decoded per "
-        f"call); value = measured time per row x M={w.M}",
+        "sample": f"{rows_done} output rows of {w.name} in {len(times)} calls of {rows_per} rows (fp64 numpy, "
+        f"weights decoded per call); value = measured time per row x M={w.M}",
     }
 
 
@@ -118,13 +195,18 @@ def main():
     ap.add_argument("--workload", default="l8b_decode")
     ap.add_argument("--tuning", default="", help="JSON dict of mlp2_tuning_t fields")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
-    ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--all", action="store_true", help="also time every workload (stderr table)")
+    ap.add_argument("--cold-iters", type=int, default=20)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
+    ap.add_argument("--no-table", action="store_true", help="skip the table of all workloads")
+    ap.add_argument("--only-pipelined", action="store_true", help="time the pipelined mode only (profiling runs)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="first copy MIB MiB device-to-device (a plain copy kernel of known size, for counter scaling)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: this build runs on a single MI355X (use --gpus 1)", file=sys.stderr)
+        print("bench.py measures one GPU only: this build runs the hot path on a single MI355X (use --gpus 1)",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -139,54 +221,93 @@ def main():
     stream = torch.cuda.current_stream()
     tuning = json.loads(args.tuning) if args.tuning else None
 
-    def bench_workload(key, steps, warmup):
-        w = I.WORKLOADS[key]
-        log(f"workload {w.name}: generating inputs (seed {w.seed})")
-        d = I.workload_inputs(w)
-        g = {k: v.to("cuda") for k, v in d.items()}
-        Y = torch.empty(w.M, w.H, dtype=torch.bfloat16, device="cuda")
-        plan = B.Plan(w.M, w.H, w.F, w.act, tuning)
-        info = plan.info()
-        for _ in range(warmup):
-            plan.run(g["X"], g["W1"], g["W2"], Y, B.MODE_TILE_PIPELINED, stream=stream)
-            plan.run(g["X"], g["W1"], g["W2"], Y, B.MODE_SEQUENTIAL, stream=stream)
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
         torch.cuda.synchronize()
-        if plan.check() != B.OK:
-            raise RuntimeError("device flag wait timed out during warm-up")
-        pipe_us, wall = time_block(plan, g, Y, B.MODE_TILE_PIPELINED, steps, stream)
-        seq_us, _ = time_block(plan, g, Y, B.MODE_SEQUENTIAL, steps, stream)
-        pipe_us2, _ = time_block(plan, g, Y, B.MODE_TILE_PIPELINED, steps, stream)
-        if plan.check() != B.OK:
-            raise RuntimeError("device flag wait timed out during timing")
-        log(f"{w.name}: pipelined {pipe_us:.2f} / {pipe_us2:.2f} us, sequential {seq_us:.2f} us  info={info}")
-        return w, d, plan, info, pipe_us, seq_us, pipe_us2, wall
+        log(f"copy calibration: 3 copies of {args.copy_calibration} MiB")
+        del src, dst
 
-    if args.all:
-        for key in I.WORKLOAD_ORDER:
-            if key == args.workload:
-                continue
-            w, _, plan, info, p, s, p2, _ = bench_workload(key, max(10, args.steps // 2), 3)
-            bound = "mfma" if w.alg_flops() / w.alg_bytes() > BF16_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3 else "hbm"
-            pm = min(p, p2)
-            log(f"TABLE {key} pipelined_us={pm:.2f} sequential_us={s:.2f} gain={(s - pm) / s * 100:.1f}% "
-                f"hbm={w.alg_bytes() / pm / 1e3:.0f}GB/s ({w.alg_bytes() / pm / 1e3 / HBM_PEAK_GBS * 100:.1f}%) "
-                f"mfma={w.alg_flops() / pm / 1e6:.0f}TF/s ({w.alg_flops() / pm / 1e6 / BF16_PEAK_TFLOPS * 100:.1f}%) "
-                f"bound={bound}")
-            plan.close()
-            torch.cuda.empty_cache()
-
-    w, d, plan, info, pipe_us, seq_us, pipe_us2, wall = bench_workload(args.workload, args.steps, args.warmup)
-    value = pipe_us  # the first timed block of exactly K pipelined steps
-    bound = "mfma" if w.alg_flops() / w.alg_bytes() > BF16_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3 else "hbm"
-    if bound == "hbm":
-        achieved = w.alg_bytes() / (value * 1e-6) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    else:
-        achieved = w.alg_flops() / (value * 1e-6) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
-    roof["frac"] = round(achieved / roof["peak"], 4)
+    # ---- headline workload: the seeded inputs
+    w = I.WORKLOADS[args.workload]
+    log(f"workload {w.name}: generating seeded inputs (seed {w.seed})")
+    d = I.workload_inputs(w)
+    g = {k: v.to("cuda") for k, v in d.items()}
+    r = Runner(B, w, g, tuning, stream)
+    log(f"plan {r.info}")
+    for _ in range(args.warmup):
+        r.run(B.MODE_TILE_PIPELINED)
+        if not args.only_pipelined:
+            r.run(B.MODE_SEQUENTIAL)
+    torch.cuda.synchronize()
+    r.check()
+    log(f"timing {args.steps} pipelined steps")
+    value = r.block(B.MODE_TILE_PIPELINED, args.steps)
+    extra = {}
+    if not args.only_pipelined:
+        seq_us = r.block(B.MODE_SEQUENTIAL, args.steps)
+        pipe2 = r.block(B.MODE_TILE_PIPELINED, args.steps)
+        log(f"pipelined {value:.2f} us (repeat {pipe2:.2f}), sequential {seq_us:.2f} us")
+        flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+        cold = r.cold([B.MODE_TILE_PIPELINED, B.MODE_SEQUENTIAL], args.cold_iters, flush)
+        del flush
+        cp, cs = cold[B.MODE_TILE_PIPELINED], cold[B.MODE_SEQUENTIAL]
+        extra = {
+            "sequential_us": round(seq_us, 3),
+            "pipelined_repeat_us": round(pipe2, 3),
+            "gain_vs_sequential_pct": round((seq_us - value) / seq_us * 100, 2),
+            "cold": {
+                "pipelined_median_us": round(statistics.median(cp), 2),
+                "pipelined_p10_p90_us": [round(pct(cp, 0.1), 2), round(pct(cp, 0.9), 2)],
+                "sequential_median_us": round(statistics.median(cs), 2),
+                "sequential_p10_p90_us": [round(pct(cs, 0.1), 2), round(pct(cs, 0.9), 2)],
+                "iters": args.cold_iters,
+                "flush": "1 GiB device write before each timed run, modes interleaved",
+            },
+        }
+        log(f"cold: pipelined {extra['cold']['pipelined_median_us']} us, sequential {extra['cold']['sequential_median_us']} us")
+    r.check()
+    info = r.info
+    roof = roofline(w, value)
     roof["traffic"] = measured_traffic(args.workload)
-    roof["kernel"] = "k_pipelined (one launch per step)"
+    roof["kernel"] = "k_mlp2 pipelined launch (one per step)"
+    r.close()
+
+    # ---- every workload: both modes (device-drawn inputs of the same shapes)
+    table = {}
+    if not args.no_table and not args.only_pipelined:
+        for key in I.WORKLOAD_ORDER:
+            wk = I.WORKLOADS[key]
+            if key == args.workload:
+                rr_p, rr_s, inf = value, extra["sequential_us"], info
+            else:
+                rr = Runner(B, wk, device_random_inputs(wk), None, stream)
+                for _ in range(5):
+                    rr.run(B.MODE_TILE_PIPELINED)
+                    rr.run(B.MODE_SEQUENTIAL)
+                steps = max(10, args.steps // 2)
+                rr_p = rr.block(B.MODE_TILE_PIPELINED, steps)
+                rr_s = rr.block(B.MODE_SEQUENTIAL, steps)
+                rr.check()
+                inf = rr.info
+                rr.close()
+                torch.cuda.empty_cache()
+            rf = roofline(wk, rr_p)
+            row = {
+                "pipelined_us": round(rr_p, 2),
+                "sequential_us": round(rr_s, 2),
+                "gain_pct": round((rr_s - rr_p) / rr_s * 100, 1),
+                "bound": rf["bound"],
+                "frac": rf["frac"],
+                "hbm_frac": round(wk.alg_bytes() / (rr_p * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                "mfma_frac": round(wk.alg_flops() / (rr_p * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                "tiles": [inf["bm"], inf["bn1"], inf["splitk1"], inf["bn2"], inf["splitk2"], inf["stages"]],
+            }
+            table[key] = row
+            log(f"TABLE {key:12s} {row}")
 
     cpu = None
     if not args.no_cpu:
@@ -213,18 +334,16 @@ def main():
             "F": w.F,
             "act": ["identity", "gelu_tanh", "swiglu"][w.act],
             "mode": "tile_pipelined",
-            "tiles": {k: info[k] for k in ("bm", "bn1", "splitk1", "bn2", "splitk2", "items1", "items2",
+            "tiles": {k: info[k] for k in ("bm", "bn1", "splitk1", "bn2", "splitk2", "stages", "items1", "items2",
                                            "grid_pipelined", "occupancy")},
         },
-        "sequential_us": round(seq_us, 3),
-        "pipelined_repeat_us": round(pipe_us2, 3),
-        "gain_vs_sequential_pct": round((seq_us - value) / seq_us * 100, 2),
+        **extra,
         "alg_bytes": w.alg_bytes(),
         "alg_flops": w.alg_flops(),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "workloads": table,
     }
-    plan.close()
     print(json.dumps(out), flush=True)
 
 

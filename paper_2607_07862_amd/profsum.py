@@ -1,0 +1,165 @@
+"""Summaries of rocprofv3 output for the committed profiles.
+
+    python -m paper_2607_07862_amd.profsum stats DIR OUT.md --cmd "<command>"
+        Kernel durations from ``--kernel-trace --stats`` CSV output in DIR.
+
+    python -m paper_2607_07862_amd.profsum traffic FETCH_DIR WRITE_DIR WORKLOAD OUT_STEM \\
+            --copy-mib N --cmd-fetch "<command>" --cmd-write "<command>"
+        HBM traffic per pipelined launch from two ``--pmc`` runs (FETCH_SIZE,
+        then WRITE_SIZE, KiB per dispatch), each scaled by what the same
+        counter reads for the plain copy of N MiB that bench.py's
+        ``--copy-calibration N`` performs first.  Writes OUT_STEM.json (read
+        by bench.py, tagged with the hash of the kernel sources) and
+        OUT_STEM.md.
+
+Reads CSV files only; runs nothing.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import json
+import os
+import re
+import sys
+from collections import defaultdict
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def short_name(n: str) -> str:
+    m = re.search(r"k_mlp2<mlp2::Tile<(\d+), (\d+), \d+, \d+, (\d+)>, (\d), mlp2::Tile<(\d+), (\d+), \d+, \d+, \d+>, (\d)>", n)
+    if m:
+        phase = ["gemm1", "gemm2", "pipelined"][int(m.group(7))]
+        return f"k_mlp2 {phase} (bm {m.group(1)}, bn1 {m.group(2)}, bn2 {m.group(6)}, nb {m.group(4)}, stages {m.group(3)})"
+    return n if len(n) < 90 else n[:87] + "..."
+
+
+def _one(pattern: str) -> str:
+    files = sorted(glob.glob(pattern, recursive=True))
+    if not files:
+        sys.exit(f"no file matches {pattern}")
+    return files[0]
+
+
+def stats(args):
+    f = _one(os.path.join(args.dir, "**", "*kernel_stats.csv"))
+    rows = list(csv.DictReader(open(f)))
+    lines = [
+        f"# {args.title}",
+        "",
+        "Command (from the repository root on the GPU host):",
+        "",
+        "```",
+        args.cmd,
+        "```",
+        "",
+        "| kernel | calls | average µs | min µs | max µs | share of GPU time |",
+        "|---|---:|---:|---:|---:|---:|",
+    ]
+    for r in rows:
+        lines.append(
+            f"| {short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+            f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} % |"
+        )
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print(args.out)
+
+
+def _counter(dirname: str, counter: str):
+    """{kernel name: [value per dispatch]} for one counter."""
+    f = _one(os.path.join(dirname, "**", "*counter_collection.csv"))
+    per = defaultdict(lambda: defaultdict(float))
+    for r in csv.DictReader(open(f)):
+        if r["Counter_Name"] != counter:
+            continue
+        per[r["Kernel_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
+    return {k: list(v.values()) for k, v in per.items()}
+
+
+def _copy_kernel(per: dict) -> str:
+    names = [k for k in per if re.search(r"copy", k, re.I) and "k_mlp2" not in k]
+    if not names:
+        sys.exit("no copy kernel in the counter output (run bench.py with --copy-calibration)")
+    return max(names, key=lambda k: max(per[k]))
+
+
+def traffic(args):
+    sys.path.insert(0, ROOT)
+    from bench import kernel_source_hash
+    from paper_2607_07862_amd import inputs as I
+
+    w = I.WORKLOADS[args.workload]
+    copy_bytes = args.copy_mib << 20
+    out = {"workload": w.name, "kernel_source_hash": kernel_source_hash(), "copy_calibration_bytes": copy_bytes}
+    lines = [f"# HBM traffic of the pipelined launch, {w.name}", ""]
+    for counter, d, cmd in (("FETCH_SIZE", args.fetch_dir, args.cmd_fetch), ("WRITE_SIZE", args.write_dir, args.cmd_write)):
+        per = _counter(d, counter)
+        ck = _copy_kernel(per)
+        copy_kib = max(per[ck])  # the largest dispatch of the copy kernel is the calibration copy
+        factor = copy_bytes / (copy_kib * 1024.0)
+        pk = [k for k in per if "k_mlp2" in k and re.search(r", 2>\(", k)]
+        if len(pk) != 1:
+            sys.exit(f"expected one pipelined kernel, found {pk}")
+        vals = per[pk[0]]
+        kib = sum(vals) / len(vals)
+        out[counter.lower()] = {
+            "kib_per_dispatch_raw": round(kib, 1),
+            "dispatches": len(vals),
+            "copy_kernel": short_name(ck),
+            "copy_kib_raw": round(copy_kib, 1),
+            "scale": round(factor, 4),
+            "bytes_per_launch": int(kib * 1024 * factor),
+        }
+        lines += [
+            f"## {counter}",
+            "",
+            "```",
+            cmd,
+            "```",
+            "",
+            f"- pipelined kernel: {kib:.1f} KiB per dispatch (mean of {len(vals)} dispatches)",
+            f"- calibration: {short_name(ck)} copying {args.copy_mib} MiB "
+            f"{'reads' if counter == 'FETCH_SIZE' else 'writes'} {copy_kib:.1f} KiB "
+            f"-> scale {factor:.4f}",
+            f"- scaled: {kib * 1024 * factor / 1e6:.1f} MB per launch",
+            "",
+        ]
+    total = out["fetch_size"]["bytes_per_launch"] + out["write_size"]["bytes_per_launch"]
+    out["hbm_bytes_per_launch"] = total
+    out["alg_bytes"] = w.alg_bytes()
+    out["ratio_to_alg"] = round(total / w.alg_bytes(), 3)
+    lines += [
+        f"HBM bytes per launch (fetch + write, scaled): {total / 1e6:.1f} MB; algorithmic bytes "
+        f"(X + weights + Y): {w.alg_bytes() / 1e6:.1f} MB; ratio {out['ratio_to_alg']}.",
+        "",
+        f"Kernel sources hash: {out['kernel_source_hash']} (bench.py reports these bytes only while it matches).",
+    ]
+    json.dump(out, open(args.out_stem + ".json", "w"), indent=1)
+    open(args.out_stem + ".md", "w").write("\n".join(lines) + "\n")
+    print(args.out_stem + ".json")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd_name", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("dir")
+    s.add_argument("out")
+    s.add_argument("--cmd", required=True)
+    s.add_argument("--title", default="rocprofv3 kernel statistics")
+    t = sub.add_parser("traffic")
+    t.add_argument("fetch_dir")
+    t.add_argument("write_dir")
+    t.add_argument("workload")
+    t.add_argument("out_stem")
+    t.add_argument("--copy-mib", type=int, required=True)
+    t.add_argument("--cmd-fetch", required=True)
+    t.add_argument("--cmd-write", required=True)
+    a = ap.parse_args()
+    (stats if a.cmd_name == "stats" else traffic)(a)
+
+
+if __name__ == "__main__":
+    main()
