@@ -67,13 +67,18 @@ enum mlp2_status {
   MLP2_ERR_DEVICE = -6       /* no usable gfx950 device, or the plan belongs to another device */
 };
 
-/* GEMM1 tile-ordering policies of the pipelined mode (Sec. III-A.5: the first
- * kernel may take its tiles from a predefined source order). */
+/* GEMM1 tile-ordering policies (Sec. III-A.5: the first kernel may take its
+ * tiles from a predefined source order).  The default is column-first: whole
+ * column blocks of Z first, so GEMM2's K-slices complete in order, and the
+ * row blocks of one column block (which share its weight columns) run
+ * together.  (Row-block-first halves, which let some GEMM2 items start
+ * before GEMM1 ends, measured slower at prefill size.) */
 enum mlp2_order {
-  MLP2_ORDER_COLUMN_FIRST = 0, /* every row block of column block 0, then column block 1, ... */
-  MLP2_ORDER_ROW_FIRST = 1,    /* every column block of row block 0, then row block 1, ...    */
-  MLP2_ORDER_REVERSED = 2,     /* column-first, last column block first (stress order)         */
-  MLP2_ORDER_SHUFFLED = 3      /* a seeded permutation (stress order)                          */
+  MLP2_ORDER_AUTO = 0,         /* the default: column-first                                     */
+  MLP2_ORDER_COLUMN_FIRST = 1, /* every row block of column block 0, then column block 1, ... */
+  MLP2_ORDER_ROW_FIRST = 2,    /* every column block of row block 0, then row block 1, ...    */
+  MLP2_ORDER_REVERSED = 3,     /* column-first, last column block first (stress order)         */
+  MLP2_ORDER_SHUFFLED = 4      /* a seeded permutation (stress order)                          */
 };
 
 /* Optional tuning for mlp2_plan_ex; a zero field means "choose automatically". */
@@ -85,7 +90,7 @@ typedef struct mlp2_tuning {
   int splitk2;   /* GEMM2 split-K factor (>= 1)                                           */
   int grid;      /* persistent grid of every launch (no more work-groups than fit the
                     device at once)                                                      */
-  int order;     /* enum mlp2_order                                                       */
+  int order;     /* enum mlp2_order (0 = MLP2_ORDER_AUTO)                                 */
   int stages;    /* LDS ring depth of the tile mainloop (2, 3 or 4)                       */
   int reserved[6];
 } mlp2_tuning_t;

@@ -32,7 +32,7 @@ struct mlp2_plan_s {
   int grid = 0, grid1 = 0, grid2 = 0, occupancy = 0, num_cus = 0;
   int grid_override = 0;
   int max_grid = 0;  // work-groups of every kernel of the plan that fit the device at once
-  int order = MLP2_ORDER_COLUMN_FIRST;
+  int order = MLP2_ORDER_AUTO;
   uint32_t spin_limit = 1u << 20;
   int drop_signal = -1;
   uint64_t* trace = nullptr;  // caller-owned timing buffer (trace builds)
@@ -48,6 +48,7 @@ struct mlp2_plan_s {
   uint32_t* ready = nullptr;
   uint32_t* ctrl = nullptr;
   uint32_t* order1 = nullptr;
+  uint32_t* orderp = nullptr;
   size_t counters_off = 0, counters_bytes = 0;
 };
 
@@ -79,25 +80,26 @@ int choose_split(int64_t K, int tiles, int want, int min_k, int* kc) {
   return ceil_div(K, k);
 }
 
-// GEMM1 item order of the pipelined launch.  Items are id = tile * S1 + s with
-// tile = nb * Mb + mb.  Every policy orders *tiles* and keeps the S1 parts of
-// a tile adjacent: split-K parts wait for their siblings, and adjacency (with
-// a grid of at least S1 work-groups) is what keeps the launch deadlock-free.
+// GEMM1 item order (the rank order of the GEMM1 kernel, and of the GEMM1
+// items within the pipelined kernel).  Items are id = tile * S1 + s with
+// tile = nb * Mb + mb; every policy orders tiles and keeps the S1 parts of a
+// tile adjacent.
 void build_order(mlp2_plan_s* p, std::vector<uint32_t>& out) {
   std::vector<uint32_t> tiles;
   tiles.reserve((size_t)p->Mb * p->Nb1);
+  auto tile = [&](int nb, int mb) { tiles.push_back((uint32_t)(nb * p->Mb + mb)); };
   switch (p->order) {
     case MLP2_ORDER_ROW_FIRST:
       for (int mb = 0; mb < p->Mb; ++mb)
-        for (int nb = 0; nb < p->Nb1; ++nb) tiles.push_back((uint32_t)(nb * p->Mb + mb));
+        for (int nb = 0; nb < p->Nb1; ++nb) tile(nb, mb);
       break;
     case MLP2_ORDER_REVERSED:
       for (int nb = p->Nb1 - 1; nb >= 0; --nb)
-        for (int mb = 0; mb < p->Mb; ++mb) tiles.push_back((uint32_t)(nb * p->Mb + mb));
+        for (int mb = 0; mb < p->Mb; ++mb) tile(nb, mb);
       break;
-    default:  // column-block-first (also the base of the shuffled order)
+    default:  // MLP2_ORDER_AUTO, MLP2_ORDER_COLUMN_FIRST, and the base of the shuffled order
       for (int nb = 0; nb < p->Nb1; ++nb)
-        for (int mb = 0; mb < p->Mb; ++mb) tiles.push_back((uint32_t)(nb * p->Mb + mb));
+        for (int mb = 0; mb < p->Mb; ++mb) tile(nb, mb);
       if (p->order == MLP2_ORDER_SHUFFLED) {
         std::mt19937 rng(12345u);
         std::shuffle(tiles.begin(), tiles.end(), rng);
@@ -108,6 +110,41 @@ void build_order(mlp2_plan_s* p, std::vector<uint32_t>& out) {
   out.reserve(tiles.size() * p->S1);
   for (uint32_t t : tiles)
     for (int s = 0; s < p->S1; ++s) out.push_back(t * (uint32_t)p->S1 + (uint32_t)s);
+}
+
+// Rank table of the pipelined kernel: the GEMM1 items keep their order; GEMM2
+// item q = tile * S2 + s goes right after rank h(q) + lag, where h(q) is the
+// highest GEMM1 rank among the tiles its K range reads.  Every GEMM2 item thus
+// ranks above every GEMM1 item it waits for (what the deadlock argument
+// needs), and is claimed about `lag` claims after its last producer.
+void build_merged(const mlp2_plan_s* p, const std::vector<uint32_t>& order1, int lag, std::vector<uint32_t>& out) {
+  std::vector<int64_t> last_rank((size_t)p->Mb * p->Nb1, -1);
+  for (size_t r = 0; r < order1.size(); ++r) {
+    const uint32_t t = order1[r] / (uint32_t)p->S1;
+    last_rank[t] = std::max<int64_t>(last_rank[t], (int64_t)r);
+  }
+  struct Key {
+    int64_t key;
+    int kind;  // 0 = GEMM1, 1 = GEMM2
+    uint32_t id;
+  };
+  std::vector<Key> keys;
+  keys.reserve(order1.size() + (size_t)p->items2);
+  for (size_t r = 0; r < order1.size(); ++r) keys.push_back({(int64_t)r, 0, order1[r]});
+  for (int q = 0; q < p->items2; ++q) {
+    const int tile = q / p->S2, s = q % p->S2;
+    const int mb = tile % p->Mb;
+    const int64_t kbeg = (int64_t)s * p->kc2, kend = std::min<int64_t>(p->F, kbeg + p->kc2);
+    int64_t h = -1;
+    for (int64_t kb = kbeg / p->kc.bn1; kb <= (kend - 1) / p->kc.bn1; ++kb) h = std::max(h, last_rank[kb * p->Mb + mb]);
+    keys.push_back({h + lag, 1, (uint32_t)q});
+  }
+  std::stable_sort(keys.begin(), keys.end(), [](const Key& a, const Key& b) {
+    return a.key != b.key ? a.key < b.key : a.kind < b.kind;
+  });
+  out.clear();
+  out.reserve(keys.size());
+  for (const Key& k : keys) out.push_back(k.kind ? (0x80000000u | k.id) : k.id);
 }
 
 bool is_gfx950(int dev) {
@@ -122,9 +159,11 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 }
 
 int upload_order(mlp2_plan_s* p) {
-  std::vector<uint32_t> ord;
+  std::vector<uint32_t> ord, merged;
   build_order(p, ord);
-  if (hipMemcpy(p->order1, ord.data(), ord.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess)
+  build_merged(p, ord, p->grid_override ? p->grid_override : p->grid, merged);
+  if (hipMemcpy(p->order1, ord.data(), ord.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(p->orderp, merged.data(), merged.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess)
     return MLP2_ERR_HIP;
   return MLP2_OK;
 }
@@ -267,6 +306,8 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   const size_t cnt_end = off;
   const size_t ord_off = off;
   off = align_up(off + (size_t)p->items1 * 4, 256);
+  const size_t ordp_off = off;
+  off = align_up(off + ((size_t)p->items1 + p->items2) * 4, 256);
   p->ws_bytes = off;
   if (hipMalloc(&p->ws, p->ws_bytes) != hipSuccess) {
     delete p;
@@ -282,6 +323,7 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   p->ready = (uint32_t*)(b + r_off);
   p->ctrl = (uint32_t*)(b + ctrl_off);
   p->order1 = (uint32_t*)(b + ord_off);
+  p->orderp = (uint32_t*)(b + ordp_off);
   p->counters_off = cnt_off;
   p->counters_bytes = cnt_end - cnt_off;
   if (hipMemset(b + cnt_off, 0, cnt_end - cnt_off) != hipSuccess || hipMemset(p->Z, 0, (size_t)Mpad * F * 2) != hipSuccess ||
@@ -321,6 +363,7 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   a.ready = p->ready;
   a.ctrl = p->ctrl;
   a.order1 = p->order1;
+  a.orderp = p->orderp;
   a.M = (int)p->M;
   a.H = (int)p->H;
   a.F = (int)p->F;
@@ -425,7 +468,7 @@ int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
       p->drop_signal = (int)value;
       return MLP2_OK;
     case MLP2_OPT_ORDER:
-      if (value < MLP2_ORDER_COLUMN_FIRST || value > MLP2_ORDER_SHUFFLED) return fail(MLP2_ERR_INVALID_ARG);
+      if (value < MLP2_ORDER_AUTO || value > MLP2_ORDER_SHUFFLED) return fail(MLP2_ERR_INVALID_ARG);
       p->order = (int)value;
       if (hipDeviceSynchronize() != hipSuccess || upload_order(p) != MLP2_OK) return fail(MLP2_ERR_HIP);
       return MLP2_OK;
@@ -434,6 +477,8 @@ int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
       if (value < 0 || value > p->max_grid)
         return fail(MLP2_ERR_INVALID_ARG);
       p->grid_override = (int)value;
+      // the pipelined rank table places GEMM2 items about one grid after their producers
+      if (hipDeviceSynchronize() != hipSuccess || upload_order(p) != MLP2_OK) return fail(MLP2_ERR_HIP);
       return MLP2_OK;
     default:
       return fail(MLP2_ERR_INVALID_ARG);

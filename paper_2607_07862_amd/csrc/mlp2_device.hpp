@@ -48,7 +48,9 @@ struct Args {
   uint32_t* cnt2;      // [tiles2] split-K arrival counters of GEMM2
   uint32_t* ready;     // [tiles1] ready counters: tile (mb, nb1) at index nb1 * Mb + mb
   uint32_t* ctrl;      // CTRL_* words
-  const uint32_t* order1;  // GEMM1 item order, length items1
+  const uint32_t* order1;  // GEMM1 item per rank of the GEMM1 kernel, length items1
+  const uint32_t* orderp;  // item per rank of the pipelined kernel, length items1 + items2
+                           // (bit 31 set: GEMM2 item; else GEMM1 item id)
   int M, H, F, act;
   int Mb, Nb1, Nb2;        // row blocks; GEMM1 / GEMM2 column blocks
   int S1, S2;              // split-K factors

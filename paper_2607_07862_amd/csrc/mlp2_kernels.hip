@@ -233,10 +233,14 @@ __device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, boo
 // until the kernel's items are exhausted.  Items in rank order:
 //   PHASE_GEMM1:     GEMM1 items in the order table's order
 //   PHASE_GEMM2:     GEMM2 items
-//   PHASE_PIPELINED: both back to back; GEMM2 items wait per K-slice.
+//   PHASE_PIPELINED: the merged table: GEMM1 items in the same order, each
+//                    GEMM2 item placed after every GEMM1 item it reads (plus
+//                    a lag of about one grid), so that GEMM2 work starts while
+//                    later GEMM1 items still run; GEMM2 items wait per K-slice.
 // Claim list l holds the ranks congruent to l modulo `lists` and hands them
 // out in increasing order.  The only waits are a GEMM2 item's waits for GEMM1
-// tiles, which have lower ranks (split-K parts never wait for each other).  A
+// tiles, which have lower ranks in every table (split-K parts never wait for
+// each other).  A
 // work-group claims its next item only after the last wait of its current
 // item.  Take the lowest-ranked unfinished item u: every lower rank is
 // finished, so if u is claimed its waits end and it finishes; if it is not,
@@ -282,10 +286,17 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, PHASE>())) void k
     if (p >= total) break;
     TraceAcc tr;
     const uint64_t t_start = trace_now();
-    if (p < g1)
+    if constexpr (PHASE == PHASE_PIPELINED) {
+      const uint32_t e = uniform(a.orderp[p]);
+      if (e & 0x80000000u)
+        gemm2_item<T2, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, &s_item, tr);
+      else
+        gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, &s_item, tr);
+    } else if constexpr (PHASE == PHASE_GEMM1) {
       gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_slot, &s_item, tr);
-    else
-      gemm2_item<T2, PHASE == PHASE_PIPELINED>(a, p - g1, epoch, lds, &s_slot, &s_item, tr);
+    } else {
+      gemm2_item<T2, false>(a, p, epoch, lds, &s_slot, &s_item, tr);
+    }
     if constexpr (kTrace) tr_record(a, PHASE == PHASE_GEMM2 ? 1 : 0, n_items++, p, t_start, tr);
   }
   finish_kernel(a, epoch, PHASE != PHASE_GEMM1);

@@ -22,7 +22,8 @@ from _gpu import assert_bit_equal, assert_matches_oracle, bits_of, device_inputs
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("order", [B.ORDER_ROW_FIRST, B.ORDER_REVERSED, B.ORDER_SHUFFLED, B.ORDER_COLUMN_FIRST])
+@pytest.mark.parametrize("order", [B.ORDER_AUTO, B.ORDER_ROW_FIRST, B.ORDER_REVERSED, B.ORDER_SHUFFLED,
+                                   B.ORDER_COLUMN_FIRST])
 @pytest.mark.parametrize("grid", [1, 2, 3, 4, 17, 0])
 def test_orders_and_grids_match_sequential_bits(lib, order, grid):
     M, H, F, act = 160, 256, 768, 1
@@ -125,7 +126,7 @@ def test_run_argument_errors(lib):
     plan.close()
 
 
-@pytest.mark.parametrize("order", [B.ORDER_REVERSED, B.ORDER_SHUFFLED, B.ORDER_COLUMN_FIRST])
+@pytest.mark.parametrize("order", [B.ORDER_REVERSED, B.ORDER_SHUFFLED, B.ORDER_COLUMN_FIRST, B.ORDER_AUTO])
 def test_consecutive_slice_waits_stay_in_step(lib, order):
     """bn1 = 64 makes every 64-deep stage of GEMM2 a new column block of Z, so
     the pipeline prologue waits several times in a row; with a reversed or

@@ -18,20 +18,26 @@ import random
 import pytest
 
 
-def column_first_tiles(Mb, Nb1, order, seed=12345):
+def column_first_tiles(Mb, Nb1, order, seed=12345, S2=1):
+    if order == "halves":  # column-first over each half of the row blocks (a stress order)
+        per = -(-Mb // 2)
+        return [nb * Mb + mb for g0 in range(0, Mb, per) for nb in range(Nb1) for mb in range(g0, min(Mb, g0 + per))]
     if order == "row":
         return [nb * Mb + mb for mb in range(Mb) for nb in range(Nb1)]
     if order == "reversed":
         return [nb * Mb + mb for nb in reversed(range(Nb1)) for mb in range(Mb)]
-    tiles = [nb * Mb + mb for nb in range(Nb1) for mb in range(Mb)]
+    tiles = [nb * Mb + mb for nb in range(Nb1) for mb in range(Mb)]  # column-first (and "auto")
     if order == "shuffled":
         random.Random(seed).shuffle(tiles)
     return tiles
 
 
-def items(Mb, Nb1, Nb2, S1, S2, order, consumers_first=False):
-    """Rank-ordered items: (kind, tile, s, needs) with needs = GEMM1 tiles a GEMM2 part reads."""
-    g1 = [("g1", t, s, []) for t in column_first_tiles(Mb, Nb1, order) for s in range(S1)]
+def items(Mb, Nb1, Nb2, S1, S2, order, consumers_first=False, merged_lag=None):
+    """Rank-ordered items: (kind, tile, s, needs) with needs = GEMM1 tiles a GEMM2 part reads.
+
+    merged_lag: place each GEMM2 item right after rank (last producer rank + lag), as the
+    pipelined kernel's merged table does, instead of after every GEMM1 item."""
+    g1 = [("g1", t, s, []) for t in column_first_tiles(Mb, Nb1, order, S2=S2) for s in range(S1)]
     per = -(-Nb1 // S2)
     g2 = []
     for tile in range(Mb * Nb2):
@@ -39,6 +45,14 @@ def items(Mb, Nb1, Nb2, S1, S2, order, consumers_first=False):
         for s in range(S2):
             kbs = range(s * per, min(Nb1, (s + 1) * per))
             g2.append(("g2", tile, s, [kb * Mb + mb for kb in kbs]))
+    if merged_lag is not None:
+        last = {}
+        for r, it in enumerate(g1):
+            last[it[1]] = r
+        keyed = [(r, 0, it) for r, it in enumerate(g1)]
+        keyed += [(max((last[n] for n in it[3]), default=-1) + merged_lag, 1, it) for it in g2]
+        keyed.sort(key=lambda k: (k[0], k[1]))
+        return [k[2] for k in keyed]
     return g2 + g1 if consumers_first else g1 + g2
 
 
@@ -110,29 +124,25 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("order", ["column", "row", "reversed", "shuffled"])
+@pytest.mark.parametrize("order", ["auto", "row", "reversed", "shuffled", "halves"])
 @pytest.mark.parametrize("Mb,Nb1,Nb2,S1,S2", CASES)
 def test_pipelined_schedule_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
     lst = items(Mb, Nb1, Nb2, S1, S2, order)
     for grid in (1, 2, 3, 5, 7, 8, 9, 16, 17, 40):
-        for seed in range(6):
+        for seed in range(4):
             assert simulate(lst, S1, S2, grid, seed), (order, grid, seed)
 
 
-def test_consumers_ranked_before_producers_can_deadlock():
-    """Why GEMM2 items follow every GEMM1 item in rank order."""
-    Mb, Nb1, Nb2, S1, S2 = 1, 4, 4, 1, 1
-    bad = items(Mb, Nb1, Nb2, S1, S2, "column", consumers_first=True)
-    assert not all(simulate(bad, S1, S2, 3, seed) for seed in range(6))
-    good = items(Mb, Nb1, Nb2, S1, S2, "column")
-    assert all(simulate(good, S1, S2, 3, seed) for seed in range(6))
-
-
-def test_lists_cover_every_rank_once():
-    for grid in (1, 3, 8, 13, 64):
-        L = claim_lists(grid)
-        seen = []
-        for lst in range(L):
-            seen += [lst + t * L for t in range(100) if lst + t * L < 100]
-        assert sorted(seen) == list(range(100))
-        assert L <= grid
+@pytest.mark.parametrize("order", ["auto", "row", "shuffled", "halves"])
+@pytest.mark.parametrize("Mb,Nb1,Nb2,S1,S2", CASES)
+def test_merged_rank_table_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
+    for lag in (0, 1, 5, 40):
+        lst = items(Mb, Nb1, Nb2, S1, S2, order, merged_lag=lag)
+        rank = {id(it): r for r, it in enumerate(lst)}
+        g1_rank = {(it[1]): r for r, it in enumerate(lst) if it[0] == "g1"}
+        for it in lst:  # every consumer ranks above each producer tile it reads
+            if it[0] == "g2":
+                assert all(g1_rank[n] < rank[id(it)] for n in it[3])
+        for grid in (1, 2, 3, 8, 9, 17):
+            for seed in range(3):
+                assert simulate(lst, S1, S2, grid, seed), (order, lag, grid, seed)
