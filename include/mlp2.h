@@ -175,9 +175,11 @@ int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
  * kernel of the sequential mode) and work-group g of that launch, the block
  * at uint64 offset (s * G + g) * (1 + 8 * records_per_group) holds the
  * item count, then one record per item of 8 uint64: item rank, start,
- * mainloop end, split-K arrival released, split-K siblings arrived (0 and 0
- * for an item without split-K), end (times on the 100 MHz device real-time
- * counter), ticks waiting for the tile loads of the work-group's own ring,
+ * mainloop end, two epilogue marks, end (times on the 100 MHz device
+ * real-time counter; the marks are: for a GEMM1 tile that signals, its Z
+ * stores complete and its ready counter released; for a split-K part that
+ * does not complete its tile, its partial stored and its arrival counted;
+ * 0 and 0 otherwise), ticks waiting for the tile loads of the work-group's own ring,
  * ticks waiting for ready counters and split-K siblings.  Items beyond records_per_group are counted, not stored.
  * G is the largest of the plan's grids (grid_pipelined, grid_gemm1,
  * grid_gemm2 of mlp2_plan_info); the buffer must hold

@@ -18,8 +18,13 @@ LIB_PATH = os.path.join(PKG, LIB_NAME)
 SOURCES = ["mlp2_kernels.hip", "mlp2_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-# Packed fp32 VALU ops are turned off for all device code.
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Packed fp32 VALU ops are turned off for all device code.  The atomic
+# optimizer is off: every atomic of the kernels is issued by a single lane,
+# and the optimizer's rewrite reads the result back at once, which stalls the
+# wave on the atomic's round trip (and on every load issued before it) where
+# the kernels mean to use the result only much later.
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
 
 
 def build(verbose: bool = False, trace: bool = False) -> str:

@@ -49,6 +49,7 @@ struct mlp2_plan_s {
   uint32_t* ctrl = nullptr;
   uint32_t* order1 = nullptr;
   uint32_t* orderp = nullptr;
+  int64_t lead1 = 0;  // leading ranks of the pipelined table that are GEMM1 items (they never wait)
   size_t counters_off = 0, counters_bytes = 0;
 };
 
@@ -162,6 +163,8 @@ int upload_order(mlp2_plan_s* p) {
   std::vector<uint32_t> ord, merged;
   build_order(p, ord);
   build_merged(p, ord, p->grid_override ? p->grid_override : p->grid, merged);
+  p->lead1 = 0;
+  while (p->lead1 < (int64_t)merged.size() && !(merged[p->lead1] & 0x80000000u)) ++p->lead1;
   if (hipMemcpy(p->order1, ord.data(), ord.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(p->orderp, merged.data(), merged.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess)
     return MLP2_ERR_HIP;
@@ -295,12 +298,13 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   const size_t p2_off = off;
   if (p->S2 > 1) off = align_up(off + (size_t)p->items2 * bm * bn2 * 4, 256);
   const size_t cnt_off = off;
+  const size_t line = mlp2::kLine * 4;  // one counter per 128-byte line
   const size_t c1_off = off;
-  off = align_up(off + (size_t)tiles1 * 4, 256);
+  off = align_up(off + (size_t)tiles1 * line, 256);
   const size_t c2_off = off;
-  off = align_up(off + (size_t)tiles2 * 4, 256);
+  off = align_up(off + (size_t)tiles2 * line, 256);
   const size_t r_off = off;
-  off = align_up(off + (size_t)tiles1 * 4, 256);
+  off = align_up(off + (size_t)tiles1 * line, 256);
   const size_t ctrl_off = off;
   off = align_up(off + mlp2::CTRL_WORDS * 4, 256);
   const size_t cnt_end = off;
@@ -389,13 +393,24 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   const int gridp = go ? go : p->grid;
   a.trace_groups = std::max(std::max(grids[0], grids[1]), gridp);
   hipError_t err;
+  // First items without tickets (Args::first_static) save a launch the round
+  // trip of its first claim, which matters for a launch of one round of
+  // items with one work-group per CU (the weight-streaming shapes); they are
+  // used only there, and only when those first items never wait.  (With two
+  // work-groups per CU, measured at prefill size, claiming every item was
+  // faster.)
+  auto one_round = [&](int64_t items, int grid) { return items <= grid && grid <= p->num_cus; };
   if (mode == MLP2_MODE_SEQUENTIAL) {
     a.lists = claim_lists(grids[0]);
+    a.first_static = one_round(p->items1, grids[0]);  // GEMM1 items never wait
     Args a2 = a;
     a2.lists = claim_lists(grids[1]);
+    a2.first_static = one_round(p->items2, grids[1]);  // nor do GEMM2 items of this mode
     err = mlp2::launch_sequential(p->kc, a, a2, grids, s);
   } else {
     a.lists = claim_lists(gridp);
+    const int64_t total = (int64_t)p->items1 + p->items2;
+    a.first_static = one_round(total, gridp) && total <= p->lead1;
     err = mlp2::launch_pipelined(p->kc, a, gridp, s);
   }
   if (err != hipSuccess) return fail(MLP2_ERR_HIP);

@@ -25,14 +25,23 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
 constexpr int kThreads = 256;  // four 64-wide waves per work-group
 constexpr int kBK = 64;        // K depth of one LDS stage
 
-// Control words of a plan (device memory, zero at plan creation).
+// Words per 128-byte line.  Every counter that work-groups update with device-
+// scope atomics sits on a line of its own: such atomics are performed at the
+// memory side of the device, one at a time per line, so counters sharing a
+// line would queue behind each other's traffic.
+constexpr int kLine = 32;
+
+// Control words of a plan (device memory, zero at plan creation), one per line.
 enum {
-  CTRL_EPOCH = 0,   // runs completed; read at kernel start, bumped by the run's last work-group
-  CTRL_DONE = 2,    // work-groups of the current kernel that have finished
-  CTRL_ERROR = 3,   // nonzero once a bounded flag wait gave up
-  CTRL_TICKET = 8,  // CTRL_TICKET + l: next ticket of claim list l (up to 8 lists)
-  CTRL_WORDS = 16
+  CTRL_EPOCH = 0,                  // runs completed; read at kernel start, bumped by the run's last work-group
+  CTRL_ERROR = 1 * kLine,          // nonzero once a bounded flag wait gave up
+  CTRL_DONE_ALL = 2 * kLine,       // claim lists of the current kernel whose work-groups have all finished
+  CTRL_TICKET = 3 * kLine,         // CTRL_TICKET + l * kLine: next ticket of claim list l (up to 8 lists)
+  CTRL_DONE = 11 * kLine,          // CTRL_DONE + l * kLine: finished work-groups of claim list l
+  CTRL_WORDS = 19 * kLine
 };
+__device__ __forceinline__ int ctrl_ticket(int l) { return CTRL_TICKET + l * kLine; }
+__device__ __forceinline__ int ctrl_done(int l) { return CTRL_DONE + l * kLine; }
 
 enum { ACT_IDENTITY = 0, ACT_GELU_TANH = 1, ACT_SWIGLU = 2 };
 
@@ -44,9 +53,9 @@ struct Args {
   uint16_t* Z;         // [Mpad, F]
   float* part1;        // GEMM1 split-K partials (fragment-native), or null
   float* part2;        // GEMM2 split-K partials, or null
-  uint32_t* cnt1;      // [tiles1] split-K arrival counters of GEMM1
-  uint32_t* cnt2;      // [tiles2] split-K arrival counters of GEMM2
-  uint32_t* ready;     // [tiles1] ready counters: tile (mb, nb1) at index nb1 * Mb + mb
+  uint32_t* cnt1;      // split-K arrival counters of GEMM1: tile t at word t * kLine
+  uint32_t* cnt2;      // split-K arrival counters of GEMM2: tile t at word t * kLine
+  uint32_t* ready;     // ready counters: tile (mb, nb1) at word (nb1 * Mb + mb) * kLine
   uint32_t* ctrl;      // CTRL_* words
   const uint32_t* order1;  // GEMM1 item per rank of the GEMM1 kernel, length items1
   const uint32_t* orderp;  // item per rank of the pipelined kernel, length items1 + items2
@@ -63,6 +72,8 @@ struct Args {
   int trace_cap;           // records per work-group
   int trace_groups;        // work-groups per trace section (the largest grid of the plan)
   int lists;               // claim lists of the launch (1 or 8; work-group g claims from list g % lists)
+  int first_static;        // nonzero: work-group g takes rank g as its first item without a ticket
+                           // (set only when the first `grid` ranks are items that never wait)
 };
 
 // ------------------------------------------------------------------ optional timing trace
@@ -197,10 +208,6 @@ __device__ __forceinline__ void wait_vm() {
 }
 
 // ------------------------------------------------------------------ mainloop
-
-struct NoWait {
-  __device__ __forceinline__ void operator()(int) {}
-};
 
 // acc[b][tn][tm] = sum over k in [kbeg, kend) of W_b[k][n] * A[m][k] for the
 // tile at (m0, n0).  A rows past `mlast` are clamped to `mlast` (their results
@@ -483,10 +490,11 @@ __device__ __forceinline__ void release_add(uint32_t* cnt) {
 // work-group acquire for the other waves).
 template <class T, int NB>
 __device__ __forceinline__ bool arrive_split(float* part, uint32_t* cnt, long tile, int S, int s, uint32_t target,
-                                             const f32x4 (&acc)[NB][T::TN][T::TM], int* s_slot) {
+                                             const f32x4 (&acc)[NB][T::TN][T::TM], int* s_slot, TraceAcc& tr) {
   store_partial<T, NB>(part, tile, S, s, acc);
   wait_all_mem();
   __syncthreads();
+  if constexpr (kTrace) tr.t_rel = trace_now();
   if (threadIdx.x == 0) {
     const uint32_t old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     *s_slot = old == target - 1u;
@@ -495,8 +503,55 @@ __device__ __forceinline__ bool arrive_split(float* part, uint32_t* cnt, long ti
   const bool last = uniform(*s_slot) != 0;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
   __syncthreads();  // *s_slot may be rewritten
+  if constexpr (kTrace) tr.t_wait = trace_now();
   return last;
 }
+
+// ------------------------------------------------------------------ claiming items
+
+// The next item of a persistent work-group.  Claim list l = blockIdx % lists
+// hands out the ranks l, l + lists, l + 2 lists, ... in increasing order: the
+// first `skip` of them without a ticket (the work-groups' first items), the
+// rest through the list's ticket word.  Taking a ticket is a device-scope
+// atomic whose result comes back from the memory side after a long round
+// trip, so `issue` sends it as early as the protocol allows (thread 0 keeps
+// the ticket in a register while the item runs) and `park` writes the rank
+// to LDS at the end of the item, where the next iteration reads it after a
+// barrier.  Every item calls `issue` exactly once, then `park`.
+struct Claim {
+  uint32_t* ticket;
+  int base, stride, skip;
+  uint32_t t;
+  __device__ __forceinline__ void issue() {
+    if (threadIdx.x == 0) t = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __device__ __forceinline__ void park(int* s_next) const {
+    if (threadIdx.x == 0) *s_next = base + stride * ((int)t + skip);
+  }
+};
+
+// The mainloop hook of every item: the item's own wait for the stage at K
+// offset k (if any), then, when the loads of the item's last stage are
+// issued, the ticket for the work-group's next item.  The last stage's wait
+// is the item's last wait, so the claim never precedes a wait of its item.
+// The atomic's round trip overlaps the last stages and the epilogue, while
+// the choice of the next item is still made late: a work-group that
+// committed to its next item a whole item ahead would keep it from a
+// work-group that frees up sooner, and lengthen the launch's tail.
+struct NoWait {
+  __device__ __forceinline__ void operator()(int) {}
+};
+
+template <class Wait>
+struct ClaimAtLastStage {
+  Wait& wait;
+  Claim* next;
+  int k_last;  // K offset of the item's last stage
+  __device__ __forceinline__ void operator()(int k) {
+    wait(k);
+    if (k == k_last) next->issue();
+  }
+};
 
 // ------------------------------------------------------------------ ready flags
 
@@ -534,7 +589,7 @@ struct ReadyWait {
     if (uniform((int)(threadIdx.x >> 6)) == 0) {  // wave 0, as a scalar branch
       const int lane = threadIdx.x & 63;
       const int j = kb + lane;
-      const uint32_t* f = ready + (long)(j <= kb_last ? j : kb_last) * Mb + mb;
+      const uint32_t* f = ready + ((long)(j <= kb_last ? j : kb_last) * Mb + mb) * kLine;
       int hi = -1;
       if (uniform(ld_relaxed(err)) == 0u) {
         // scalar loop: every exit condition is wave-uniform

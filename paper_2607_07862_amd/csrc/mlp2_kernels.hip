@@ -11,12 +11,13 @@
 // GEMM1 tile that produced it has signalled (Sec. III-A of the paper: the
 // consumer runs once every producer tile it reads is complete).
 //
-// Scheduling of the pipelined launch: a global ticket hands out the GEMM1
-// items first, in the order of the plan's order table (column-block-first by
-// default, Sec. III-A.5: the first kernel may follow a predefined order), then
-// the GEMM2 items.  A GEMM2 item only ever waits for GEMM1 items that were
-// claimed before it by running work-groups that never wait, so the launch
-// cannot deadlock whatever its grid size or residency.
+// Scheduling of the pipelined launch: claim lists hand out the items of one
+// rank table, the GEMM1 items in the order of the plan's order table
+// (column-block-first by default, Sec. III-A.5: the first kernel may follow a
+// predefined order) and each GEMM2 item after the GEMM1 items it reads.  A
+// GEMM2 item only ever waits for lower-ranked GEMM1 items, which never wait,
+// so the launch cannot deadlock whatever its grid size or residency (the
+// argument is given with the kernels below).
 #include "mlp2_device.hpp"
 #include "mlp2_launch.h"
 
@@ -47,20 +48,16 @@ __device__ __forceinline__ void store_y(const Args& a, int row, int col, const f
   if (row < a.M) *reinterpret_cast<u32x4*>(a.Y + (long)row * a.H + col) = pack_bf16x8(v);
 }
 
-// Claims the next item early: thread 0 takes a ticket t of its claim list
-// l = blockIdx.x % lists and parks the item rank l + t * lists in *s_next; it
-// is read after the item's closing barrier.  Called once per item, after the
-// item's last wait, so that an item never holds a claim it might itself be
-// waiting for.  Work-groups are placed on the XCDs round-robin by index, so
-// with 8 lists every XCD takes every 8th item of the rank order: the same
-// number of weight-streaming items per XCD (and per L2 and fabric link),
-// while the chip as a whole still works through the ranks in order.
-__device__ __forceinline__ void claim_next(const Args& a, int* s_next) {
-  if (threadIdx.x == 0) {
-    const int l = (int)(blockIdx.x % (unsigned)a.lists);
-    const uint32_t t = __hip_atomic_fetch_add(a.ctrl + CTRL_TICKET + l, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *s_next = l + (int)t * a.lists;
-  }
+// Claim lists.  Work-groups are placed on the XCDs round-robin by index, so
+// with 8 lists (work-group g on list g % 8) every XCD takes every 8th item of
+// the rank order: the same number of weight-streaming items per XCD (and per
+// L2 and fabric link), while the chip as a whole still works through the
+// ranks in order.  When the launch's first `grid` ranks are items that never
+// wait, work-group g takes rank g as its first item without a ticket.
+__device__ __forceinline__ Claim make_claim(const Args& a) {
+  const int l = (int)(blockIdx.x % (unsigned)a.lists);
+  const int skip = a.first_static ? (int)((gridDim.x - 1u - (unsigned)l) / (unsigned)a.lists) + 1 : 0;
+  return Claim{a.ctrl + ctrl_ticket(l), l, a.lists, skip, 0u};
 }
 
 // ------------------------------------------------------------------ trace records (MLP2_TRACE builds)
@@ -69,8 +66,10 @@ __device__ __forceinline__ void claim_next(const Args& a, int* s_next) {
 // kernel, 1 = GEMM2 kernel of the sequential mode; trace_groups work-groups
 // per section) and work-group, one word
 // with the item count, then trace_cap records of kTraceWords words: rank,
-// start, mainloop end, split-K arrival released, siblings arrived (both 0
-// without split-K), end, ring-wait ticks, flag-wait ticks.  Records past
+// start, mainloop end, two epilogue marks (a signalling GEMM1 tile: Z stores
+// complete, ready counter released; a split-K part that leaves the tile to a
+// sibling: partial stored, arrival counted; else 0 and 0), end, ring-wait
+// ticks, flag-wait ticks.  Records past
 // trace_cap are counted, not stored.  Written by thread 0 with plain stores.
 __device__ __forceinline__ void tr_mark_mainloop(TraceAcc& tr) { tr.t_main = trace_now(); }
 
@@ -122,7 +121,7 @@ __device__ __forceinline__ void reduce_epilogue(const float* part, long tile, in
 // GEMM1 item id = tile * S1 + s, tile = nb * Mb + mb.
 template <class T, int NB>
 __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t epoch, char* lds, int* s_slot,
-                                           int* s_next, TraceAcc& tr) {
+                                           Claim& next, int* s_next, TraceAcc& tr) {
   const int id = uniform(id_in);
   const int tile = id / a.S1, s = id - tile * a.S1;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
@@ -134,12 +133,13 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
   const uint16_t* Bp[NB];
   Bp[0] = a.W1;
   if constexpr (NB == 2) Bp[1] = a.W1 + (long)a.H * a.F;
-  NoWait nowait;
-  mainloop<T, NB>(a.X, a.H, m0, a.M - 1, Bp, a.F, n0, kbeg, kend, acc, lds, nowait, tr);
+  NoWait nowait;  // a GEMM1 item never waits
+  ClaimAtLastStage<NoWait> hook{nowait, &next, kend - kBK};
+  mainloop<T, NB>(a.X, a.H, m0, a.M - 1, Bp, a.F, n0, kbeg, kend, acc, lds, hook, tr);
   if constexpr (kTrace) tr_mark_mainloop(tr);
 
   if (a.S1 == 1) {
-    claim_next(a, s_next);
+    next.park(s_next);
     FragPos<T> fp(m0, n0);
 #pragma unroll
     for (int tm = 0; tm < T::TM; ++tm)
@@ -151,16 +151,21 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
         store_z<NB>(a, fp.row0 + 16 * tm, fp.col0 + 32 * tp, v);
       }
   } else {
-    const bool last = arrive_split<T, NB>(a.part1, a.cnt1 + tile, tile, a.S1, s, (epoch + 1u) * (uint32_t)a.S1, acc, s_slot);
-    if constexpr (kTrace) tr.t_rel = tr.t_wait = trace_now();
-    claim_next(a, s_next);
+    const bool last = arrive_split<T, NB>(a.part1, a.cnt1 + (long)tile * kLine, tile, a.S1, s,
+                                          (epoch + 1u) * (uint32_t)a.S1, acc, s_slot, tr);
+    next.park(s_next);
     if (!last) return;
     reduce_epilogue<T, NB>(a.part1, tile, a.S1, [&](const Unit<T>& u, int lane, const float (&v)[NB][8]) {
       store_z<NB>(a, u.row(m0, lane), u.col(n0, lane), v);
     });
   }
   // Producer signal (one per tile and run): the tile's Z rows are released, ready[tile] += 1.
-  if (tile != a.drop_signal) signal_ready(a.ready + tile);
+  if constexpr (kTrace) {
+    wait_all_mem();
+    tr.t_rel = trace_now();
+  }
+  if (tile != a.drop_signal) signal_ready(a.ready + (long)tile * kLine);
+  if constexpr (kTrace) tr.t_wait = trace_now();
 }
 
 // GEMM2 item p = tile * S2 + s (the parts of a tile are adjacent tickets,
@@ -168,7 +173,7 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
 // only after its GEMM1 tile has signalled.
 template <class T, bool WAIT>
 __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epoch, char* lds, int* s_slot,
-                                           int* s_next, TraceAcc& tr) {
+                                           Claim& next, int* s_next, TraceAcc& tr) {
   const int p = uniform(p_in);
   const int tile = p / a.S2, s = p - (p / a.S2) * a.S2;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
@@ -182,15 +187,17 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
   if constexpr (WAIT) {
     ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1, epoch + 1u, a.spin_limit, s_slot,
                 -1, &tr};
-    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, w, tr);
+    ClaimAtLastStage<ReadyWait> hook{w, &next, kend - kBK};
+    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   } else {
     NoWait nowait;
-    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, nowait, tr);
+    ClaimAtLastStage<NoWait> hook{nowait, &next, kend - kBK};
+    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   }
   if constexpr (kTrace) tr_mark_mainloop(tr);
 
   if (a.S2 == 1) {
-    claim_next(a, s_next);
+    next.park(s_next);
     FragPos<T> fp(m0, n0);
 #pragma unroll
     for (int tm = 0; tm < T::TM; ++tm)
@@ -201,9 +208,9 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
         store_y(a, fp.row0 + 16 * tm, fp.col0 + 32 * tp, v);
       }
   } else {
-    const bool last = arrive_split<T, 1>(a.part2, a.cnt2 + tile, tile, a.S2, s, (epoch + 1u) * (uint32_t)a.S2, acc, s_slot);
-    if constexpr (kTrace) tr.t_rel = tr.t_wait = trace_now();
-    claim_next(a, s_next);
+    const bool last = arrive_split<T, 1>(a.part2, a.cnt2 + (long)tile * kLine, tile, a.S2, s,
+                                         (epoch + 1u) * (uint32_t)a.S2, acc, s_slot, tr);
+    next.park(s_next);
     if (!last) return;
     reduce_epilogue<T, 1>(a.part2, tile, a.S2, [&](const Unit<T>& u, int lane, const float (&v)[1][8]) {
       store_y(a, u.row(m0, lane), u.col(n0, lane), v[0]);
@@ -211,26 +218,36 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
   }
 }
 
-// The last work-group of a kernel resets the ticket and the done count; the
-// run's final kernel also advances the epoch (all stream-ordered before the
-// next kernel of the plan).
+// Counter lifetime across kernels and runs.  The last work-group of each
+// claim list to finish resets that list's ticket and done count (no
+// work-group of the list claims again); the last list to finish resets the
+// list count and, at the end of a run, advances the epoch.  Everything is
+// stream-ordered before the plan's next kernel.  Spreading the done counts
+// over the lists keeps the exit atomics, one per work-group, off a single
+// line.
 __device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, bool end_of_run) {
   __syncthreads();
   if (threadIdx.x == 0) {
-    const uint32_t old = __hip_atomic_fetch_add(a.ctrl + CTRL_DONE, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    if (old == gridDim.x - 1) {
-      for (int l = 0; l < a.lists; ++l)
-        __hip_atomic_store(a.ctrl + CTRL_TICKET + l, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(a.ctrl + CTRL_DONE, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (end_of_run) __hip_atomic_store(a.ctrl + CTRL_EPOCH, epoch + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    const int l = (int)(blockIdx.x % (unsigned)a.lists);
+    const uint32_t in_list = (gridDim.x - 1u - (unsigned)l) / (unsigned)a.lists + 1u;
+    const uint32_t old = __hip_atomic_fetch_add(a.ctrl + ctrl_done(l), 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == in_list - 1u) {
+      __hip_atomic_store(a.ctrl + ctrl_ticket(l), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.ctrl + ctrl_done(l), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t lists_done =
+          __hip_atomic_fetch_add(a.ctrl + CTRL_DONE_ALL, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      if (lists_done == (uint32_t)a.lists - 1u) {
+        __hip_atomic_store(a.ctrl + CTRL_DONE_ALL, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (end_of_run) __hip_atomic_store(a.ctrl + CTRL_EPOCH, epoch + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
 }
 
 // ------------------------------------------------------------------ kernels
 //
-// Every kernel is persistent: a work-group claims item ranks (claim_next)
-// until the kernel's items are exhausted.  Items in rank order:
+// Every kernel is persistent: a work-group claims item ranks (Claim) until
+// the kernel's items are exhausted.  Items in rank order:
 //   PHASE_GEMM1:     GEMM1 items in the order table's order
 //   PHASE_GEMM2:     GEMM2 items
 //   PHASE_PIPELINED: the merged table: GEMM1 items in the same order, each
@@ -240,9 +257,10 @@ __device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, boo
 // Claim list l holds the ranks congruent to l modulo `lists` and hands them
 // out in increasing order.  The only waits are a GEMM2 item's waits for GEMM1
 // tiles, which have lower ranks in every table (split-K parts never wait for
-// each other).  A
-// work-group claims its next item only after the last wait of its current
-// item.  Take the lowest-ranked unfinished item u: every lower rank is
+// each other).  A work-group takes the ticket for its next item only after the
+// last wait of its current item.  First items taken without a ticket are items
+// that never wait, so they finish whether or not their work-group is resident
+// yet.  Take the lowest-ranked unfinished item u: every lower rank is
 // finished, so if u is claimed its waits end and it finishes; if it is not,
 // every claimed item of its list ranks below u and is finished, so a
 // work-group of that list is free to claim it.  Hence no launch deadlocks for
@@ -273,31 +291,43 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, PHASE>())) void k
   constexpr int kLds = kernel_lds<T1, NB, T2, PHASE>();
   __shared__ __attribute__((aligned(1024))) char lds[kLds];
   __shared__ int s_item, s_slot;
-  const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
+  // The epoch is needed only by split-K arrivals and ready waits, well after
+  // its load has returned; it stays in a vector register until then.
+  const uint32_t epoch = ld_relaxed(a.ctrl + CTRL_EPOCH);
   const int g1 = PHASE == PHASE_GEMM2 ? 0 : a.items1;
   const int g2 = PHASE == PHASE_GEMM1 ? 0 : a.items2;
   const int total = g1 + g2;
-  claim_next(a, &s_item);
+  int p;
+  if (a.first_static) {
+    p = (int)blockIdx.x;
+  } else {
+    Claim first = make_claim(a);
+    first.issue();
+    first.park(&s_item);
+    __syncthreads();
+    p = uniform(s_item);
+  }
   int n_items = 0;
   for (;;) {
-    __syncthreads();
-    int p = uniform(s_item);
-    __syncthreads();  // s_item is rewritten by the item's claim_next
     if (p >= total) break;
+    __syncthreads();  // every wave has read s_item before the item's claim rewrites it
     TraceAcc tr;
     const uint64_t t_start = trace_now();
+    Claim next = make_claim(a);
     if constexpr (PHASE == PHASE_PIPELINED) {
       const uint32_t e = uniform(a.orderp[p]);
       if (e & 0x80000000u)
-        gemm2_item<T2, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, &s_item, tr);
+        gemm2_item<T2, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr);
       else
-        gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, &s_item, tr);
+        gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
     } else if constexpr (PHASE == PHASE_GEMM1) {
-      gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_slot, &s_item, tr);
+      gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_slot, next, &s_item, tr);
     } else {
-      gemm2_item<T2, false>(a, p, epoch, lds, &s_slot, &s_item, tr);
+      gemm2_item<T2, false>(a, p, epoch, lds, &s_slot, next, &s_item, tr);
     }
     if constexpr (kTrace) tr_record(a, PHASE == PHASE_GEMM2 ? 1 : 0, n_items++, p, t_start, tr);
+    __syncthreads();
+    p = uniform(s_item);
   }
   finish_kernel(a, epoch, PHASE != PHASE_GEMM1);
 }

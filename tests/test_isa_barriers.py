@@ -25,8 +25,9 @@ def asm(tmp_path_factory):
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
     out = tmp_path_factory.mktemp("isa") / "k.s"
-    cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-S", "--cuda-device-only",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    from paper_2607_07862_amd.build import DEVICE_FLAGS  # lint exactly what the library build compiles
+
+    cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-S", "--cuda-device-only", *DEVICE_FLAGS,
            "-I" + os.path.join(ROOT, "include"), SRC, "-o", str(out)]
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     assert r.returncode == 0, r.stdout

@@ -61,8 +61,22 @@ def claim_lists(grid):
     return min(8, max(1, grid))
 
 
-def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000):
-    """Returns True if every item completes."""
+def first_static_allowed(item_list, grid):
+    """The host's rule: work-groups take their first rank without a ticket only
+    when the first `grid` ranks are items that never wait."""
+    return all(item_list[r][0] == "g1" for r in range(min(grid, len(item_list))))
+
+
+def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000, first_static=False, late_start=0):
+    """Returns True if every item completes.
+
+    A work-group takes the ticket for its next item as soon as its current
+    item has no wait left (at the start of a GEMM1 item, after the last wait
+    of a GEMM2 item): the earliest point the kernels allow (they take it a
+    little later, when the item's last stage is loaded).  With `first_static`, work-group g
+    takes rank g as its first item without a ticket and the lists' tickets
+    continue after those ranks.  `late_start` > 0 makes work-groups become
+    resident after random delays of up to that many steps."""
     rng = random.Random(seed)
     lists = lists or claim_lists(grid)
     S = {"g1": S1, "g2": S2}
@@ -70,23 +84,27 @@ def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000):
     signals = set()  # GEMM1 tiles whose last part has finished the tile
     done = 0
     ticket = [0] * lists
+    skip = [len(range(l, grid, lists)) if first_static else 0 for l in range(lists)]
 
     def claim(g):
         lst = g % lists
         t = ticket[lst]
         ticket[lst] += 1
-        return lst + t * lists
+        return lst + (t + skip[lst]) * lists
 
-    # work-group state: [item rank or None, phase, remaining time]
+    # work-group state: [item rank or None, remaining time, next rank or None, start step]
     order = list(range(grid))
     rng.shuffle(order)  # first claims in any order
-    first = {g: claim(g) for g in order}
-    wgs = [[first[g], "main", rng.randint(1, 5)] for g in range(grid)]
-    for _ in range(max_steps):
+    first = {g: (g if first_static else claim(g)) for g in order}
+    wgs = [[first[g], rng.randint(1, 5), None, rng.randint(0, late_start)] for g in range(grid)]
+    for step in range(max_steps):
         progressed = False
         for g, w in enumerate(wgs):
-            p, phase, rem = w
+            p, rem, nxt, start = w
             if p is None:
+                continue
+            if step < start:
+                progressed = True  # not resident yet
                 continue
             if p >= len(item_list):
                 w[0] = None
@@ -95,8 +113,10 @@ def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000):
             kind, tile, s, needs = item_list[p]
             if kind == "g2" and any(n not in signals for n in needs):
                 continue  # waiting for producer tiles
+            if nxt is None:
+                w[2] = nxt = claim(g)  # no wait left in this item: take the next ticket
             if rem > 0:
-                w[2] -= 1
+                w[1] -= 1
                 progressed = True
                 continue
             key = (kind, tile)
@@ -104,7 +124,7 @@ def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000):
             if arrived[key] == S[kind] and kind == "g1":
                 signals.add(tile)  # the completing part reduces, stores Z and signals
             done += 1
-            w[0], w[2] = claim(g), rng.randint(1, 5)
+            w[0], w[1], w[2] = nxt, rng.randint(1, 5), None
             progressed = True
         if done == len(item_list):
             return True
@@ -146,3 +166,26 @@ def test_merged_rank_table_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
         for grid in (1, 2, 3, 8, 9, 17):
             for seed in range(3):
                 assert simulate(lst, S1, S2, grid, seed), (order, lag, grid, seed)
+
+
+@pytest.mark.parametrize("order", ["auto", "row", "shuffled"])
+@pytest.mark.parametrize("Mb,Nb1,Nb2,S1,S2", CASES)
+def test_static_first_items_and_late_residency(order, Mb, Nb1, Nb2, S1, S2):
+    """Static first items (when the host allows them) and work-groups that become
+    resident late: every launch still finishes."""
+    for lag in (0, 5, 40):
+        lst = items(Mb, Nb1, Nb2, S1, S2, order, merged_lag=lag)
+        for grid in (1, 3, 8, 9, 17):
+            fs = first_static_allowed(lst, grid)
+            for seed in range(3):
+                assert simulate(lst, S1, S2, grid, seed, first_static=fs, late_start=30), (order, lag, grid, seed, fs)
+    for grid in (2, 8, 17):  # the sequential kernels: no item waits, first items always static
+        g1 = [it for it in items(Mb, Nb1, Nb2, S1, S2, order) if it[0] == "g1"]
+        assert first_static_allowed(g1, grid)
+        assert simulate(g1, S1, S2, grid, 7, first_static=True, late_start=30)
+
+
+def test_host_rule_refuses_static_first_items_that_wait():
+    lst = items(1, 4, 2, 1, 2, "auto", consumers_first=True)
+    assert not first_static_allowed(lst, 3)
+    assert first_static_allowed(items(1, 4, 2, 1, 2, "auto", merged_lag=4), 4)
