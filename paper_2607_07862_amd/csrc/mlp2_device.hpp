@@ -482,12 +482,15 @@ __device__ __forceinline__ void release_add(uint32_t* cnt) {
   if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// A split-K part's arrival: store the partial, then one acquire-release
+// A split-K part's arrival: store the partial, then one agent-scope release
 // increment of the tile's counter (after every wave's stores are complete).
 // Returns true (uniformly) on the part that arrives last in this run, i.e.
-// that reads `target - 1`; that part has also acquired the others' partials
-// (agent-scope acquire by the incrementing thread, then a barrier and a
-// work-group acquire for the other waves).
+// that reads `target - 1`; that part then reads the others' partials after a
+// barrier and a work-group-scope acquire.  No agent-scope acquire is needed,
+// for the reason given for Z with the ready waits below: each tile's
+// partials (whole 1 KB runs, never sharing a line with another tile's) are
+// read once per launch, only by the completing part, after every part has
+// released them.
 template <class T, int NB>
 __device__ __forceinline__ bool arrive_split(float* part, uint32_t* cnt, long tile, int S, int s, uint32_t target,
                                              const f32x4 (&acc)[NB][T::TN][T::TM], int* s_slot, TraceAcc& tr) {
@@ -496,7 +499,7 @@ __device__ __forceinline__ bool arrive_split(float* part, uint32_t* cnt, long ti
   __syncthreads();
   if constexpr (kTrace) tr.t_rel = trace_now();
   if (threadIdx.x == 0) {
-    const uint32_t old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     *s_slot = old == target - 1u;
   }
   __syncthreads();
@@ -564,14 +567,28 @@ __device__ __forceinline__ void signal_ready(uint32_t* flag) { release_add(flag)
 // GEMM1 tile (mb, k / bn1) must have signalled in this run (once per tile and
 // run), i.e. its counter must have reached epoch + 1 (compared wrap-safe).
 //
-// Wave 0 reads up to 64 consecutive counters of the item's K range in one
-// vector load and takes the longest ready prefix (a ballot), so that one
-// agent-scope acquire covers every K-slice that is already available; an
-// acquire invalidates the L2 of the XCD, so it is issued once per newly ready
-// prefix, not once per slice and wave.  Between polls the wave sleeps; after
+// Wave 0 polls the first counter it needs; once that is ready it reads up to
+// 64 consecutive counters of the item's K range in one vector load and takes
+// the longest ready prefix (a ballot).  Between polls the wave sleeps; after
 // spin_limit polls it gives up, latches CTRL_ERROR and stops waiting for the
-// rest of the run.  The result reaches the other waves through LDS and a
-// work-group barrier.  Every call is made by all waves with the same k.
+// rest of the run.  The result reaches the other waves
+// through LDS and a work-group barrier.  Every call is made by all waves with
+// the same k.
+//
+// Visibility of Z.  The producer's agent-scope release writes its Z lines
+// back from its XCD's L2 before the counter moves.  The consumer needs no
+// agent-scope acquire (on this chip an invalidation of its XCD's whole L2,
+// which throws away the lines every other work-group of the XCD is
+// streaming, and measured several percent of a run where consumers wait
+// often): a cache can only return a stale Z line if it already held that
+// line, and none can.  Every launch starts with the caches invalidated, and
+// within a launch a line of Z (128 bytes of one row in one 64-column block;
+// rows and blocks are 128-byte aligned) is read only after the counter of
+// the tile that writes it has been seen complete, by the work-group whose
+// wait returned or by another that waited for it the same way.  The
+// observing load is an atomic, so it reads the counter at the device's
+// point of coherence; the Z loads are issued after it, in program order,
+// and a work-group-scope acquire orders them for the compiler.
 struct ReadyWait {
   const uint32_t* ready;
   uint32_t* err;  // CTRL_ERROR word
@@ -589,23 +606,29 @@ struct ReadyWait {
     if (uniform((int)(threadIdx.x >> 6)) == 0) {  // wave 0, as a scalar branch
       const int lane = threadIdx.x & 63;
       const int j = kb + lane;
-      const uint32_t* f = ready + ((long)(j <= kb_last ? j : kb_last) * Mb + mb) * kLine;
       int hi = -1;
       if (uniform(ld_relaxed(err)) == 0u) {
-        // scalar loop: every exit condition is wave-uniform
+        // Poll the first counter needed, every lane at the same address (one
+        // request per poll: a long wait must not flood the memory side that
+        // the running producers stream from); scalar loop, uniform exits.
+        const uint32_t* first = ready + ((long)kb * Mb + mb) * kLine;
         uint64_t m = 0;
         for (uint32_t polls = 0;; ++polls) {
-          const uint32_t v = ld_relaxed(f);  // every lane loads (address clamped in range)
-          m = __builtin_amdgcn_ballot_w64((j <= kb_last) & ((int32_t)(v - target) >= 0));
+          const uint32_t v = ld_relaxed(first);
+          m = __builtin_amdgcn_ballot_w64((int32_t)(v - target) >= 0);
           if ((m & 1u) || polls >= spin_limit) break;
           __builtin_amdgcn_s_sleep(2);
         }
-        if (m & 1u)
+        if (m & 1u) {
+          // then the longest ready prefix of up to 64 counters in one gather
+          // (counters only grow during a run, so the first is still ready)
+          const uint32_t v = ld_relaxed(ready + ((long)(j <= kb_last ? j : kb_last) * Mb + mb) * kLine);
+          m = __builtin_amdgcn_ballot_w64((j <= kb_last) & ((int32_t)(v - target) >= 0));
           hi = kb + (int)__builtin_ctzll(~m) - 1;
-        else if (lane == 0)
+        } else if (lane == 0) {
           __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
       }
-      if (hi >= 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       if (lane == 0) *s_known = hi >= 0 ? hi : 0x7fffffff;
     }
     __syncthreads();

@@ -291,9 +291,7 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, PHASE>())) void k
   constexpr int kLds = kernel_lds<T1, NB, T2, PHASE>();
   __shared__ __attribute__((aligned(1024))) char lds[kLds];
   __shared__ int s_item, s_slot;
-  // The epoch is needed only by split-K arrivals and ready waits, well after
-  // its load has returned; it stays in a vector register until then.
-  const uint32_t epoch = ld_relaxed(a.ctrl + CTRL_EPOCH);
+  const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
   const int g1 = PHASE == PHASE_GEMM2 ? 0 : a.items1;
   const int g2 = PHASE == PHASE_GEMM1 ? 0 : a.items2;
   const int total = g1 + g2;
