@@ -393,24 +393,24 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   const int gridp = go ? go : p->grid;
   a.trace_groups = std::max(std::max(grids[0], grids[1]), gridp);
   hipError_t err;
-  // First items without tickets (Args::first_static) save a launch the round
-  // trip of its first claim, which matters for a launch of one round of
-  // items with one work-group per CU (the weight-streaming shapes); they are
-  // used only there, and only when those first items never wait.  (With two
-  // work-groups per CU, measured at prefill size, claiming every item was
-  // faster.)
-  auto one_round = [&](int64_t items, int grid) { return items <= grid && grid <= p->num_cus; };
+  // First items without tickets (Args::first_static): with one work-group
+  // per CU, work-group g starts at once on rank g when rank g is an item that
+  // never waits, which saves the round trip of a first claim and keeps the
+  // first round's ranks in launch order.  (With two work-groups per CU,
+  // measured at prefill size, claiming every item was faster.)
+  auto statics = [&](int64_t never_wait_lead, int grid) -> int {
+    return grid <= p->num_cus ? (int)std::min<int64_t>(grid, never_wait_lead) : 0;
+  };
   if (mode == MLP2_MODE_SEQUENTIAL) {
     a.lists = claim_lists(grids[0]);
-    a.first_static = one_round(p->items1, grids[0]);  // GEMM1 items never wait
+    a.first_static = statics(p->items1, grids[0]);  // GEMM1 items never wait
     Args a2 = a;
     a2.lists = claim_lists(grids[1]);
-    a2.first_static = one_round(p->items2, grids[1]);  // nor do GEMM2 items of this mode
+    a2.first_static = statics(p->items2, grids[1]);  // nor do GEMM2 items of this mode
     err = mlp2::launch_sequential(p->kc, a, a2, grids, s);
   } else {
     a.lists = claim_lists(gridp);
-    const int64_t total = (int64_t)p->items1 + p->items2;
-    a.first_static = one_round(total, gridp) && total <= p->lead1;
+    a.first_static = statics(p->lead1, gridp);
     err = mlp2::launch_pipelined(p->kc, a, gridp, s);
   }
   if (err != hipSuccess) return fail(MLP2_ERR_HIP);

@@ -72,8 +72,8 @@ struct Args {
   int trace_cap;           // records per work-group
   int trace_groups;        // work-groups per trace section (the largest grid of the plan)
   int lists;               // claim lists of the launch (1 or 8; work-group g claims from list g % lists)
-  int first_static;        // nonzero: work-group g takes rank g as its first item without a ticket
-                           // (set only when the first `grid` ranks are items that never wait)
+  int first_static;        // work-groups g < first_static take rank g as their first item without a
+                           // ticket (ranks below it are items that never wait); the others claim
 };
 
 // ------------------------------------------------------------------ optional timing trace
@@ -223,7 +223,13 @@ template <class T, int NB, class Wait>
 __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long lda, int m0, int mlast,
                                          const uint16_t* const (&Bp)[NB], long ldb, int n0, int kbeg, int kend,
                                          f32x4 (&acc)[NB][T::TN][T::TM], char* lds, Wait& wait, TraceAcc& tr) {
-  const int tid = threadIdx.x;
+  // The thread index passes through an empty asm, so the compiler derives
+  // this call's per-lane offsets here instead of hoisting them out of the
+  // persistent item loop: in the pipelined kernel, whose items take one of
+  // two tile shapes, hoisted offsets of both shapes would stay live across
+  // the whole kernel and push the mainloop's accumulators out of registers.
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave % T::WM;
@@ -514,8 +520,9 @@ __device__ __forceinline__ bool arrive_split(float* part, uint32_t* cnt, long ti
 
 // The next item of a persistent work-group.  Claim list l = blockIdx % lists
 // hands out the ranks l, l + lists, l + 2 lists, ... in increasing order: the
-// first `skip` of them without a ticket (the work-groups' first items), the
-// rest through the list's ticket word.  Taking a ticket is a device-scope
+// first `skip` of them without a ticket (first items of the list's
+// work-groups below Args::first_static), the rest through the list's ticket
+// word.  Taking a ticket is a device-scope
 // atomic whose result comes back from the memory side after a long round
 // trip, so `issue` sends it as early as the protocol allows (thread 0 keeps
 // the ticket in a register while the item runs) and `park` writes the rank

@@ -52,11 +52,12 @@ __device__ __forceinline__ void store_y(const Args& a, int row, int col, const f
 // with 8 lists (work-group g on list g % 8) every XCD takes every 8th item of
 // the rank order: the same number of weight-streaming items per XCD (and per
 // L2 and fabric link), while the chip as a whole still works through the
-// ranks in order.  When the launch's first `grid` ranks are items that never
-// wait, work-group g takes rank g as its first item without a ticket.
+// ranks in order.  Work-groups g < first_static take rank g as their first
+// item without a ticket (those ranks are items that never wait); list l then
+// skips the ranks below first_static it would hand out.
 __device__ __forceinline__ Claim make_claim(const Args& a) {
   const int l = (int)(blockIdx.x % (unsigned)a.lists);
-  const int skip = a.first_static ? (int)((gridDim.x - 1u - (unsigned)l) / (unsigned)a.lists) + 1 : 0;
+  const int skip = l < a.first_static ? (a.first_static - 1 - l) / a.lists + 1 : 0;
   return Claim{a.ctrl + ctrl_ticket(l), l, a.lists, skip, 0u};
 }
 
@@ -170,29 +171,37 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
 
 // GEMM2 item p = tile * S2 + s (the parts of a tile are adjacent tickets,
 // see the kernels' deadlock argument).  WAIT: each K-slice of Z is consumed
-// only after its GEMM1 tile has signalled.
-template <class T, bool WAIT>
+// only after its GEMM1 tile has signalled.  The tile is HV column halves of
+// T side by side (HV = 1 or 2): with HV = 2 the mainloop treats the halves
+// as two weight operands (W2 at the tile's column and T::BN columns further
+// on), the same instantiation the gated GEMM1 uses for its Wg and Wu, so a
+// kernel that holds both item kinds carries one mainloop shape and one
+// register budget.  Each output element still accumulates over K in the
+// same order.
+template <class T, int HV, bool WAIT>
 __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epoch, char* lds, int* s_slot,
                                            Claim& next, int* s_next, TraceAcc& tr) {
   const int p = uniform(p_in);
   const int tile = p / a.S2, s = p - (p / a.S2) * a.S2;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
-  const int m0 = mb * T::BM, n0 = nb * T::BN;
+  const int m0 = mb * T::BM, n0 = nb * T::BN * HV;
   const int kbeg = s * a.kc2;
   const int kend = min(a.F, kbeg + a.kc2);
 
-  f32x4 acc[1][T::TN][T::TM];
-  const uint16_t* Bp[1] = {a.W2};
+  f32x4 acc[HV][T::TN][T::TM];
+  const uint16_t* Bp[HV];
+#pragma unroll
+  for (int h = 0; h < HV; ++h) Bp[h] = a.W2 + h * T::BN;
   const int zlast = a.Mb * T::BM - 1;
   if constexpr (WAIT) {
     ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1, epoch + 1u, a.spin_limit, s_slot,
                 -1, &tr};
     ClaimAtLastStage<ReadyWait> hook{w, &next, kend - kBK};
-    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
+    mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   } else {
     NoWait nowait;
     ClaimAtLastStage<NoWait> hook{nowait, &next, kend - kBK};
-    mainloop<T, 1>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
+    mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   }
   if constexpr (kTrace) tr_mark_mainloop(tr);
 
@@ -200,20 +209,23 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
     next.park(s_next);
     FragPos<T> fp(m0, n0);
 #pragma unroll
-    for (int tm = 0; tm < T::TM; ++tm)
+    for (int h = 0; h < HV; ++h)
 #pragma unroll
-      for (int tp = 0; tp < T::TN / 2; ++tp) {
-        float v[8];
-        pair_values<T>(acc[0], tp, tm, v);
-        store_y(a, fp.row0 + 16 * tm, fp.col0 + 32 * tp, v);
-      }
+      for (int tm = 0; tm < T::TM; ++tm)
+#pragma unroll
+        for (int tp = 0; tp < T::TN / 2; ++tp) {
+          float v[8];
+          pair_values<T>(acc[h], tp, tm, v);
+          store_y(a, fp.row0 + 16 * tm, fp.col0 + h * T::BN + 32 * tp, v);
+        }
   } else {
-    const bool last = arrive_split<T, 1>(a.part2, a.cnt2 + (long)tile * kLine, tile, a.S2, s,
-                                         (epoch + 1u) * (uint32_t)a.S2, acc, s_slot, tr);
+    const bool last = arrive_split<T, HV>(a.part2, a.cnt2 + (long)tile * kLine, tile, a.S2, s,
+                                          (epoch + 1u) * (uint32_t)a.S2, acc, s_slot, tr);
     next.park(s_next);
     if (!last) return;
-    reduce_epilogue<T, 1>(a.part2, tile, a.S2, [&](const Unit<T>& u, int lane, const float (&v)[1][8]) {
-      store_y(a, u.row(m0, lane), u.col(n0, lane), v[0]);
+    reduce_epilogue<T, HV>(a.part2, tile, a.S2, [&](const Unit<T>& u, int lane, const float (&v)[HV][8]) {
+#pragma unroll
+      for (int h = 0; h < HV; ++h) store_y(a, u.row(m0, lane), u.col(n0, lane) + h * T::BN, v[h]);
     });
   }
 }
@@ -273,22 +285,23 @@ struct MaxI {
   static constexpr int value = A > B ? A : B;
 };
 
-template <class T1, int NB, class T2, int PHASE>
+template <class T1, int NB, class T2, int HV, int PHASE>
 constexpr int kernel_lds() {
   return PHASE == PHASE_GEMM1   ? T1::template lds_bytes<NB>()
-         : PHASE == PHASE_GEMM2 ? T2::template lds_bytes<1>()
-                                : MaxI<T1::template lds_bytes<NB>(), T2::template lds_bytes<1>()>::value;
+         : PHASE == PHASE_GEMM2 ? T2::template lds_bytes<HV>()
+                                : MaxI<T1::template lds_bytes<NB>(), T2::template lds_bytes<HV>()>::value;
 }
 
 // Work-groups per CU the register budget must allow: two whenever two rings fit in LDS.
-template <class T1, int NB, class T2, int PHASE>
+template <class T1, int NB, class T2, int HV, int PHASE>
 constexpr int min_blocks() {
-  return kernel_lds<T1, NB, T2, PHASE>() <= 80 * 1024 ? 2 : 1;
+  return kernel_lds<T1, NB, T2, HV, PHASE>() <= 80 * 1024 ? 2 : 1;
 }
 
-template <class T1, int NB, class T2, int PHASE>
-__global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, PHASE>())) void k_mlp2(Args a) {
-  constexpr int kLds = kernel_lds<T1, NB, T2, PHASE>();
+// T1, NB: GEMM1 tile and weight operands; T2, HV: GEMM2 tile half and halves.
+template <class T1, int NB, class T2, int HV, int PHASE>
+__global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) void k_mlp2(Args a) {
+  constexpr int kLds = kernel_lds<T1, NB, T2, HV, PHASE>();
   __shared__ __attribute__((aligned(1024))) char lds[kLds];
   __shared__ int s_item, s_slot;
   const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
@@ -296,7 +309,7 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, PHASE>())) void k
   const int g2 = PHASE == PHASE_GEMM1 ? 0 : a.items2;
   const int total = g1 + g2;
   int p;
-  if (a.first_static) {
+  if ((int)blockIdx.x < a.first_static) {
     p = (int)blockIdx.x;
   } else {
     Claim first = make_claim(a);
@@ -315,13 +328,13 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, PHASE>())) void k
     if constexpr (PHASE == PHASE_PIPELINED) {
       const uint32_t e = uniform(a.orderp[p]);
       if (e & 0x80000000u)
-        gemm2_item<T2, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr);
+        gemm2_item<T2, HV, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr);
       else
         gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
     } else if constexpr (PHASE == PHASE_GEMM1) {
       gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_slot, next, &s_item, tr);
     } else {
-      gemm2_item<T2, false>(a, p, epoch, lds, &s_slot, next, &s_item, tr);
+      gemm2_item<T2, HV, false>(a, p, epoch, lds, &s_slot, next, &s_item, tr);
     }
     if constexpr (kTrace) tr_record(a, PHASE == PHASE_GEMM2 ? 1 : 0, n_items++, p, t_start, tr);
     __syncthreads();
@@ -354,14 +367,16 @@ struct Entry {
   const void* pipe;
 };
 
-#define MLP2_K(BM, BN1, BN2, NB, NS, PH) \
-  (const void*)&k_mlp2<typename TileFor<BM, BN1, NS>::type, NB, typename TileFor<BM, BN2, NS>::type, PH>
-#define MLP2_ENTRY(BM, BN1, BN2, NB, NS)                                                             \
-  Entry {                                                                                           \
-    BM, BN1, BN2, NB, NS, MLP2_K(BM, BN1, BN2, NB, NS, PHASE_GEMM1),                               \
-        MLP2_K(BM, BN1, BN2, NB, NS, PHASE_GEMM2),                                                  \
-        MLP2_K(BM, BN1, BN2, NB, NS, PHASE_PIPELINED)                                               \
+// GEMM2 of BN2 columns as one tile (HV = 1), or as two halves of BN2 / 2 that
+// share the GEMM1 tile shape (HV = 2).
+#define MLP2_K(BM, BN1, BN2, NB, NS, HV, PH)                                                             \
+  (const void*)&k_mlp2<typename TileFor<BM, BN1, NS>::type, NB, typename TileFor<BM, (BN2) / (HV), NS>::type, HV, PH>
+#define MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, HV)                                                       \
+  Entry {                                                                                             \
+    BM, BN1, BN2, NB, NS, MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_GEMM1),                             \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_GEMM2), MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_PIPELINED) \
   }
+#define MLP2_ENTRY(BM, BN1, BN2, NB, NS) MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, 1)
 
 static const Entry kEntries[] = {
     MLP2_ENTRY(32, 128, 128, 1, 4), MLP2_ENTRY(32, 128, 64, 1, 4), MLP2_ENTRY(32, 64, 128, 1, 4), MLP2_ENTRY(32, 64, 64, 1, 4),
@@ -375,8 +390,9 @@ static const Entry kEntries[] = {
     // wide weight tiles: half the activation traffic per weight byte
     MLP2_ENTRY(128, 256, 256, 1, 3), MLP2_ENTRY(128, 256, 128, 1, 3), MLP2_ENTRY(128, 128, 256, 1, 3),
     MLP2_ENTRY(128, 256, 256, 1, 2), MLP2_ENTRY(32, 256, 256, 1, 4), MLP2_ENTRY(64, 256, 256, 1, 3),
-    // 256-row blocks: the weights of a 129..256-row batch are streamed once
-    MLP2_ENTRY(256, 64, 128, 2, 3), MLP2_ENTRY(256, 64, 64, 2, 3), MLP2_ENTRY(256, 128, 128, 1, 3),
+    // 256-row blocks: the weights of a 129..256-row batch are streamed once; the
+    // gated GEMM2 of 128 columns runs as two 64-column halves (the GEMM1 shape)
+    MLP2_ENTRY_HV(256, 64, 128, 2, 3, 2), MLP2_ENTRY(256, 64, 64, 2, 3), MLP2_ENTRY(256, 128, 128, 1, 3),
     MLP2_ENTRY(256, 64, 64, 1, 3),
 };
 

@@ -61,13 +61,17 @@ def claim_lists(grid):
     return min(8, max(1, grid))
 
 
-def first_static_allowed(item_list, grid):
-    """The host's rule: work-groups take their first rank without a ticket only
-    when the first `grid` ranks are items that never wait."""
-    return all(item_list[r][0] == "g1" for r in range(min(grid, len(item_list))))
+def static_count(item_list, grid):
+    """The host's rule: work-groups g below the number of leading ranks that
+    never wait (GEMM1 items), and below the grid, take rank g as their first
+    item without a ticket."""
+    lead = 0
+    while lead < len(item_list) and item_list[lead][0] == "g1":
+        lead += 1
+    return min(grid, lead)
 
 
-def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000, first_static=False, late_start=0):
+def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000, first_static=0, late_start=0):
     """Returns True if every item completes.
 
     A work-group takes the ticket for its next item as soon as its current
@@ -84,7 +88,7 @@ def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000, first_
     signals = set()  # GEMM1 tiles whose last part has finished the tile
     done = 0
     ticket = [0] * lists
-    skip = [len(range(l, grid, lists)) if first_static else 0 for l in range(lists)]
+    skip = [len(range(l, first_static, lists)) for l in range(lists)]
 
     def claim(g):
         lst = g % lists
@@ -95,7 +99,7 @@ def simulate(item_list, S1, S2, grid, seed, lists=None, max_steps=200000, first_
     # work-group state: [item rank or None, remaining time, next rank or None, start step]
     order = list(range(grid))
     rng.shuffle(order)  # first claims in any order
-    first = {g: (g if first_static else claim(g)) for g in order}
+    first = {g: (g if g < first_static else claim(g)) for g in order}
     wgs = [[first[g], rng.randint(1, 5), None, rng.randint(0, late_start)] for g in range(grid)]
     for step in range(max_steps):
         progressed = False
@@ -171,21 +175,23 @@ def test_merged_rank_table_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
 @pytest.mark.parametrize("order", ["auto", "row", "shuffled"])
 @pytest.mark.parametrize("Mb,Nb1,Nb2,S1,S2", CASES)
 def test_static_first_items_and_late_residency(order, Mb, Nb1, Nb2, S1, S2):
-    """Static first items (when the host allows them) and work-groups that become
-    resident late: every launch still finishes."""
+    """Static first items (as many as the host allows) and work-groups that
+    become resident late: every launch still finishes."""
     for lag in (0, 5, 40):
         lst = items(Mb, Nb1, Nb2, S1, S2, order, merged_lag=lag)
         for grid in (1, 3, 8, 9, 17):
-            fs = first_static_allowed(lst, grid)
+            fs = static_count(lst, grid)
+            assert all(lst[r][0] == "g1" for r in range(fs))
             for seed in range(3):
                 assert simulate(lst, S1, S2, grid, seed, first_static=fs, late_start=30), (order, lag, grid, seed, fs)
-    for grid in (2, 8, 17):  # the sequential kernels: no item waits, first items always static
+    for grid in (2, 8, 17):  # the sequential kernels: no item waits
         g1 = [it for it in items(Mb, Nb1, Nb2, S1, S2, order) if it[0] == "g1"]
-        assert first_static_allowed(g1, grid)
-        assert simulate(g1, S1, S2, grid, 7, first_static=True, late_start=30)
+        assert simulate(g1, S1, S2, grid, 7, first_static=static_count(g1, grid), late_start=30)
 
 
-def test_host_rule_refuses_static_first_items_that_wait():
+def test_host_rule_takes_static_first_items_only_below_the_first_waiting_rank():
     lst = items(1, 4, 2, 1, 2, "auto", consumers_first=True)
-    assert not first_static_allowed(lst, 3)
-    assert first_static_allowed(items(1, 4, 2, 1, 2, "auto", merged_lag=4), 4)
+    assert static_count(lst, 3) == 0
+    merged = items(1, 4, 2, 1, 2, "auto", merged_lag=4)
+    n = static_count(merged, 8)
+    assert 0 < n < 8 and merged[n][0] == "g2"
