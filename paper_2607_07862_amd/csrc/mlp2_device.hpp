@@ -631,7 +631,10 @@ struct ReadyWait {
           // (counters only grow during a run, so the first is still ready)
           const uint32_t v = ld_relaxed(ready + ((long)(j <= kb_last ? j : kb_last) * Mb + mb) * kLine);
           m = __builtin_amdgcn_ballot_w64((j <= kb_last) & ((int32_t)(v - target) >= 0));
-          hi = kb + (int)__builtin_ctzll(~m) - 1;
+          // ~m == 0 (all 64 ready) must be taken apart: a count of trailing
+          // zeros of 0 is undefined, and the scalar find-first-one the
+          // compiler emits for it returns -1.
+          hi = ~m ? kb + (int)__builtin_ctzll(~m) - 1 : kb + 63;
         } else if (lane == 0) {
           __hip_atomic_fetch_or(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }

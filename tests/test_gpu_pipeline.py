@@ -8,7 +8,9 @@
   counters and the epoch carry over from run to run without host resets);
 * a dropped producer signal (failure injection from the host) makes the
   bounded wait give up, every kernel still exits, mlp2_check reports the
-  timeout and the plan recovers.
+  timeout and the plan recovers; so does one beyond the first 64 column
+  blocks of a consumer whose first 64 are all ready (the wait reads
+  readiness 64 blocks at a time).
 """
 import pytest
 import torch
@@ -96,6 +98,37 @@ def test_dropped_signal_times_out_and_recovers(lib):
     assert_bit_equal(Ys, Yp, "after recovery")
     ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
     assert_matches_oracle(Yp, ref, "after recovery")
+    plan.close()
+
+
+@pytest.mark.parametrize("dropped", [63, 64, 80, 99])
+def test_wait_covers_blocks_past_one_full_window(lib, dropped):
+    """A consumer whose first 64 column blocks are all ready still waits for later ones.
+
+    One work-group runs every GEMM1 item before the single GEMM2 item, whose
+    K range covers 100 column blocks; when it starts, every block but the
+    dropped one is ready, so its first gather finds a full 64-block window.
+    The missing signal must end in a time-out, never in a skipped wait.
+    """
+    M, H, F, act = 32, 64, 6400, 1
+    d = I.make_inputs(M, H, F, act, seed=71)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, {"bm": 32, "bn1": 64, "splitk1": 1, "bn2": 64, "splitk2": 1})
+    info = plan.info()
+    assert (info["items1"], info["items2"], info["row_blocks"]) == (100, 1, 1)
+    plan.set_option(B.OPT_GRID, 1)
+    plan.set_option(B.OPT_SPIN_LIMIT, 2000)
+    plan.set_option(B.OPT_DROP_SIGNAL, dropped)
+    run(plan, g, B.MODE_TILE_PIPELINED)
+    torch.cuda.synchronize()
+    assert plan.check() == B.ERR_TIMEOUT
+    plan.set_option(B.OPT_DROP_SIGNAL, -1)
+    plan.set_option(B.OPT_SPIN_LIMIT, 1 << 20)
+    Yp = run(plan, g, B.MODE_TILE_PIPELINED)
+    Ys = run(plan, g, B.MODE_SEQUENTIAL)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    assert_bit_equal(Ys, Yp, "after recovery")
     plan.close()
 
 
