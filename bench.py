@@ -11,8 +11,9 @@ L2s and the 256 MB MALL before each timed run, modes interleaved), the
 roofline fraction of the dominant kernel (the pipelined launch, timed with HIP
 events on the stream it is launched on), HBM traffic from committed
 rocprofv3 counter summaries when they match the current kernel sources, a
-table of both modes on every MLP workload, and the fp64 CPU oracle timed on a
-bounded sample of the headline workload.
+table of both modes on every MLP workload (beside eager PyTorch on the same
+inputs, hipBLASLt GEMMs plus an activation kernel, as a reference point), and
+the fp64 CPU oracle timed on a bounded sample of the headline workload.
 
 Only ``--gpus 1`` is supported: the build targets a single GPU.
 """
@@ -89,6 +90,41 @@ def device_random_inputs(w):
     W1 = (torch.randn(n1 * w.H, w.F, device="cuda", generator=gen) * w.H ** -0.5).to(torch.bfloat16)
     W2 = (torch.randn(w.F, w.H, device="cuda", generator=gen) * w.F ** -0.5).to(torch.bfloat16)
     return {"X": X, "W1": W1, "W2": W2}
+
+
+def torch_eager_us(w, g, steps):
+    """Mean µs per step of the same MLP in eager PyTorch on the platform
+    libraries (hipBLASLt GEMMs plus an elementwise activation kernel), bf16
+    in and out, on the same device inputs: a reference point, not the target.
+    The gated GEMM1 runs as one GEMM over the gate and up columns side by side."""
+    import torch
+    import torch.nn.functional as Fn
+
+    X, W2 = g["X"], g["W2"]
+    if w.gated:
+        W1 = torch.cat([g["W1"][: w.H], g["W1"][w.H :]], dim=1)  # [H, 2F]: gate columns, then up columns
+
+        def step():
+            gu = X @ W1
+            return (Fn.silu(gu[:, : w.F]) * gu[:, w.F :]) @ W2
+    else:
+        W1 = g["W1"]
+        gelu = w.act == 1
+
+        def step():
+            z = X @ W1
+            return (Fn.gelu(z, approximate="tanh") if gelu else z) @ W2
+
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) * 1e3 / steps
 
 
 class Runner:
@@ -198,7 +234,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=100, help="untimed warm-up steps (each mode once per step); clocks settle before the timed block")
     ap.add_argument("--workload", default="l8b_decode")
     ap.add_argument("--tuning", default="", help="JSON dict of mlp2_tuning_t fields")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
@@ -289,25 +325,30 @@ def main():
     if not args.no_table and not args.only_pipelined:
         for key in I.WORKLOAD_ORDER:
             wk = I.WORKLOADS[key]
+            steps = max(10, args.steps // 2)
             if key == args.workload:
                 rr_p, rr_s, inf = value, extra["sequential_us"], info
+                te = torch_eager_us(wk, g, steps)
             else:
-                rr = Runner(B, wk, device_random_inputs(wk), None, stream)
-                for _ in range(5):
+                gk = device_random_inputs(wk)
+                rr = Runner(B, wk, gk, None, stream)
+                for _ in range(30):
                     rr.run(B.MODE_TILE_PIPELINED)
                     rr.run(B.MODE_SEQUENTIAL)
-                steps = max(10, args.steps // 2)
                 rr_p = rr.block(B.MODE_TILE_PIPELINED, steps)
                 rr_s = rr.block(B.MODE_SEQUENTIAL, steps)
                 rr.check()
                 inf = rr.info
                 rr.close()
+                te = torch_eager_us(wk, gk, steps)
+                del gk
                 torch.cuda.empty_cache()
             rf = roofline(wk, rr_p)
             row = {
                 "pipelined_us": round(rr_p, 2),
                 "sequential_us": round(rr_s, 2),
                 "gain_pct": round((rr_s - rr_p) / rr_s * 100, 1),
+                "torch_eager_us": round(te, 2),
                 "bound": rf["bound"],
                 "frac": rf["frac"],
                 "hbm_frac": round(wk.alg_bytes() / (rr_p * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),

@@ -68,13 +68,19 @@ enum mlp2_status {
 };
 
 /* GEMM1 tile-ordering policies (Sec. III-A.5: the first kernel may take its
- * tiles from a predefined source order).  The default is column-first: whole
- * column blocks of Z first, so GEMM2's K-slices complete in order, and the
- * row blocks of one column block (which share its weight columns) run
- * together.  (Row-block-first halves, which let some GEMM2 items start
- * before GEMM1 ends, measured slower at prefill size.) */
+ * tiles from a predefined source order).  The base order is column-first:
+ * whole column blocks of Z first, so GEMM2's K-slices complete in order, and
+ * the row blocks of one column block (which share its weight columns) run
+ * together.  The default refines it for plans with several row blocks and no
+ * split-K: ranks r, r + 8, ... run on one XCD, and each wave of the grid's
+ * worth of tiles (still whole column blocks) is dealt to the 8 XCDs as
+ * near-square sub-blocks, so the operand slices a stage reads are shared
+ * inside each XCD's L2; the GEMM2 kernel's items are dealt the same way.
+ * (Row-block-first halves, which let some GEMM2 items start before GEMM1
+ * ends, measured slower at prefill size.) */
 enum mlp2_order {
-  MLP2_ORDER_AUTO = 0,         /* the default: column-first                                     */
+  MLP2_ORDER_AUTO = 0,         /* the default: XCD-grouped column-first with several row
+                                  blocks and no split-K, else column-first                     */
   MLP2_ORDER_COLUMN_FIRST = 1, /* every row block of column block 0, then column block 1, ... */
   MLP2_ORDER_ROW_FIRST = 2,    /* every column block of row block 0, then row block 1, ...    */
   MLP2_ORDER_REVERSED = 3,     /* column-first, last column block first (stress order)         */
@@ -91,7 +97,7 @@ typedef struct mlp2_tuning {
   int grid;      /* persistent grid of every launch (no more work-groups than fit the
                     device at once)                                                      */
   int order;     /* enum mlp2_order (0 = MLP2_ORDER_AUTO)                                 */
-  int stages;    /* LDS ring depth of the tile mainloop (2, 3 or 4)                       */
+  int stages;    /* LDS ring depth of the tile mainloop (2, 3 or 4, as built for the shape)*/
   int reserved[6];
 } mlp2_tuning_t;
 

@@ -48,6 +48,7 @@ struct mlp2_plan_s {
   uint32_t* ready = nullptr;
   uint32_t* ctrl = nullptr;
   uint32_t* order1 = nullptr;
+  uint32_t* order2 = nullptr;
   uint32_t* orderp = nullptr;
   int64_t lead1 = 0;  // leading ranks of the pipelined table that are GEMM1 items (they never wait)
   size_t counters_off = 0, counters_bytes = 0;
@@ -81,10 +82,53 @@ int choose_split(int64_t K, int tiles, int want, int min_k, int* kc) {
   return ceil_div(K, k);
 }
 
+// XCD-grouped order of an Mb x N tile grid (tile = nb * Mb + mb), for plans
+// with several row blocks.  A launch deals rank r to the work-groups of claim
+// list r % 8, which all sit on XCD r % 8 (work-groups are dispatched to the 8
+// XCDs round-robin), so the tiles at ranks x, x + 8, ... share XCD x's L2.
+// Consecutive waves of `wave` tiles cover whole column blocks (every row
+// block of C columns, so column blocks still complete in order); each wave
+// is cut into 8 sub-blocks as close to square as the divisors of 8 allow, one
+// per XCD, walked column-first.  Every stage of a wave then reads rows + cols
+// distinct operand slices per XCD instead of (rows of the XCD) + C: an 8 x 8
+// sub-block reads 16 slices where the plain column-first deal reads 2 + 32.
+std::vector<uint32_t> xcd_grouped(int Mb, int N, int wave) {
+  constexpr int kXcds = 8;
+  std::vector<uint32_t> out;
+  out.reserve((size_t)Mb * N);
+  const int C = std::max(1, wave / Mb);
+  std::vector<uint32_t> per[kXcds];
+  for (int c0 = 0; c0 < N; c0 += C) {
+    const int cw = std::min(C, N - c0);
+    int best_r = 1, best_cost = INT32_MAX;
+    for (int r = 1; r <= kXcds && r <= Mb; r *= 2) {
+      const int cost = ceil_div(Mb, r) + ceil_div(cw, kXcds / r);
+      if (cost < best_cost) { best_cost = cost; best_r = r; }
+    }
+    const int rows = ceil_div(Mb, best_r), cols = ceil_div(cw, kXcds / best_r);
+    for (int x = 0; x < kXcds; ++x) {
+      per[x].clear();
+      const int rg = x % best_r, cg = x / best_r;
+      for (int nb = c0 + cg * cols; nb < std::min(c0 + cw, c0 + (cg + 1) * cols); ++nb)
+        for (int mb = rg * rows; mb < std::min(Mb, (rg + 1) * rows); ++mb) per[x].push_back((uint32_t)(nb * Mb + mb));
+    }
+    // Deal the wave: its j-th group of 8 ranks takes the j-th tile of every
+    // sub-block; once a sub-block runs out (ragged edges), the rest close up.
+    for (size_t j = 0;; ++j) {
+      bool any = false;
+      for (int x = 0; x < kXcds; ++x)
+        if (j < per[x].size()) { out.push_back(per[x][j]); any = true; }
+      if (!any) break;
+    }
+  }
+  return out;
+}
+
 // GEMM1 item order (the rank order of the GEMM1 kernel, and of the GEMM1
 // items within the pipelined kernel).  Items are id = tile * S1 + s with
 // tile = nb * Mb + mb; every policy orders tiles and keeps the S1 parts of a
-// tile adjacent.
+// tile adjacent.  MLP2_ORDER_AUTO is the XCD-grouped column-first order when
+// there are several row blocks and no split-K, else plain column-first.
 void build_order(mlp2_plan_s* p, std::vector<uint32_t>& out) {
   std::vector<uint32_t> tiles;
   tiles.reserve((size_t)p->Mb * p->Nb1);
@@ -98,7 +142,13 @@ void build_order(mlp2_plan_s* p, std::vector<uint32_t>& out) {
       for (int nb = p->Nb1 - 1; nb >= 0; --nb)
         for (int mb = 0; mb < p->Mb; ++mb) tile(nb, mb);
       break;
-    default:  // MLP2_ORDER_AUTO, MLP2_ORDER_COLUMN_FIRST, and the base of the shuffled order
+    case MLP2_ORDER_AUTO:
+      if (p->Mb > 1 && p->S1 == 1) {
+        tiles = xcd_grouped(p->Mb, p->Nb1, p->grid1);
+        break;
+      }
+      [[fallthrough]];
+    default:  // MLP2_ORDER_COLUMN_FIRST, and the base of the shuffled order
       for (int nb = 0; nb < p->Nb1; ++nb)
         for (int mb = 0; mb < p->Mb; ++mb) tile(nb, mb);
       if (p->order == MLP2_ORDER_SHUFFLED) {
@@ -113,12 +163,27 @@ void build_order(mlp2_plan_s* p, std::vector<uint32_t>& out) {
     for (int s = 0; s < p->S1; ++s) out.push_back(t * (uint32_t)p->S1 + (uint32_t)s);
 }
 
+// GEMM2 item order (ranks of the GEMM2 kernel; GEMM2 items of the pipelined
+// table are placed in this order among equal keys): XCD-grouped under
+// MLP2_ORDER_AUTO with several row blocks and no split-K, else item order
+// (q = tile * S2 + s, tile = nb * Mb + mb).  No GEMM2 item waits in the
+// GEMM2 kernel, so any order is valid there.
+void build_order2(const mlp2_plan_s* p, std::vector<uint32_t>& out) {
+  if (p->order == MLP2_ORDER_AUTO && p->Mb > 1 && p->S2 == 1) {
+    out = xcd_grouped(p->Mb, p->Nb2, p->grid2);
+    return;
+  }
+  out.resize((size_t)p->items2);
+  for (int q = 0; q < p->items2; ++q) out[(size_t)q] = (uint32_t)q;
+}
+
 // Rank table of the pipelined kernel: the GEMM1 items keep their order; GEMM2
 // item q = tile * S2 + s goes right after rank h(q) + lag, where h(q) is the
 // highest GEMM1 rank among the tiles its K range reads.  Every GEMM2 item thus
 // ranks above every GEMM1 item it waits for (what the deadlock argument
 // needs), and is claimed about `lag` claims after its last producer.
-void build_merged(const mlp2_plan_s* p, const std::vector<uint32_t>& order1, int lag, std::vector<uint32_t>& out) {
+void build_merged(const mlp2_plan_s* p, const std::vector<uint32_t>& order1, const std::vector<uint32_t>& order2, int lag,
+                  std::vector<uint32_t>& out) {
   std::vector<int64_t> last_rank((size_t)p->Mb * p->Nb1, -1);
   for (size_t r = 0; r < order1.size(); ++r) {
     const uint32_t t = order1[r] / (uint32_t)p->S1;
@@ -132,7 +197,8 @@ void build_merged(const mlp2_plan_s* p, const std::vector<uint32_t>& order1, int
   std::vector<Key> keys;
   keys.reserve(order1.size() + (size_t)p->items2);
   for (size_t r = 0; r < order1.size(); ++r) keys.push_back({(int64_t)r, 0, order1[r]});
-  for (int q = 0; q < p->items2; ++q) {
+  for (const uint32_t q2 : order2) {
+    const int q = (int)q2;
     const int tile = q / p->S2, s = q % p->S2;
     const int mb = tile % p->Mb;
     const int64_t kbeg = (int64_t)s * p->kc2, kend = std::min<int64_t>(p->F, kbeg + p->kc2);
@@ -160,12 +226,14 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 }
 
 int upload_order(mlp2_plan_s* p) {
-  std::vector<uint32_t> ord, merged;
+  std::vector<uint32_t> ord, ord2, merged;
   build_order(p, ord);
-  build_merged(p, ord, p->grid_override ? p->grid_override : p->grid, merged);
+  build_order2(p, ord2);
+  build_merged(p, ord, ord2, p->grid_override ? p->grid_override : p->grid, merged);
   p->lead1 = 0;
   while (p->lead1 < (int64_t)merged.size() && !(merged[p->lead1] & 0x80000000u)) ++p->lead1;
   if (hipMemcpy(p->order1, ord.data(), ord.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(p->order2, ord2.data(), ord2.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(p->orderp, merged.data(), merged.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess)
     return MLP2_ERR_HIP;
   return MLP2_OK;
@@ -218,15 +286,29 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   p->M = M; p->H = H; p->F = F; p->act = act; p->device = dev;
   p->num_cus = prop.multiProcessorCount;
 
-  // ---- tile choice by regime.  Up to 256 rows (weight streaming): one row
-  // block holds every row, so each weight byte is read once; 128-wide weight
-  // tiles except at 128 rows, where the activation tile is the larger operand
-  // and 64-wide tiles give enough items with little or no split-K.  Beyond
-  // 256 rows (MFMA-bound): 128 x 128 tiles, two work-groups per CU.
-  const bool big = M > 256;
-  const int bm0 = M <= 32 ? 32 : M <= 64 ? 64 : M <= 128 ? 128 : M <= 256 ? 256 : 128;
-  const int wide = (bm0 != 128 || big) ? 128 : 64;
-  const int pref[4] = {bm0, nb == 1 ? wide : 64, bm0 == 128 && !big ? 64 : 128, big ? 2 : bm0 == 256 ? 3 : 4};
+  // ---- tile choice by regime (each row chosen by measurement on MI355X).
+  // Up to 256 rows the plan streams weights: one row block holds every row,
+  // so each weight byte is read once, and split-K makes enough items.  At 32
+  // and 64 rows the per-item costs (pipeline fill, epilogue, split-K arrival)
+  // weigh more than idle CUs, so both GEMMs keep their K ranges deep; at 64
+  // rows small tiles shorten the latency-bound critical path.  Beyond 256 rows (MFMA-bound): 128 x 128 tiles, two work-groups
+  // per CU.
+  int pref[4];
+  int min_k1 = 256, min_k2 = 256;  // shallowest K range of one split-K part
+  if (M <= 32) {
+    pref[0] = 32; pref[1] = 64; pref[2] = 128; pref[3] = 4;
+    min_k1 = 2048;
+    min_k2 = 1536;
+  } else if (M <= 64) {
+    pref[0] = 64; pref[1] = 64; pref[2] = 64; pref[3] = 4;
+    min_k1 = min_k2 = 1024;
+  } else if (M <= 128) {
+    pref[0] = 128; pref[1] = 64; pref[2] = 64; pref[3] = 4;
+  } else if (M <= 256) {
+    pref[0] = 256; pref[1] = nb == 1 ? 128 : 64; pref[2] = 128; pref[3] = 3;
+  } else {
+    pref[0] = 128; pref[1] = 128; pref[2] = 128; pref[3] = 2;
+  }
   // Fallbacks when the preferred tiles do not divide F / H or are not built.
   const int cand[][4] = {
       {pref[0], pref[1], pref[2], pref[3]}, {pref[0], pref[1], 64, pref[3]}, {pref[0], 64, 64, pref[3]},
@@ -264,13 +346,13 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
     p->kc1 = (int)align_up((size_t)ceil_div(H, tz.splitk1), mlp2::kBK);
     p->S1 = ceil_div(H, p->kc1);
   } else {
-    p->S1 = choose_split(H, tiles1, occ[0] * p->num_cus, 256, &p->kc1);
+    p->S1 = choose_split(H, tiles1, occ[0] * p->num_cus, min_k1, &p->kc1);
   }
   if (tz.splitk2) {
     p->kc2 = (int)align_up((size_t)ceil_div(F, tz.splitk2), mlp2::kBK);
     p->S2 = ceil_div(F, p->kc2);
   } else {
-    p->S2 = choose_split(F, tiles2, occ[1] * p->num_cus, 256, &p->kc2);
+    p->S2 = choose_split(F, tiles2, occ[1] * p->num_cus, min_k2, &p->kc2);
   }
   p->order = tz.order;
   p->items1 = tiles1 * p->S1;
@@ -310,6 +392,8 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   const size_t cnt_end = off;
   const size_t ord_off = off;
   off = align_up(off + (size_t)p->items1 * 4, 256);
+  const size_t ord2_off = off;
+  off = align_up(off + (size_t)p->items2 * 4, 256);
   const size_t ordp_off = off;
   off = align_up(off + ((size_t)p->items1 + p->items2) * 4, 256);
   p->ws_bytes = off;
@@ -327,6 +411,7 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   p->ready = (uint32_t*)(b + r_off);
   p->ctrl = (uint32_t*)(b + ctrl_off);
   p->order1 = (uint32_t*)(b + ord_off);
+  p->order2 = (uint32_t*)(b + ord2_off);
   p->orderp = (uint32_t*)(b + ordp_off);
   p->counters_off = cnt_off;
   p->counters_bytes = cnt_end - cnt_off;
@@ -367,6 +452,7 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   a.ready = p->ready;
   a.ctrl = p->ctrl;
   a.order1 = p->order1;
+  a.order2 = p->order2;
   a.orderp = p->orderp;
   a.M = (int)p->M;
   a.H = (int)p->H;

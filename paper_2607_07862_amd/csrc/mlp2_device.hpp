@@ -58,6 +58,7 @@ struct Args {
   uint32_t* ready;     // ready counters: tile (mb, nb1) at word (nb1 * Mb + mb) * kLine
   uint32_t* ctrl;      // CTRL_* words
   const uint32_t* order1;  // GEMM1 item per rank of the GEMM1 kernel, length items1
+  const uint32_t* order2;  // GEMM2 item per rank of the GEMM2 kernel, length items2
   const uint32_t* orderp;  // item per rank of the pipelined kernel, length items1 + items2
                            // (bit 31 set: GEMM2 item; else GEMM1 item id)
   int M, H, F, act;
@@ -207,6 +208,19 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Wait until this wave's loads of the current stage are complete while the
+// `after` (<= A) stages issued behind it stay in flight.  `after` is uniform.
+template <int PER, int A>
+__device__ __forceinline__ void wait_stages_behind(int after) {
+  if constexpr (A <= 0) {
+    wait_vm<0>();
+  } else {
+    static_assert(A * PER <= 63, "vmcnt holds at most 63 outstanding loads");
+    if (after >= A) wait_vm<A * PER>();
+    else wait_stages_behind<PER, A - 1>(after);
+  }
+}
+
 // ------------------------------------------------------------------ mainloop
 
 // acc[b][tn][tm] = sum over k in [kbeg, kend) of W_b[k][n] * A[m][k] for the
@@ -338,17 +352,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   for (int it = 0; it < nk; ++it) {
     const uint64_t t0 = trace_now();
     // Own loads of stage `it` complete: the stages issued after it may stay in flight.
-    const int after = min(T::NS - 2, nk - 1 - it);
-    if constexpr (T::NS >= 4) {
-      if (after >= 2) wait_vm<2 * PER_STAGE>();
-      else if (after == 1) wait_vm<PER_STAGE>();
-      else wait_vm<0>();
-    } else if constexpr (T::NS == 3) {
-      if (after >= 1) wait_vm<PER_STAGE>();
-      else wait_vm<0>();
-    } else {
-      wait_vm<0>();
-    }
+    wait_stages_behind<PER_STAGE, T::NS - 2>(min(T::NS - 2, nk - 1 - it));
     __syncthreads();
     if constexpr (kTrace) tr.ring += trace_now() - t0;
     if (it + T::NS - 1 < nk) issue(it + T::NS - 1);

@@ -334,7 +334,7 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
     } else if constexpr (PHASE == PHASE_GEMM1) {
       gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_slot, next, &s_item, tr);
     } else {
-      gemm2_item<T2, HV, false>(a, p, epoch, lds, &s_slot, next, &s_item, tr);
+      gemm2_item<T2, HV, false>(a, (int)a.order2[p], epoch, lds, &s_slot, next, &s_item, tr);
     }
     if constexpr (kTrace) tr_record(a, PHASE == PHASE_GEMM2 ? 1 : 0, n_items++, p, t_start, tr);
     __syncthreads();

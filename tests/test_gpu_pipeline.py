@@ -132,6 +132,29 @@ def test_wait_covers_blocks_past_one_full_window(lib, dropped):
     plan.close()
 
 
+@pytest.mark.parametrize("grid", [0, 1, 5, 24])
+def test_xcd_grouped_default_order(lib, grid):
+    """Several row blocks and no split-K: the default order deals the tiles of
+    both kernels to the XCDs in sub-blocks (ragged here: 5 row blocks).  The
+    pipelined mode gives the sequential mode's bits, within the oracle's bound."""
+    M, H, F, act = 640, 256, 1024, 1
+    d = I.make_inputs(M, H, F, act, seed=90)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, {"bm": 128, "bn1": 128, "bn2": 128, "splitk1": 1, "splitk2": 1})
+    info = plan.info()
+    assert (info["row_blocks"], info["splitk1"], info["splitk2"], info["order"]) == (5, 1, 1, B.ORDER_AUTO)
+    if grid:
+        plan.set_option(B.OPT_GRID, grid)
+    Ys = run(plan, g, B.MODE_SEQUENTIAL).clone()
+    Yp = run(plan, g, B.MODE_TILE_PIPELINED)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    assert_bit_equal(Ys, Yp, f"grid {grid}")
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
+    assert_matches_oracle(Yp, ref, f"grid {grid}")
+    plan.close()
+
+
 def test_run_argument_errors(lib):
     M, H, F = 32, 64, 128
     g = device_inputs(I.make_inputs(M, H, F, 0, seed=1))

@@ -18,7 +18,30 @@ import random
 import pytest
 
 
-def column_first_tiles(Mb, Nb1, order, seed=12345, S2=1):
+def xcd_grouped(Mb, N, wave):
+    """The host's XCD-grouped deal: waves of whole column blocks, cut into 8
+    near-square sub-blocks (one per XCD, walked column-first); within a wave,
+    rank 8 j + x is the j-th tile of sub-block x, and exhausted sub-blocks
+    close up."""
+    out = []
+    C = max(1, wave // Mb)
+    for c0 in range(0, N, C):
+        cw = min(C, N - c0)
+        r = min((r for r in (1, 2, 4, 8) if r <= Mb), key=lambda r: -(-Mb // r) + -(-cw // (8 // r)))
+        rows, cols = -(-Mb // r), -(-cw // (8 // r))
+        per = [[] for _ in range(8)]
+        for x in range(8):
+            rg, cg = x % r, x // r
+            for nb in range(c0 + cg * cols, min(c0 + cw, c0 + (cg + 1) * cols)):
+                per[x] += [nb * Mb + mb for mb in range(rg * rows, min(Mb, (rg + 1) * rows))]
+        for j in range(max(len(p) for p in per)):
+            out += [p[j] for p in per if j < len(p)]
+    return out
+
+
+def column_first_tiles(Mb, Nb1, order, seed=12345, S2=1, wave=16):
+    if order == "xcd":
+        return xcd_grouped(Mb, Nb1, wave)
     if order == "halves":  # column-first over each half of the row blocks (a stress order)
         per = -(-Mb // 2)
         return [nb * Mb + mb for g0 in range(0, Mb, per) for nb in range(Nb1) for mb in range(g0, min(Mb, g0 + per))]
@@ -40,7 +63,8 @@ def items(Mb, Nb1, Nb2, S1, S2, order, consumers_first=False, merged_lag=None):
     g1 = [("g1", t, s, []) for t in column_first_tiles(Mb, Nb1, order, S2=S2) for s in range(S1)]
     per = -(-Nb1 // S2)
     g2 = []
-    for tile in range(Mb * Nb2):
+    tiles2 = xcd_grouped(Mb, Nb2, 16) if order == "xcd" else range(Mb * Nb2)
+    for tile in tiles2:
         mb = tile % Mb
         for s in range(S2):
             kbs = range(s * per, min(Nb1, (s + 1) * per))
@@ -148,7 +172,7 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("order", ["auto", "row", "reversed", "shuffled", "halves"])
+@pytest.mark.parametrize("order", ["auto", "xcd", "row", "reversed", "shuffled", "halves"])
 @pytest.mark.parametrize("Mb,Nb1,Nb2,S1,S2", CASES)
 def test_pipelined_schedule_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
     lst = items(Mb, Nb1, Nb2, S1, S2, order)
@@ -157,7 +181,7 @@ def test_pipelined_schedule_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
             assert simulate(lst, S1, S2, grid, seed), (order, grid, seed)
 
 
-@pytest.mark.parametrize("order", ["auto", "row", "shuffled", "halves"])
+@pytest.mark.parametrize("order", ["auto", "xcd", "row", "shuffled", "halves"])
 @pytest.mark.parametrize("Mb,Nb1,Nb2,S1,S2", CASES)
 def test_merged_rank_table_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
     for lag in (0, 1, 5, 40):
@@ -195,3 +219,18 @@ def test_host_rule_takes_static_first_items_only_below_the_first_waiting_rank():
     merged = items(1, 4, 2, 1, 2, "auto", merged_lag=4)
     n = static_count(merged, 8)
     assert 0 < n < 8 and merged[n][0] == "g2"
+
+
+@pytest.mark.parametrize("Mb,N,wave", [(16, 112, 512), (16, 32, 512), (3, 10, 17), (5, 7, 8), (1, 9, 4), (40, 3, 64), (8, 64, 64)])
+def test_xcd_grouped_deal_is_a_permutation_of_whole_column_waves(Mb, N, wave):
+    order = xcd_grouped(Mb, N, wave)
+    assert sorted(order) == list(range(Mb * N))
+    C = max(1, wave // Mb)
+    done = set()
+    for r, t in enumerate(order):  # column blocks complete wave by wave
+        assert t // Mb < (r // (C * Mb) + 1) * C
+        done.add(t)
+    if Mb == 16 and N == 112 and wave == 512:  # prefill: XCD x holds an 8 x 8 sub-block of each wave
+        for x in range(8):
+            tiles = [order[8 * j + x] for j in range(64)]
+            assert len({t % Mb for t in tiles}) == 8 and len({t // Mb for t in tiles}) == 8
