@@ -180,7 +180,9 @@ int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
  * for section s (0 = the GEMM1 kernel or the pipelined kernel, 1 = the GEMM2
  * kernel of the sequential mode) and work-group g of that launch, the block
  * at uint64 offset (s * G + g) * (1 + 8 * records_per_group) holds the
- * item count, then one record per item of 8 uint64: item rank, start,
+ * item count, then one record per item of 8 uint64: the item's rank (high
+ * 32 bits) and its order-table entry (low 32 bits: the GEMM1 item id
+ * tile * S1 + s, or for a GEMM2 item 0x80000000 | (tile * S2 + s)), start,
  * mainloop end, two epilogue marks, end (times on the 100 MHz device
  * real-time counter; the marks are: for a GEMM1 tile that signals, its Z
  * stores complete and its ready counter released; for a split-K part that

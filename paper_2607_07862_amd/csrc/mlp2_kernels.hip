@@ -66,22 +66,23 @@ __device__ __forceinline__ Claim make_claim(const Args& a) {
 // Layout of the trace buffer: per kernel section (0 = GEMM1 or pipelined
 // kernel, 1 = GEMM2 kernel of the sequential mode; trace_groups work-groups
 // per section) and work-group, one word
-// with the item count, then trace_cap records of kTraceWords words: rank,
-// start, mainloop end, two epilogue marks (a signalling GEMM1 tile: Z stores
+// with the item count, then trace_cap records of kTraceWords words: rank
+// (high half) and item (low half: the order-table entry, bit 31 set for a
+// GEMM2 item), start, mainloop end, two epilogue marks (a signalling GEMM1 tile: Z stores
 // complete, ready counter released; a split-K part that leaves the tile to a
 // sibling: partial stored, arrival counted; else 0 and 0), end, ring-wait
 // ticks, flag-wait ticks.  Records past
 // trace_cap are counted, not stored.  Written by thread 0 with plain stores.
 __device__ __forceinline__ void tr_mark_mainloop(TraceAcc& tr) { tr.t_main = trace_now(); }
 
-__device__ __forceinline__ void tr_record(const Args& a, int section, int n, int ticket, uint64_t t_start,
-                                          const TraceAcc& tr) {
+__device__ __forceinline__ void tr_record(const Args& a, int section, int n, int rank, uint32_t item,
+                                          uint64_t t_start, const TraceAcc& tr) {
   if (a.trace == nullptr || threadIdx.x != 0) return;
   uint64_t* slot = a.trace + ((long)section * a.trace_groups + blockIdx.x) * (1 + (long)a.trace_cap * kTraceWords);
   slot[0] = (uint64_t)(n + 1);
   if (n >= a.trace_cap) return;
   uint64_t* r = slot + 1 + (long)n * kTraceWords;
-  r[0] = (uint64_t)ticket;
+  r[0] = ((uint64_t)(uint32_t)rank << 32) | item;
   r[1] = t_start;
   r[2] = tr.t_main;
   r[3] = tr.t_rel;
@@ -325,18 +326,22 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
     TraceAcc tr;
     const uint64_t t_start = trace_now();
     Claim next = make_claim(a);
+    uint32_t e;  // order-table entry: item id, bit 31 set for a GEMM2 item
     if constexpr (PHASE == PHASE_PIPELINED) {
-      const uint32_t e = uniform(a.orderp[p]);
+      e = uniform(a.orderp[p]);
       if (e & 0x80000000u)
         gemm2_item<T2, HV, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr);
       else
         gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
     } else if constexpr (PHASE == PHASE_GEMM1) {
-      gemm1_item<T1, NB>(a, (int)a.order1[p], epoch, lds, &s_slot, next, &s_item, tr);
+      e = uniform(a.order1[p]);
+      gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
     } else {
-      gemm2_item<T2, HV, false>(a, (int)a.order2[p], epoch, lds, &s_slot, next, &s_item, tr);
+      e = uniform(a.order2[p]);
+      gemm2_item<T2, HV, false>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
+      e |= 0x80000000u;
     }
-    if constexpr (kTrace) tr_record(a, PHASE == PHASE_GEMM2 ? 1 : 0, n_items++, p, t_start, tr);
+    if constexpr (kTrace) tr_record(a, PHASE == PHASE_GEMM2 ? 1 : 0, n_items++, p, e, t_start, tr);
     __syncthreads();
     p = uniform(s_item);
   }

@@ -12,6 +12,10 @@
         by bench.py, tagged with the hash of the kernel sources) and
         OUT_STEM.md.
 
+    python -m paper_2607_07862_amd.profsum counters OUT.md DIR [DIR ...] --cmd "<command>" [--cmd ...]
+        Per-kernel means of every counter of one or more ``--pmc`` runs
+        (and the L2 hit rate when TCC_HIT and TCC_MISS were collected).
+
 Reads CSV files only; runs nothing.
 """
 from __future__ import annotations
@@ -142,6 +146,38 @@ def traffic(args):
     print(args.out_stem + ".json")
 
 
+def counters(args):
+    """Per-kernel means (over dispatches) of every counter of one or more --pmc runs."""
+    per = defaultdict(lambda: defaultdict(list))  # kernel -> counter -> values per dispatch
+    for d in args.dirs:
+        f = _one(os.path.join(d, "**", "*counter_collection.csv"))
+        acc = defaultdict(lambda: defaultdict(float))
+        for r in csv.DictReader(open(f)):
+            if "k_mlp2" not in r["Kernel_Name"]:
+                continue
+            acc[(r["Kernel_Name"], r["Dispatch_Id"])][r["Counter_Name"]] += float(r["Counter_Value"])
+        for (k, _), cs in acc.items():
+            for c, v in cs.items():
+                per[k][c].append(v)
+    lines = [f"# {args.title}", "", "Commands (from the repository root on the GPU host), one counter pass each:", ""]
+    for c in args.cmd:
+        lines += ["```", c, "```", ""]
+    names = sorted({c for k in per for c in per[k]})
+    lines += ["| kernel | " + " | ".join(names) + " |", "|---|" + "---:|" * len(names)]
+    for k in sorted(per, key=short_name):
+        vals = [sum(per[k][c]) / len(per[k][c]) if per[k][c] else float("nan") for c in names]
+        lines.append(f"| {short_name(k)} | " + " | ".join(f"{v:,.0f}" for v in vals) + " |")
+    hit, miss = "TCC_HIT_sum", "TCC_MISS_sum"
+    if hit in names and miss in names:
+        lines += ["", "L2 hit rate per kernel (TCC_HIT / (TCC_HIT + TCC_MISS)):", ""]
+        for k in sorted(per, key=short_name):
+            if per[k][hit] and per[k][miss]:
+                h, m = sum(per[k][hit]) / len(per[k][hit]), sum(per[k][miss]) / len(per[k][miss])
+                lines.append(f"- {short_name(k)}: {100 * h / (h + m):.1f} %")
+    open(args.out, "w").write("\n".join(lines) + "\n")
+    print(args.out)
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd_name", required=True)
@@ -158,8 +194,13 @@ def main():
     t.add_argument("--copy-mib", type=int, required=True)
     t.add_argument("--cmd-fetch", required=True)
     t.add_argument("--cmd-write", required=True)
+    c = sub.add_parser("counters")
+    c.add_argument("out")
+    c.add_argument("dirs", nargs="+")
+    c.add_argument("--cmd", action="append", required=True)
+    c.add_argument("--title", default="rocprofv3 counters")
     a = ap.parse_args()
-    (stats if a.cmd_name == "stats" else traffic)(a)
+    {"stats": stats, "traffic": traffic, "counters": counters}[a.cmd_name](a)
 
 
 if __name__ == "__main__":

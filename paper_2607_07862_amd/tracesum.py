@@ -1,0 +1,151 @@
+"""Where the time of one run goes, from the per-item timing trace.
+
+    python -m paper_2607_07862_amd.tracesum [--workloads a,b,...] [--out FILE.md]
+
+Needs the trace build (``python -m paper_2607_07862_amd.build --trace``) and
+a GPU.  For each workload (device-drawn inputs of its shapes): warm-up runs,
+then one traced warm run per mode.  Per item kind it reports the mean item
+time split into mainloop, waits for the work-group's own ring loads, waits
+for ready counters (flag waits) and epilogue, and for the GEMM2 items of the
+pipelined mode the share of their time spent in flag waits beside the wait
+their producers' completion times imply (the latest end among the GEMM1
+items that write the Z columns the item reads, minus the item's start).
+"""
+from __future__ import annotations
+
+import argparse
+import os
+import sys
+
+os.environ["MLP2_TRACE"] = "1"
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+TICK_US = 0.01  # 100 MHz device real-time counter
+CAP = 64        # records per work-group
+
+
+def _records(buf, G):
+    """(kind, item, rank, start, main, end, ring, flag) per recorded item, sections merged."""
+    import numpy as np
+
+    a = buf.cpu().numpy().reshape(2, G, 1 + 8 * CAP)
+    out = []
+    for sec in (0, 1):
+        for g in range(G):
+            n = min(int(a[sec, g, 0]), CAP)
+            for j in range(n):
+                r = a[sec, g, 1 + 8 * j: 9 + 8 * j].astype(np.uint64)
+                w0 = int(r[0])
+                entry, rank = w0 & 0xFFFFFFFF, w0 >> 32
+                kind = 1 if entry & 0x80000000 else 0
+                out.append((kind, entry & 0x7FFFFFFF, rank, int(r[1]), int(r[2]), int(r[5]), int(r[6]), int(r[7])))
+    return out
+
+
+def _dependencies(info, F):
+    """GEMM2 item -> GEMM1 tiles whose Z columns it reads (closed form of the plan)."""
+    Mb, S2, bn1 = info["row_blocks"], info["splitk2"], info["bn1"]
+    per = -(-F // S2)              # ceil(F / S2), as the plan splits K ...
+    kc2 = -(-per // 64) * 64       # ... rounded up to whole 64-deep stages
+    deps = {}
+    for q in range(info["items2"]):
+        tile, s = divmod(q, S2)
+        mb = tile % Mb
+        kb0, kb1 = s * kc2 // bn1, (min(F, (s + 1) * kc2) - 1) // bn1
+        deps[q] = [kb * Mb + mb for kb in range(kb0, kb1 + 1)]
+    return deps
+
+
+def summarise(B, I, bench, key):
+    import numpy as np
+    import torch
+
+    w = I.WORKLOADS[key]
+    g = bench.device_random_inputs(w)
+    r = bench.Runner(B, w, g, None, torch.cuda.current_stream())
+    info = r.info
+    G = max(info["grid_pipelined"], info["grid_gemm1"], info["grid_gemm2"])
+    buf = torch.zeros(2 * G * (1 + 8 * CAP), dtype=torch.int64, device="cuda")
+    for _ in range(5):
+        r.run(B.MODE_TILE_PIPELINED)
+        r.run(B.MODE_SEQUENTIAL)
+    torch.cuda.synchronize()
+    rows = []
+    for mode, name in ((B.MODE_SEQUENTIAL, "sequential"), (B.MODE_TILE_PIPELINED, "pipelined")):
+        buf.zero_()
+        r.plan.attach_trace(buf, CAP)
+        r.run(mode)
+        torch.cuda.synchronize()
+        r.plan.attach_trace(None, 1)
+        recs = _records(buf, G)
+        t0 = min(x[3] for x in recs)
+        span = (max(x[5] for x in recs) - t0) * TICK_US
+        for kind in (0, 1):
+            K = [x for x in recs if x[0] == kind]
+            if not K:
+                continue
+            R = np.array([x[3:] for x in K], dtype=np.float64)  # start, main, end, ring, flag
+            item = (R[:, 2] - R[:, 0]) * TICK_US
+            main = (R[:, 1] - R[:, 0]) * TICK_US
+            ring, flag = R[:, 3] * TICK_US, R[:, 4] * TICK_US
+            row = {
+                "mode": name, "kind": "GEMM1" if kind == 0 else "GEMM2", "n": len(K), "span": span,
+                "item": item.mean(), "main": main.mean(), "ring": ring.mean(), "flag": flag.mean(),
+                "epi": (item - main).mean(), "flag_share": flag.sum() / item.sum(),
+            }
+            if kind == 1 and name == "pipelined":
+                S1 = info["splitk1"]
+                ready = {}
+                for x in recs:
+                    if x[0] == 0:
+                        t = x[1] // S1
+                        ready[t] = max(ready.get(t, 0), x[5])
+                deps = _dependencies(info, w.F)
+                exp = [max(0.0, (max(ready[t] for t in deps[x[1]]) - x[3]) * TICK_US) for x in K]
+                row["implied"] = float(np.mean(exp))
+            rows.append(row)
+    r.check()
+    r.close()
+    del g
+    torch.cuda.empty_cache()
+    tiles = [info[k] for k in ("bm", "bn1", "splitk1", "bn2", "splitk2", "stages")]
+    return w, tiles, rows
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workloads", default="tiny,l8b_decode,l8b_prefill,l70b_gated,l70b_shard8")
+    ap.add_argument("--out", default=None)
+    args = ap.parse_args()
+    from paper_2607_07862_amd import binding as B
+    from paper_2607_07862_amd import inputs as I
+    import bench
+
+    B.load()
+    lines = ["| workload | mode | launch µs | kind | items | item µs | mainloop µs | ring wait µs | flag wait µs | epilogue µs | flag share | producer-implied wait µs |",
+             "|---|---|---:|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for key in args.workloads.split(","):
+        w, tiles, rows = summarise(B, I, bench, key)
+        for x in rows:
+            implied = f"{x['implied']:.1f}" if "implied" in x else ""
+            lines.append(f"| {key} {tiles} | {x['mode']} | {x['span']:.1f} | {x['kind']} | {x['n']} | {x['item']:.1f} | "
+                         f"{x['main']:.1f} | {x['ring']:.1f} | {x['flag']:.1f} | {x['epi']:.2f} | {100 * x['flag_share']:.1f} % | {implied} |")
+        print(lines[-1] if rows else key, flush=True)
+    cmd = " ".join(["python -m paper_2607_07862_amd.tracesum"] + sys.argv[1:])
+    head = ["# Flag waits and where item time goes (timing-trace build, one warm run per mode)", "",
+            "Command (from the repository root on the GPU host, after `python -m paper_2607_07862_amd.build --trace`):", "",
+            "```", cmd, "```", "",
+            "Times are means over the items of a kind; the flag share is the kind's flag-wait time over its item",
+            "time; the producer-implied wait is, per GEMM2 item of the pipelined run, the latest end among the GEMM1",
+            "items writing the Z columns it reads minus its start (0 when they were done before it started).", ""]
+    text = "\n".join(head + lines) + "\n"
+    if args.out:
+        with open(args.out, "w") as f:
+            f.write(text)
+    else:
+        print(text)
+
+
+if __name__ == "__main__":
+    main()
