@@ -13,7 +13,11 @@ events on the stream it is launched on), HBM traffic from committed
 rocprofv3 counter summaries when they match the current kernel sources, a
 table of both modes on every MLP workload (beside eager PyTorch on the same
 inputs, hipBLASLt GEMMs plus an activation kernel, as a reference point), and
-the fp64 CPU oracle timed on a bounded sample of the headline workload.
+the fp64 CPU oracle timed on a bounded sample of the headline workload.  Two
+more legs guard the comparison: both modes timed run by run in alternating
+order (medians, p10/p90), and what the GPU attains outside the library (a
+4 GiB read-only stream, an 8192^3 hipBLASLt GEMM) as context for the
+roofline fractions, which stay against the published peaks.
 
 Only ``--gpus 1`` is supported: the build targets a single GPU.
 """
@@ -179,6 +183,25 @@ class Runner:
         torch.cuda.synchronize()
         return {m: [a.elapsed_time(b) * 1e3 for a, b in v] for m, v in out.items()}
 
+    def interleaved(self, iters):
+        """Per-run µs of both modes, run by run in alternating order (ABBA...), warm.
+
+        Clock and thermal drift then reach both modes alike, which back-to-back
+        blocks of one mode do not guarantee."""
+        import torch
+
+        out = {self.B.MODE_TILE_PIPELINED: [], self.B.MODE_SEQUENTIAL: []}
+        order = (self.B.MODE_TILE_PIPELINED, self.B.MODE_SEQUENTIAL)
+        for i in range(iters):
+            for m in (order if i % 2 == 0 else order[::-1]):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(self.stream)
+                self.run(m)
+                b.record(self.stream)
+                out[m].append((a, b))
+        torch.cuda.synchronize()
+        return {m: [a.elapsed_time(b) * 1e3 for a, b in v] for m, v in out.items()}
+
     def check(self):
         if self.plan.check() != self.B.OK:
             raise RuntimeError(f"{self.w.name}: a device flag wait timed out")
@@ -190,6 +213,46 @@ class Runner:
 def pct(v, q):
     v = sorted(v)
     return v[min(len(v) - 1, max(0, int(round(q * (len(v) - 1)))))]
+
+
+def attainable():
+    """What this GPU reaches outside the library, as context for the roofline
+    fractions (which stay against the published peaks): a read-only stream of
+    4 GiB (row maxima of a [65536, 16384] fp32 view, far beyond the 256 MB
+    last-level cache; a single full reduction reads at little more than half
+    that rate) and an 8192^3 bf16 GEMM through torch.matmul (hipBLASLt).
+    Best of 5 runs each."""
+    import torch
+
+    buf = torch.ones(65536, 16384, dtype=torch.float32, device="cuda")
+    sink = torch.empty(65536, dtype=torch.float32, device="cuda")
+    a = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    b = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    c = torch.empty(8192, 8192, dtype=torch.bfloat16, device="cuda")
+
+    def best(f, n=5):
+        f()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(n):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            f()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        return min(ts)
+
+    t_read = best(lambda: torch.amax(buf, dim=1, out=sink))
+    t_gemm = best(lambda: torch.matmul(a, b, out=c))
+    out = {
+        "hbm_read_GBs": round(buf.numel() * 4 / t_read / 1e9, 1),
+        "bf16_gemm_TFLOPs": round(2 * 8192 ** 3 / t_gemm / 1e12, 1),
+        "how": "4 GiB read-only stream (row maxima, torch.amax) and an 8192^3 bf16 torch.matmul (hipBLASLt), best of 5",
+    }
+    del buf, a, b, c
+    torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(w, d, budget_s: float):
@@ -239,6 +302,9 @@ def main():
     ap.add_argument("--tuning", default="", help="JSON dict of mlp2_tuning_t fields")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--cold-iters", type=int, default=20)
+    ap.add_argument("--interleave-iters", type=int, default=100,
+                    help="warm runs per mode timed one by one in alternating order (0 skips; a third of it per table row)")
+    ap.add_argument("--no-attainable", action="store_true", help="skip the stream and library-GEMM references")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--no-table", action="store_true", help="skip the table of all workloads")
     ap.add_argument("--only-pipelined", action="store_true", help="time the pipelined mode only (profiling runs)")
@@ -313,6 +379,20 @@ def main():
                 "flush": "1 GiB device read before each timed run (evicts L2 and the last-level cache), modes interleaved",
             }
             log(f"cold: pipelined {extra['cold']['pipelined_median_us']} us, sequential {extra['cold']['sequential_median_us']} us")
+        if args.interleave_iters > 0:
+            iv = r.interleaved(args.interleave_iters)
+            ip, is_ = iv[B.MODE_TILE_PIPELINED], iv[B.MODE_SEQUENTIAL]
+            mp, ms = statistics.median(ip), statistics.median(is_)
+            extra["interleaved"] = {
+                "pipelined_median_us": round(mp, 2),
+                "pipelined_p10_p90_us": [round(pct(ip, 0.1), 2), round(pct(ip, 0.9), 2)],
+                "sequential_median_us": round(ms, 2),
+                "sequential_p10_p90_us": [round(pct(is_, 0.1), 2), round(pct(is_, 0.9), 2)],
+                "gain_median_pct": round((ms - mp) / ms * 100, 2),
+                "iters": args.interleave_iters,
+                "how": "warm, one HIP event pair per run, modes alternating run by run",
+            }
+            log(f"interleaved: pipelined {mp:.2f} us, sequential {ms:.2f} us")
     r.check()
     info = r.info
     roof = roofline(w, value)
@@ -326,9 +406,12 @@ def main():
         for key in I.WORKLOAD_ORDER:
             wk = I.WORKLOADS[key]
             steps = max(10, args.steps // 2)
+            iters = max(10, args.interleave_iters // 3)
             if key == args.workload:
                 rr_p, rr_s, inf = value, extra["sequential_us"], info
                 te = torch_eager_us(wk, g, steps)
+                iv = extra.get("interleaved")
+                med = (iv["pipelined_median_us"], iv["sequential_median_us"]) if iv else None
             else:
                 gk = device_random_inputs(wk)
                 rr = Runner(B, wk, gk, None, stream)
@@ -337,6 +420,8 @@ def main():
                     rr.run(B.MODE_SEQUENTIAL)
                 rr_p = rr.block(B.MODE_TILE_PIPELINED, steps)
                 rr_s = rr.block(B.MODE_SEQUENTIAL, steps)
+                ivk = rr.interleaved(iters)
+                med = (statistics.median(ivk[B.MODE_TILE_PIPELINED]), statistics.median(ivk[B.MODE_SEQUENTIAL]))
                 rr.check()
                 inf = rr.info
                 rr.close()
@@ -355,8 +440,24 @@ def main():
                 "mfma_frac": round(wk.alg_flops() / (rr_p * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
                 "tiles": [inf["bm"], inf["bn1"], inf["splitk1"], inf["bn2"], inf["splitk2"], inf["stages"]],
             }
+            if med:
+                row["interleaved_median_us"] = {"pipelined": round(med[0], 2), "sequential": round(med[1], 2),
+                                                "gain_pct": round((med[1] - med[0]) / med[1] * 100, 1)}
             table[key] = row
             log(f"TABLE {key:12s} {row}")
+
+    att = None
+    if not args.no_attainable:
+        att = attainable()
+        log(f"attainable: {att}")
+        roof["frac_of_attainable"] = round(
+            roof["achieved"] / (att["hbm_read_GBs"] if roof["bound"] == "hbm" else att["bf16_gemm_TFLOPs"]), 4)
+        for key, row in table.items():
+            wk = I.WORKLOADS[key]
+            t = row["pipelined_us"] * 1e-6
+            row["frac_of_attainable"] = round(
+                wk.alg_bytes() / t / 1e9 / att["hbm_read_GBs"] if row["bound"] == "hbm"
+                else wk.alg_flops() / t / 1e12 / att["bf16_gemm_TFLOPs"], 4)
 
     cpu = None
     if not args.no_cpu:
@@ -390,6 +491,7 @@ def main():
         "alg_bytes": w.alg_bytes(),
         "alg_flops": w.alg_flops(),
         "roofline": roof,
+        "attainable": att,
         "cpu_baseline": cpu,
         "workloads": table,
     }
