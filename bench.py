@@ -6,7 +6,8 @@ signals + GEMM2) over one batch of synthetic inputs already resident in HBM.
 W warm-up steps, then exactly K back-to-back steps of the tile-pipelined mode
 timed between a synchronise on each side; ``value`` is that block's mean
 latency per step.  Beside it the line carries the sequential mode's latency
-(same block timing), cold latencies of both modes (a 1 GiB read evicts the
+(same block timing), the workqueue mode's (the paper's scoreboard-and-queue
+scheduling of GEMM2 units, same block timing), cold latencies of both modes (a 1 GiB read evicts the
 L2s and the 256 MB MALL before each timed run, modes interleaved), the
 roofline fraction of the dominant kernel (the pipelined launch, timed with HIP
 events on the stream it is launched on), HBM traffic from committed
@@ -351,6 +352,7 @@ def main():
         r.run(B.MODE_TILE_PIPELINED)
         if not args.only_pipelined:
             r.run(B.MODE_SEQUENTIAL)
+            r.run(B.MODE_WORKQUEUE)
     torch.cuda.synchronize()
     r.check()
     log(f"timing {args.steps} pipelined steps")
@@ -358,10 +360,12 @@ def main():
     extra = {}
     if not args.only_pipelined:
         seq_us = r.block(B.MODE_SEQUENTIAL, args.steps)
+        wq_us = r.block(B.MODE_WORKQUEUE, args.steps)
         pipe2 = r.block(B.MODE_TILE_PIPELINED, args.steps)
-        log(f"pipelined {value:.2f} us (repeat {pipe2:.2f}), sequential {seq_us:.2f} us")
+        log(f"pipelined {value:.2f} us (repeat {pipe2:.2f}), sequential {seq_us:.2f} us, workqueue {wq_us:.2f} us")
         extra = {
             "sequential_us": round(seq_us, 3),
+            "workqueue_us": round(wq_us, 3),
             "pipelined_repeat_us": round(pipe2, 3),
             "gain_vs_sequential_pct": round((seq_us - value) / seq_us * 100, 2),
         }
@@ -408,7 +412,7 @@ def main():
             steps = max(10, args.steps // 2)
             iters = max(10, args.interleave_iters // 3)
             if key == args.workload:
-                rr_p, rr_s, inf = value, extra["sequential_us"], info
+                rr_p, rr_s, rr_q, inf = value, extra["sequential_us"], extra["workqueue_us"], info
                 te = torch_eager_us(wk, g, steps)
                 iv = extra.get("interleaved")
                 med = (iv["pipelined_median_us"], iv["sequential_median_us"]) if iv else None
@@ -418,8 +422,10 @@ def main():
                 for _ in range(30):
                     rr.run(B.MODE_TILE_PIPELINED)
                     rr.run(B.MODE_SEQUENTIAL)
+                    rr.run(B.MODE_WORKQUEUE)
                 rr_p = rr.block(B.MODE_TILE_PIPELINED, steps)
                 rr_s = rr.block(B.MODE_SEQUENTIAL, steps)
+                rr_q = rr.block(B.MODE_WORKQUEUE, steps)
                 ivk = rr.interleaved(iters)
                 med = (statistics.median(ivk[B.MODE_TILE_PIPELINED]), statistics.median(ivk[B.MODE_SEQUENTIAL]))
                 rr.check()
@@ -433,6 +439,7 @@ def main():
                 "pipelined_us": round(rr_p, 2),
                 "sequential_us": round(rr_s, 2),
                 "gain_pct": round((rr_s - rr_p) / rr_s * 100, 1),
+                "workqueue_us": round(rr_q, 2),
                 "torch_eager_us": round(te, 2),
                 "bound": rf["bound"],
                 "frac": rf["frac"],

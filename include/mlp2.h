@@ -8,7 +8,7 @@
  *     Z = act(X . W1)        first GEMM, fused activation epilogue
  *     Y = Z . W2             second GEMM
  *
- * Two execution modes compute bit-identical Y:
+ * Three execution modes compute bit-identical Y:
  *   MLP2_MODE_SEQUENTIAL      GEMM1 then GEMM2, two kernels on the stream.
  *   MLP2_MODE_TILE_PIPELINED  one persistent launch; a GEMM2 work-group
  *                             consumes each K-slice of Z as soon as the GEMM1
@@ -17,6 +17,13 @@
  *                             fences, then signals; consumer prologue polls;
  *                             Sec. III-A.5 host organisation; Sec. III-B.2
  *                             persistent kernels fetching work tiles).
+ *   MLP2_MODE_WORKQUEUE       one persistent launch with the paper's own
+ *                             consumer scheduling (Sec. III-A.2-3): each
+ *                             completed GEMM1 tile counts down the scoreboard
+ *                             of every GEMM2 unit that reads it, the producer
+ *                             completing a unit pushes it onto a device
+ *                             ring-buffer workqueue, and work-groups that run
+ *                             out of GEMM1 items pop whole units from it.
  *
  * Data layout (all device memory, row-major, bf16, 16-byte aligned):
  *   X   [M, H]            input activations             (caller owns)
@@ -55,7 +62,7 @@ typedef struct mlp2_plan_s* mlp2_plan_t; /* opaque; created by mlp2_plan, freed 
 
 enum mlp2_act { MLP2_ACT_IDENTITY = 0, MLP2_ACT_GELU_TANH = 1, MLP2_ACT_SWIGLU = 2 };
 enum mlp2_dtype { MLP2_DTYPE_BF16 = 0 };
-enum mlp2_mode { MLP2_MODE_SEQUENTIAL = 0, MLP2_MODE_TILE_PIPELINED = 1 };
+enum mlp2_mode { MLP2_MODE_SEQUENTIAL = 0, MLP2_MODE_TILE_PIPELINED = 1, MLP2_MODE_WORKQUEUE = 2 };
 
 enum mlp2_status {
   MLP2_OK = 0,

@@ -46,6 +46,8 @@ struct mlp2_plan_s {
   uint32_t* cnt1 = nullptr;
   uint32_t* cnt2 = nullptr;
   uint32_t* ready = nullptr;
+  uint32_t* board = nullptr;
+  uint32_t* queue = nullptr;
   uint32_t* ctrl = nullptr;
   uint32_t* order1 = nullptr;
   uint32_t* order2 = nullptr;
@@ -333,8 +335,8 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   p->Mb = ceil_div(M, bm);
   p->Nb1 = (int)(F / bn1);
   p->Nb2 = (int)(H / bn2);
-  int occ[3] = {0, 0, 0};
-  for (int w = 0; w < 3; ++w) {
+  int occ[4] = {0, 0, 0, 0};
+  for (int w = 0; w < 4; ++w) {
     if (mlp2::occupancy(p->kc, w, &occ[w]) != hipSuccess || occ[w] < 1) {
       delete p;
       fail(MLP2_ERR_HIP);
@@ -359,7 +361,7 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   p->items2 = tiles2 * p->S2;
 
   p->occupancy = occ[2];
-  p->max_grid = std::min(std::min(occ[0], occ[1]), occ[2]) * p->num_cus;
+  p->max_grid = std::min(std::min(occ[0], occ[1]), std::min(occ[2], occ[3])) * p->num_cus;
   if (tz.grid > p->max_grid) {
     delete p;
     fail(MLP2_ERR_UNSUPPORTED);
@@ -368,7 +370,12 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   p->grid_override = tz.grid;
   p->grid1 = std::min(occ[0] * p->num_cus, p->items1);
   p->grid2 = std::min(occ[1] * p->num_cus, p->items2);
-  p->grid = std::min(occ[2] * p->num_cus, p->items1 + p->items2);
+  p->grid = std::min(std::min(occ[2], occ[3]) * p->num_cus, p->items1 + p->items2);
+  if (p->items2 >= (1 << 24)) {  // workqueue entries hold a unit id in 24 bits
+    delete p;
+    fail(MLP2_ERR_UNSUPPORTED);
+    return nullptr;
+  }
 
   // ---- workspace: Z, partials, counters, order table
   const int64_t Mpad = (int64_t)p->Mb * bm;
@@ -387,6 +394,10 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   off = align_up(off + (size_t)tiles2 * line, 256);
   const size_t r_off = off;
   off = align_up(off + (size_t)tiles1 * line, 256);
+  const size_t b_off = off;
+  off = align_up(off + (size_t)p->items2 * line, 256);
+  const size_t q_off = off;
+  off = align_up(off + ((size_t)p->items2 + 1) * 4, 256);
   const size_t ctrl_off = off;
   off = align_up(off + mlp2::CTRL_WORDS * 4, 256);
   const size_t cnt_end = off;
@@ -409,6 +420,8 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   p->cnt1 = (uint32_t*)(b + c1_off);
   p->cnt2 = (uint32_t*)(b + c2_off);
   p->ready = (uint32_t*)(b + r_off);
+  p->board = (uint32_t*)(b + b_off);
+  p->queue = (uint32_t*)(b + q_off);
   p->ctrl = (uint32_t*)(b + ctrl_off);
   p->order1 = (uint32_t*)(b + ord_off);
   p->order2 = (uint32_t*)(b + ord2_off);
@@ -431,7 +444,8 @@ mlp2_plan_t mlp2_plan(int64_t M, int64_t H, int64_t F, int act, int dtype) {
 
 int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void* Y, void* stream, int mode) {
   if (!p || !X || !W1 || !W2 || !Y) return fail(MLP2_ERR_INVALID_ARG);
-  if (mode != MLP2_MODE_SEQUENTIAL && mode != MLP2_MODE_TILE_PIPELINED) return fail(MLP2_ERR_INVALID_ARG);
+  if (mode != MLP2_MODE_SEQUENTIAL && mode != MLP2_MODE_TILE_PIPELINED && mode != MLP2_MODE_WORKQUEUE)
+    return fail(MLP2_ERR_INVALID_ARG);
   if (((uintptr_t)X | (uintptr_t)W1 | (uintptr_t)W2 | (uintptr_t)Y) & 15u) return fail(MLP2_ERR_ALIGNMENT);
   const int nb = p->act == MLP2_ACT_SWIGLU ? 2 : 1;
   const size_t xb = (size_t)p->M * p->H * 2, w1b = (size_t)nb * p->H * p->F * 2, w2b = (size_t)p->F * p->H * 2;
@@ -450,6 +464,8 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   a.cnt1 = p->cnt1;
   a.cnt2 = p->cnt2;
   a.ready = p->ready;
+  a.board = p->board;
+  a.queue = p->queue;
   a.ctrl = p->ctrl;
   a.order1 = p->order1;
   a.order2 = p->order2;
@@ -494,10 +510,14 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
     a2.lists = claim_lists(grids[1]);
     a2.first_static = statics(p->items2, grids[1]);  // nor do GEMM2 items of this mode
     err = mlp2::launch_sequential(p->kc, a, a2, grids, s);
-  } else {
+  } else if (mode == MLP2_MODE_TILE_PIPELINED) {
     a.lists = claim_lists(gridp);
     a.first_static = statics(p->lead1, gridp);
     err = mlp2::launch_pipelined(p->kc, a, gridp, s);
+  } else {
+    a.lists = claim_lists(gridp);
+    a.first_static = statics(p->items1, gridp);  // every ranked item is a GEMM1 item
+    err = mlp2::launch_workqueue(p->kc, a, gridp, s);
   }
   if (err != hipSuccess) return fail(MLP2_ERR_HIP);
   return MLP2_OK;

@@ -38,7 +38,10 @@ enum {
   CTRL_DONE_ALL = 2 * kLine,       // claim lists of the current kernel whose work-groups have all finished
   CTRL_TICKET = 3 * kLine,         // CTRL_TICKET + l * kLine: next ticket of claim list l (up to 8 lists)
   CTRL_DONE = 11 * kLine,          // CTRL_DONE + l * kLine: finished work-groups of claim list l
-  CTRL_WORDS = 19 * kLine
+  CTRL_QHEAD = 19 * kLine,         // workqueue mode: next queue slot a consumer claims
+  CTRL_QTAIL = 20 * kLine,         // workqueue mode: next queue slot a producer fills
+  CTRL_EPOCH_WQ = 21 * kLine,      // workqueue runs completed (the scoreboards advance in those only)
+  CTRL_WORDS = 22 * kLine
 };
 __device__ __forceinline__ int ctrl_ticket(int l) { return CTRL_TICKET + l * kLine; }
 __device__ __forceinline__ int ctrl_done(int l) { return CTRL_DONE + l * kLine; }
@@ -56,6 +59,9 @@ struct Args {
   uint32_t* cnt1;      // split-K arrival counters of GEMM1: tile t at word t * kLine
   uint32_t* cnt2;      // split-K arrival counters of GEMM2: tile t at word t * kLine
   uint32_t* ready;     // ready counters: tile (mb, nb1) at word (nb1 * Mb + mb) * kLine
+  uint32_t* board;     // workqueue mode: scoreboard of GEMM2 unit q at word q * kLine
+  uint32_t* queue;     // workqueue mode: ring of ready GEMM2 units, items2 + 1 slots (one per unit and
+                       // run, and a spare)
   uint32_t* ctrl;      // CTRL_* words
   const uint32_t* order1;  // GEMM1 item per rank of the GEMM1 kernel, length items1
   const uint32_t* order2;  // GEMM2 item per rank of the GEMM2 kernel, length items2
@@ -556,15 +562,22 @@ struct NoWait {
   __device__ __forceinline__ void operator()(int) {}
 };
 
-template <class Wait>
+template <class Wait, class C = Claim>
 struct ClaimAtLastStage {
   Wait& wait;
-  Claim* next;
+  C* next;
   int k_last;  // K offset of the item's last stage
   __device__ __forceinline__ void operator()(int k) {
     wait(k);
     if (k == k_last) next->issue();
   }
+};
+
+// The claim of an item whose successor comes from somewhere else (a
+// workqueue consumer pops its next unit after the item).
+struct NoClaim {
+  __device__ __forceinline__ void issue() {}
+  __device__ __forceinline__ void park(int*) const {}
 };
 
 // ------------------------------------------------------------------ ready flags
@@ -654,5 +667,112 @@ struct ReadyWait {
     if constexpr (kTrace) tr->flag += trace_now() - t0;
   }
 };
+
+// ------------------------------------------------------------------ workqueue mode
+//
+// The paper's own consumer scheduling (Sec. III-A.2-3): a scoreboard per
+// consumer unit counts its finished producers, and the producer that
+// completes a unit's count pushes the unit onto a ring-buffer workqueue from
+// which consumer work-groups pop whole units.  Here a unit is a GEMM2 item
+// (tile, split-K part) and its producers are the GEMM1 tiles of its row
+// block whose Z columns overlap its K range (a closed form, so no dependency
+// array is stored).  Counts only grow, and only in workqueue runs: with w
+// the number of earlier workqueue runs (CTRL_EPOCH_WQ), a unit with n
+// producers reaches (w + 1) * n in this run.  (The producers also signal
+// their ready counters, which thus advance once per run in every mode.)  A
+// queue entry carries the low 8 bits of w + 1 above the unit id, so a
+// consumer never takes a slot filled by an earlier run (every slot below
+// the run's unit count is rewritten in every workqueue run).  Every unit has at least one producer (the plan
+// makes S2 = ceil(F / kc2) parts, none of them empty), so every unit is
+// pushed exactly once per run.
+
+__device__ __forceinline__ uint32_t queue_tag(uint32_t wq_epoch) { return ((wq_epoch + 1u) & 0xffu) << 24; }
+
+// Producer side: every wave's Z stores of the tile are complete, then wave 0
+// increments the scoreboard of each unit that reads the tile, one unit per
+// lane (agent-scope release: the tile's Z lines are written back before the
+// count moves).  The units whose count this completes are then pushed one
+// at a time, in a scalar loop over the ballot: lane 0 reserves a queue slot
+// and publishes the unit with a release store.  The queue has one spare slot
+// past the run's unit count; a reservation beyond it (impossible: each unit
+// completes once per run) would land there, no consumer reads it, and the
+// unit's consumer would time out and report the error.
+__device__ __forceinline__ void push_ready(const Args& a, int tile, uint32_t wq_epoch) {
+  wait_all_mem();
+  __syncthreads();
+  if (uniform((int)(threadIdx.x >> 6)) == 0) {  // wave 0, as a scalar branch
+    const int lane = threadIdx.x & 63;
+    const int mb = tile % a.Mb, kb = tile / a.Mb;
+    const int k0 = kb * a.bn1, k1 = min(a.F, k0 + a.bn1) - 1;  // the tile's Z columns
+    const int s_lo = k0 / a.kc2, s_hi = k1 / a.kc2;            // the K ranges they fall in
+    const int units = a.Nb2 * (s_hi - s_lo + 1);
+    for (int i0 = 0; i0 < units; i0 += 64) {  // uniform trip count; one unit per lane
+      const int i = i0 + lane;
+      int q = 0;
+      bool complete = false;
+      if (i < units) {
+        const int s = s_lo + i / a.Nb2, nb2 = i % a.Nb2;
+        q = (nb2 * a.Mb + mb) * a.S2 + s;
+        const int kbeg = s * a.kc2, kend = min(a.F, kbeg + a.kc2);
+        const uint32_t n = (uint32_t)((kend - 1) / a.bn1 - kbeg / a.bn1 + 1);
+        const uint32_t old =
+            __hip_atomic_fetch_add(a.board + (long)q * kLine, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        complete = old + 1u == (wq_epoch + 1u) * n;
+      }
+      for (uint64_t m = __builtin_amdgcn_ballot_w64(complete); m; m &= m - 1) {
+        const uint32_t unit = (uint32_t)__builtin_amdgcn_readlane(q, (int)__builtin_ctzll(m));
+        if (lane == 0) {
+          const uint32_t slot = __hip_atomic_fetch_add(a.ctrl + CTRL_QTAIL, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(a.queue + min(slot, (uint32_t)a.items2), queue_tag(wq_epoch) | unit, __ATOMIC_RELEASE,
+                             __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
+  }
+}
+
+// Consumer side: wave 0 claims the next queue slot and polls it (every lane
+// at the same address, a scalar loop with uniform exits) until a producer of
+// this run has filled it, sleeping between polls; after spin_limit polls, or
+// once another wait gave up, it latches CTRL_ERROR and returns no unit.
+// Returns the unit for every wave, or -1 once the run's units are all
+// claimed.  Z visibility follows the ready counters' argument: every
+// producer of the unit released its Z lines before its increment, the
+// completing increment precedes the release store of the entry, and no L2
+// holds a Z line before a consumer has seen its producers complete.
+__device__ __forceinline__ int pop_ready(const Args& a, uint32_t wq_epoch, int* s_bcast) {
+  if (uniform((int)(threadIdx.x >> 6)) == 0) {  // wave 0, as a scalar branch
+    const int lane = threadIdx.x & 63;
+    uint32_t h = 0;
+    if (lane == 0) h = __hip_atomic_fetch_add(a.ctrl + CTRL_QHEAD, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    h = uniform(h);
+    int q = -1;
+    if (h < (uint32_t)a.items2) {
+      const uint32_t want = uniform(queue_tag(wq_epoch));
+      for (uint32_t polls = 0;; ++polls) {
+        const uint32_t v = uniform(ld_relaxed(a.queue + h));
+        if ((v & 0xff000000u) == want) {
+          q = (int)(v & 0x00ffffffu);
+          if (q >= a.items2) {  // not an entry any producer writes: give up loudly
+            if (lane == 0) __hip_atomic_fetch_or(a.ctrl + CTRL_ERROR, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            q = -1;
+          }
+          break;
+        }
+        if (polls >= a.spin_limit || ((polls & 63u) == 63u && uniform(ld_relaxed(a.ctrl + CTRL_ERROR)) != 0u)) {
+          if (lane == 0) __hip_atomic_fetch_or(a.ctrl + CTRL_ERROR, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+      }
+    }
+    if (lane == 0) *s_bcast = q;
+  }
+  __syncthreads();
+  const int q = uniform(*s_bcast);
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  __syncthreads();  // every wave has read the slot before wave 0 writes it again
+  return q;
+}
 
 }  // namespace mlp2

@@ -120,10 +120,11 @@ __device__ __forceinline__ void reduce_epilogue(const float* part, long tile, in
 // the others claim their next item at once.  A GEMM1 tile signals its ready
 // counter once per run, after the tile's Z rows are stored.
 
-// GEMM1 item id = tile * S1 + s, tile = nb * Mb + mb.
-template <class T, int NB>
+// GEMM1 item id = tile * S1 + s, tile = nb * Mb + mb.  WQ: the completed
+// tile also feeds the workqueue's scoreboards (wq_epoch: workqueue runs so far).
+template <class T, int NB, bool WQ = false>
 __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t epoch, char* lds, int* s_slot,
-                                           Claim& next, int* s_next, TraceAcc& tr) {
+                                           Claim& next, int* s_next, TraceAcc& tr, uint32_t wq_epoch = 0) {
   const int id = uniform(id_in);
   const int tile = id / a.S1, s = id - tile * a.S1;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
@@ -166,7 +167,10 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
     wait_all_mem();
     tr.t_rel = trace_now();
   }
-  if (tile != a.drop_signal) signal_ready(a.ready + (long)tile * kLine);
+  if (tile != a.drop_signal) {
+    signal_ready(a.ready + (long)tile * kLine);
+    if constexpr (WQ) push_ready(a, tile, wq_epoch);
+  }
   if constexpr (kTrace) tr.t_wait = trace_now();
 }
 
@@ -179,9 +183,9 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
 // kernel that holds both item kinds carries one mainloop shape and one
 // register budget.  Each output element still accumulates over K in the
 // same order.
-template <class T, int HV, bool WAIT>
+template <class T, int HV, bool WAIT, class C = Claim>
 __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epoch, char* lds, int* s_slot,
-                                           Claim& next, int* s_next, TraceAcc& tr) {
+                                           C& next, int* s_next, TraceAcc& tr) {
   const int p = uniform(p_in);
   const int tile = p / a.S2, s = p - (p / a.S2) * a.S2;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
@@ -197,11 +201,11 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
   if constexpr (WAIT) {
     ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1, epoch + 1u, a.spin_limit, s_slot,
                 -1, &tr};
-    ClaimAtLastStage<ReadyWait> hook{w, &next, kend - kBK};
+    ClaimAtLastStage<ReadyWait, C> hook{w, &next, kend - kBK};
     mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   } else {
     NoWait nowait;
-    ClaimAtLastStage<NoWait> hook{nowait, &next, kend - kBK};
+    ClaimAtLastStage<NoWait, C> hook{nowait, &next, kend - kBK};
     mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   }
   if constexpr (kTrace) tr_mark_mainloop(tr);
@@ -238,7 +242,8 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
 // stream-ordered before the plan's next kernel.  Spreading the done counts
 // over the lists keeps the exit atomics, one per work-group, off a single
 // line.
-__device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, bool end_of_run) {
+__device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, bool end_of_run, bool wq_run = false,
+                                              uint32_t wq_epoch = 0) {
   __syncthreads();
   if (threadIdx.x == 0) {
     const int l = (int)(blockIdx.x % (unsigned)a.lists);
@@ -251,6 +256,9 @@ __device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, boo
           __hip_atomic_fetch_add(a.ctrl + CTRL_DONE_ALL, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
       if (lists_done == (uint32_t)a.lists - 1u) {
         __hip_atomic_store(a.ctrl + CTRL_DONE_ALL, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(a.ctrl + CTRL_QHEAD, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(a.ctrl + CTRL_QTAIL, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (wq_run) __hip_atomic_store(a.ctrl + CTRL_EPOCH_WQ, wq_epoch + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (end_of_run) __hip_atomic_store(a.ctrl + CTRL_EPOCH, epoch + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
@@ -278,8 +286,15 @@ __device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, boo
 // every claimed item of its list ranks below u and is finished, so a
 // work-group of that list is free to claim it.  Hence no launch deadlocks for
 // any grid with at least one work-group per list, whatever the residency.
+//
+//   PHASE_WORKQUEUE: GEMM1 items by rank as in PHASE_GEMM1; a work-group whose
+//                    claim runs past them pops GEMM2 units from the device
+//                    workqueue until every unit of the run is claimed.  It
+//                    pops only once every GEMM1 item is claimed, and GEMM1
+//                    items never wait, so every producer finishes and every
+//                    claimed queue slot is filled: no deadlock either.
 
-enum { PHASE_GEMM1 = 0, PHASE_GEMM2 = 1, PHASE_PIPELINED = 2 };
+enum { PHASE_GEMM1 = 0, PHASE_GEMM2 = 1, PHASE_PIPELINED = 2, PHASE_WORKQUEUE = 3 };
 
 template <int A, int B>
 struct MaxI {
@@ -306,8 +321,9 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
   __shared__ __attribute__((aligned(1024))) char lds[kLds];
   __shared__ int s_item, s_slot;
   const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
+  const uint32_t wq_epoch = PHASE == PHASE_WORKQUEUE ? uniform(ld_relaxed(a.ctrl + CTRL_EPOCH_WQ)) : 0u;
   const int g1 = PHASE == PHASE_GEMM2 ? 0 : a.items1;
-  const int g2 = PHASE == PHASE_GEMM1 ? 0 : a.items2;
+  const int g2 = PHASE == PHASE_GEMM2 || PHASE == PHASE_PIPELINED ? a.items2 : 0;
   const int total = g1 + g2;
   int p;
   if ((int)blockIdx.x < a.first_static) {
@@ -333,9 +349,9 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
         gemm2_item<T2, HV, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr);
       else
         gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
-    } else if constexpr (PHASE == PHASE_GEMM1) {
+    } else if constexpr (PHASE == PHASE_GEMM1 || PHASE == PHASE_WORKQUEUE) {
       e = uniform(a.order1[p]);
-      gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
+      gemm1_item<T1, NB, PHASE == PHASE_WORKQUEUE>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr, wq_epoch);
     } else {
       e = uniform(a.order2[p]);
       gemm2_item<T2, HV, false>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
@@ -345,7 +361,18 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
     __syncthreads();
     p = uniform(s_item);
   }
-  finish_kernel(a, epoch, PHASE != PHASE_GEMM1);
+  if constexpr (PHASE == PHASE_WORKQUEUE) {
+    __syncthreads();  // every wave is done with s_item before pop_ready rewrites it
+    for (int q = pop_ready(a, wq_epoch, &s_item); q >= 0; q = pop_ready(a, wq_epoch, &s_item)) {
+      TraceAcc tr;
+      const uint64_t t_start = trace_now();
+      NoClaim none;
+      gemm2_item<T2, HV, false, NoClaim>(a, q, epoch, lds, &s_slot, none, &s_item, tr);
+      if constexpr (kTrace) tr_record(a, 0, n_items++, -1, 0x80000000u | (uint32_t)q, t_start, tr);
+      __syncthreads();  // the item's divergent stores close, and s_item is free again
+    }
+  }
+  finish_kernel(a, epoch, PHASE != PHASE_GEMM1, PHASE == PHASE_WORKQUEUE, wq_epoch);
 }
 
 // ------------------------------------------------------------------ dispatch table
@@ -370,6 +397,7 @@ struct Entry {
   const void* seq1;
   const void* seq2;
   const void* pipe;
+  const void* wq;
 };
 
 // GEMM2 of BN2 columns as one tile (HV = 1), or as two halves of BN2 / 2 that
@@ -379,7 +407,8 @@ struct Entry {
 #define MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, HV)                                                       \
   Entry {                                                                                             \
     BM, BN1, BN2, NB, NS, MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_GEMM1),                             \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_GEMM2), MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_PIPELINED) \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_GEMM2), MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_PIPELINED), \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_WORKQUEUE)                                                 \
   }
 #define MLP2_ENTRY(BM, BN1, BN2, NB, NS) MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, 1)
 
@@ -412,7 +441,7 @@ bool config_supported(const KernelConfig& c) { return find_entry(c) != nullptr; 
 hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu) {
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
-  const void* k = which == 0 ? e->seq1 : which == 1 ? e->seq2 : e->pipe;
+  const void* k = which == 0 ? e->seq1 : which == 1 ? e->seq2 : which == 2 ? e->pipe : e->wq;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, kThreads, 0);
 }
 
@@ -432,6 +461,13 @@ hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipS
   if (!e) return hipErrorInvalidValue;
   void* args[] = {const_cast<Args*>(&a)};
   return hipLaunchKernel(e->pipe, dim3(grid), dim3(kThreads), args, 0, stream);
+}
+
+hipError_t launch_workqueue(const KernelConfig& c, const Args& a, int grid, hipStream_t stream) {
+  const Entry* e = find_entry(c);
+  if (!e) return hipErrorInvalidValue;
+  void* args[] = {const_cast<Args*>(&a)};
+  return hipLaunchKernel(e->wq, dim3(grid), dim3(kThreads), args, 0, stream);
 }
 
 }  // namespace mlp2

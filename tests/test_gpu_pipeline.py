@@ -55,7 +55,7 @@ def test_alternating_inputs_and_modes(lib, act):
     outs = []
     seq = [0, 1, 2, 2, 0, 1, 0, 0, 2, 1] * 3
     for n, i in enumerate(seq):
-        mode = B.MODE_TILE_PIPELINED if n % 3 else B.MODE_SEQUENTIAL
+        mode = (B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_WORKQUEUE)[n % 3]
         outs.append((i, run(plan, sets[i], mode)))
     torch.cuda.synchronize()
     assert plan.check() == B.OK
@@ -155,6 +155,60 @@ def test_xcd_grouped_default_order(lib, grid):
     plan.close()
 
 
+WQ_CASES = [
+    # M, H, F, act, tuning
+    (160, 256, 768, 1, {"bm": 64, "splitk1": 2, "splitk2": 3}),
+    (96, 256, 512, 0, {"bm": 32, "splitk1": 1, "splitk2": 2}),
+    (256, 1024, 4096, 2, {"bm": 128, "bn1": 64, "bn2": 128, "splitk2": 2}),
+    (640, 256, 1024, 1, {"bm": 128, "bn1": 128, "bn2": 128, "splitk1": 1, "splitk2": 1}),
+    # K ranges of 192 across 128-column blocks: one GEMM1 tile feeds two parts of each GEMM2 tile
+    (64, 256, 1152, 1, {"bm": 64, "bn1": 128, "bn2": 64, "splitk2": 6}),
+]
+
+
+@pytest.mark.parametrize("case", range(len(WQ_CASES)))
+@pytest.mark.parametrize("grid", [1, 3, 0])
+def test_workqueue_mode_matches_sequential_bits(lib, case, grid):
+    """The paper's scoreboard-and-workqueue scheduling (Sec. III-A.2-3) gives
+    the sequential mode's bits for any grid, split-K and activation."""
+    M, H, F, act, tun = WQ_CASES[case]
+    d = I.make_inputs(M, H, F, act, seed=100 + case)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, tun)
+    Ys = run(plan, g, B.MODE_SEQUENTIAL).clone()
+    if grid:
+        plan.set_option(B.OPT_GRID, grid)
+    outs = [run(plan, g, B.MODE_WORKQUEUE).clone() for _ in range(3)]
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    for n, y in enumerate(outs):
+        assert_bit_equal(Ys, y, f"case {case} grid {grid} run {n}")
+    if case == 4 and grid == 0:
+        ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
+        assert_matches_oracle(outs[0], ref, "workqueue")
+    plan.close()
+
+
+def test_workqueue_dropped_signal_times_out_and_recovers(lib):
+    M, H, F, act = 64, 128, 256, 1
+    d = I.make_inputs(M, H, F, act, seed=72)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act)
+    plan.set_option(B.OPT_SPIN_LIMIT, 2000)
+    plan.set_option(B.OPT_DROP_SIGNAL, 0)
+    run(plan, g, B.MODE_WORKQUEUE)
+    torch.cuda.synchronize()
+    assert plan.check() == B.ERR_TIMEOUT
+    plan.set_option(B.OPT_DROP_SIGNAL, -1)
+    plan.set_option(B.OPT_SPIN_LIMIT, 1 << 20)
+    Yq = run(plan, g, B.MODE_WORKQUEUE).clone()
+    Ys = run(plan, g, B.MODE_SEQUENTIAL)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    assert_bit_equal(Ys, Yq, "after recovery")
+    plan.close()
+
+
 def test_run_argument_errors(lib):
     M, H, F = 32, 64, 128
     g = device_inputs(I.make_inputs(M, H, F, 0, seed=1))
@@ -162,7 +216,8 @@ def test_run_argument_errors(lib):
     Y = torch.empty(M, H, dtype=torch.bfloat16, device="cuda")
     s = torch.cuda.current_stream().cuda_stream
     X, W1, W2, y = (t.data_ptr() for t in (g["X"], g["W1"], g["W2"], Y))
-    assert plan.run_raw(X, W1, W2, y, s, 2) == B.ERR_INVALID_ARG
+    assert plan.run_raw(X, W1, W2, y, s, 3) == B.ERR_INVALID_ARG
+    assert plan.run_raw(X, W1, W2, y, s, -1) == B.ERR_INVALID_ARG
     assert plan.run_raw(X + 2, W1, W2, y, s, 0) == B.ERR_ALIGNMENT
     assert plan.run_raw(X, W1, W2, X, s, 0) == B.ERR_INVALID_ARG  # Y aliases X
     assert plan.run_raw(0, W1, W2, y, s, 0) == B.ERR_INVALID_ARG

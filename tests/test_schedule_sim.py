@@ -234,3 +234,149 @@ def test_xcd_grouped_deal_is_a_permutation_of_whole_column_waves(Mb, N, wave):
         for x in range(8):
             tiles = [order[8 * j + x] for j in range(64)]
             assert len({t % Mb for t in tiles}) == 8 and len({t // Mb for t in tiles}) == 8
+
+
+def simulate_workqueue(Mb, Nb1, Nb2, S1, S2, grid, seed, k_ranges=None, order="auto", late_start=0):
+    """Step simulation of the workqueue mode (Sec. III-A.2-3 scheduling).
+
+    GEMM1 items are claimed by rank through the claim lists (the first
+    min(grid, items) ranks taken without tickets, as the host arranges);
+    a work-group whose claim runs past them takes the next queue slot and
+    waits until a unit is there.  A GEMM2 unit enters the queue when the last
+    part of the last GEMM1 tile it reads finishes (its scoreboard reaches its
+    producer count).  `k_ranges[s]` lists the Z column blocks part s reads
+    (default: even shares); parts of neighbouring ranges may share a block.
+    Returns the units in run order with their start step and the step at
+    which their producers were all done, or None on deadlock."""
+    rng = random.Random(seed)
+    lists = claim_lists(grid)
+    items1 = [(t, s) for t in column_first_tiles(Mb, Nb1, order) for s in range(S1)]
+    per = -(-Nb1 // S2)
+    k_ranges = k_ranges or [list(range(s * per, min(Nb1, (s + 1) * per))) for s in range(S2)]
+    k_ranges = [r for r in k_ranges if r]  # the host's S2 = ceil(F / kc2): no part reads nothing
+    S2 = len(k_ranges)
+    units = [(tile, s) for tile in range(Mb * Nb2) for s in range(S2)]
+    needs = {u: [kb * Mb + u[0] % Mb for kb in k_ranges[u[1]]] for u in units}
+    users = {}
+    for u in units:
+        for t in needs[u]:
+            users.setdefault(t, []).append(u)
+    board = {u: 0 for u in units}
+    parts = {}
+    queue, head = [], [0]
+    ready_at, ran = {}, []
+    first_static = min(grid, len(items1))
+    ticket = [0] * lists
+    skip = [len(range(l, first_static, lists)) for l in range(lists)]
+
+    def claim(g):
+        l = g % lists
+        t = ticket[l]
+        ticket[l] += 1
+        return l + (t + skip[l]) * lists
+
+    # work-group: [phase, item, remaining, start]; phase "g1", "pop", "g2", "done"
+    wgs = []
+    for g in range(grid):
+        r = g if g < first_static else claim(g)
+        wgs.append(["g1", r, rng.randint(1, 6), rng.randint(0, late_start)])
+    for step in range(200000):
+        if all(w[0] == "done" for w in wgs):
+            return ran
+        progressed = False
+        for g, w in enumerate(wgs):
+            phase = w[0]
+            if phase == "done" or step < w[3]:
+                progressed |= phase != "done"
+                continue
+            progressed = True
+            if phase == "g1":
+                if w[1] >= len(items1):
+                    w[0], w[1] = "pop", None
+                    continue
+                if w[2] > 0:
+                    w[2] -= 1
+                    continue
+                tile, s = items1[w[1]]
+                parts[tile] = parts.get(tile, 0) + 1
+                if parts[tile] == S1:  # the tile is complete: count down its users' scoreboards
+                    for u in users.get(tile, []):
+                        board[u] += 1
+                        if board[u] == len(needs[u]):
+                            queue.append(u)
+                            ready_at[u] = step
+                w[1], w[2] = claim(g), rng.randint(1, 6)
+            elif phase == "pop":
+                if w[1] is None:
+                    w[1] = head[0]
+                    head[0] += 1
+                if w[1] >= len(units):
+                    w[0] = "done"
+                elif w[1] < len(queue):  # the slot is filled
+                    u = queue[w[1]]
+                    ran.append((u, step, ready_at[u]))
+                    w[0], w[1], w[2] = "g2", u, rng.randint(1, 6)
+                else:
+                    progressed = any(x[0] in ("g1", "g2") for x in wgs) or progressed
+            elif phase == "g2":
+                if w[2] > 0:
+                    w[2] -= 1
+                else:
+                    w[0], w[1] = "pop", None
+        if not progressed:
+            return None
+    return None
+
+
+@pytest.mark.parametrize("Mb,Nb1,Nb2,S1,S2", CASES)
+@pytest.mark.parametrize("order", ["auto", "xcd", "reversed", "shuffled"])
+def test_workqueue_schedule_runs_every_unit_after_its_producers(Mb, Nb1, Nb2, S1, S2, order):
+    for grid in (1, 2, 3, 8, 9, 17):
+        for seed in range(3):
+            ran = simulate_workqueue(Mb, Nb1, Nb2, S1, S2, grid, seed, order=order, late_start=20 if seed else 0)
+            assert ran is not None, (grid, seed)
+            parts = len({s for _, s in (u for u, _, _ in ran)})
+            assert sorted(u for u, _, _ in ran) == sorted((t, s) for t in range(Mb * Nb2) for s in range(parts))
+            assert all(start >= ready for _, start, ready in ran)
+
+
+def test_workqueue_schedule_with_parts_sharing_a_column_block():
+    # 1152 columns in blocks of 128 split into parts of 192: block 1 feeds parts 0 and 1, ...
+    k_ranges = [sorted({c // 128 for c in range(s * 192, (s + 1) * 192)}) for s in range(6)]
+    assert k_ranges[0] == [0, 1] and k_ranges[1] == [1, 2]
+    for grid in (1, 4, 9):
+        ran = simulate_workqueue(2, 9, 3, 1, 6, grid, seed=grid, k_ranges=k_ranges)
+        assert ran is not None and len(ran) == 2 * 3 * 6
+        assert all(start >= ready for _, start, ready in ran)
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_counter_targets_hold_across_any_sequence_of_modes(seed):
+    """Counters carry over from run to run without host resets.  Ready counters
+    advance once per run in every mode (workqueue producers signal them too),
+    so a pipelined consumer's target is epoch + 1; scoreboards advance only in
+    workqueue runs, so a unit with n producers completes at (w + 1) * n, w the
+    number of earlier workqueue runs; split-K arrivals count S per run."""
+    rng = random.Random(seed)
+    tiles, n_of = list(range(6)), {"u0": 2, "u1": 3, "u2": 1}
+    users = {"u0": [0, 1], "u1": [2, 3, 4], "u2": [5]}
+    ready = {t: 0 for t in tiles}
+    board = {u: 0 for u in n_of}
+    arrivals, S = 0, 3
+    epoch = wq = 0
+    for _ in range(60):
+        mode = rng.choice(["sequential", "pipelined", "workqueue"])
+        for t in tiles:  # every GEMM1 tile signals once per run
+            ready[t] += 1
+        if mode == "pipelined":
+            assert all(ready[t] >= epoch + 1 for t in tiles)
+        if mode == "workqueue":
+            for u, ts in users.items():
+                for k, t in enumerate(ts):
+                    board[u] += 1
+                    assert (board[u] == (wq + 1) * n_of[u]) == (k == len(ts) - 1), (u, board[u], wq)
+        for s in range(S):  # split-K parts of one tile: the last arrival completes it
+            arrivals += 1
+            assert (arrivals == (epoch + 1) * S) == (s == S - 1)
+        epoch += 1
+        wq += mode == "workqueue"
