@@ -691,9 +691,11 @@ __device__ __forceinline__ uint32_t queue_tag(uint32_t wq_epoch) { return ((wq_e
 // Producer side: every wave's Z stores of the tile are complete, then wave 0
 // increments the scoreboard of each unit that reads the tile, one unit per
 // lane (agent-scope release: the tile's Z lines are written back before the
-// count moves).  The units whose count this completes are then pushed one
-// at a time, in a scalar loop over the ballot: lane 0 reserves a queue slot
-// and publishes the unit with a release store.  The queue has one spare slot
+// count moves).  The units whose count this completes are pushed together:
+// lane 0 reserves as many queue slots as the ballot has bits with one atomic
+// (a tile that completes a whole split's units would otherwise pay one
+// round trip per unit, one after the other), and each completing lane
+// publishes its unit in its slot with a release store.  The queue has one spare slot
 // past the run's unit count; a reservation beyond it (impossible: each unit
 // completes once per run) would land there, no consumer reads it, and the
 // unit's consumer would time out and report the error.
@@ -719,12 +721,17 @@ __device__ __forceinline__ void push_ready(const Args& a, int tile, uint32_t wq_
             __hip_atomic_fetch_add(a.board + (long)q * kLine, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         complete = old + 1u == (wq_epoch + 1u) * n;
       }
-      for (uint64_t m = __builtin_amdgcn_ballot_w64(complete); m; m &= m - 1) {
-        const uint32_t unit = (uint32_t)__builtin_amdgcn_readlane(q, (int)__builtin_ctzll(m));
-        if (lane == 0) {
-          const uint32_t slot = __hip_atomic_fetch_add(a.ctrl + CTRL_QTAIL, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          __hip_atomic_store(a.queue + min(slot, (uint32_t)a.items2), queue_tag(wq_epoch) | unit, __ATOMIC_RELEASE,
-                             __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t m = __builtin_amdgcn_ballot_w64(complete);
+      if (m) {  // a scalar branch: m is the same in every lane
+        uint32_t base = 0;
+        if (lane == 0)
+          base = __hip_atomic_fetch_add(a.ctrl + CTRL_QTAIL, (uint32_t)__builtin_popcountll(m), __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
+        base = uniform(base);
+        if (complete) {
+          const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+          __hip_atomic_store(a.queue + min(base + below, (uint32_t)a.items2), queue_tag(wq_epoch) | (uint32_t)q,
+                             __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         }
       }
     }

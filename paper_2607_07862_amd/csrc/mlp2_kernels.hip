@@ -363,13 +363,15 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
   }
   if constexpr (PHASE == PHASE_WORKQUEUE) {
     __syncthreads();  // every wave is done with s_item before pop_ready rewrites it
+    uint64_t t_pop = trace_now();  // a unit's trace starts when its work-group begins to pop it
     for (int q = pop_ready(a, wq_epoch, &s_item); q >= 0; q = pop_ready(a, wq_epoch, &s_item)) {
       TraceAcc tr;
-      const uint64_t t_start = trace_now();
+      if constexpr (kTrace) tr.flag = trace_now() - t_pop;  // waiting for the queue slot to fill
       NoClaim none;
       gemm2_item<T2, HV, false, NoClaim>(a, q, epoch, lds, &s_slot, none, &s_item, tr);
-      if constexpr (kTrace) tr_record(a, 0, n_items++, -1, 0x80000000u | (uint32_t)q, t_start, tr);
+      if constexpr (kTrace) tr_record(a, 0, n_items++, -1, 0x80000000u | (uint32_t)q, t_pop, tr);
       __syncthreads();  // the item's divergent stores close, and s_item is free again
+      t_pop = trace_now();
     }
   }
   finish_kernel(a, epoch, PHASE != PHASE_GEMM1, PHASE == PHASE_WORKQUEUE, wq_epoch);

@@ -5,11 +5,13 @@
 Needs the trace build (``python -m paper_2607_07862_amd.build --trace``) and
 a GPU.  For each workload (device-drawn inputs of its shapes): warm-up runs,
 then one traced warm run per mode.  Per item kind it reports the mean item
-time split into mainloop, waits for the work-group's own ring loads, waits
-for ready counters (flag waits) and epilogue, and for the GEMM2 items of the
-pipelined mode the share of their time spent in flag waits beside the wait
-their producers' completion times imply (the latest end among the GEMM1
-items that write the Z columns the item reads, minus the item's start).
+time split into mainloop, waits for the work-group's own ring loads, flag
+waits (ready counters in the pipelined mode; in the workqueue mode the wait
+for the popped queue slot to fill, counted from when the work-group began to
+pop) and epilogue, and for the GEMM2 items of the two one-launch modes the
+share of their time spent in flag waits beside the wait their producers'
+completion times imply (the latest end among the GEMM1 items that write the
+Z columns the item reads, minus the item's start).
 """
 from __future__ import annotations
 
@@ -72,7 +74,8 @@ def summarise(B, I, bench, key):
         r.run(B.MODE_SEQUENTIAL)
     torch.cuda.synchronize()
     rows = []
-    for mode, name in ((B.MODE_SEQUENTIAL, "sequential"), (B.MODE_TILE_PIPELINED, "pipelined")):
+    for mode, name in ((B.MODE_SEQUENTIAL, "sequential"), (B.MODE_TILE_PIPELINED, "pipelined"),
+                       (B.MODE_WORKQUEUE, "workqueue")):
         buf.zero_()
         r.plan.attach_trace(buf, CAP)
         r.run(mode)
@@ -94,7 +97,7 @@ def summarise(B, I, bench, key):
                 "item": item.mean(), "main": main.mean(), "ring": ring.mean(), "flag": flag.mean(),
                 "epi": (item - main).mean(), "flag_share": flag.sum() / item.sum(),
             }
-            if kind == 1 and name == "pipelined":
+            if kind == 1 and name != "sequential":
                 S1 = info["splitk1"]
                 ready = {}
                 for x in recs:
@@ -137,8 +140,10 @@ def main():
             "Command (from the repository root on the GPU host, after `python -m paper_2607_07862_amd.build --trace`):", "",
             "```", cmd, "```", "",
             "Times are means over the items of a kind; the flag share is the kind's flag-wait time over its item",
-            "time; the producer-implied wait is, per GEMM2 item of the pipelined run, the latest end among the GEMM1",
-            "items writing the Z columns it reads minus its start (0 when they were done before it started).", ""]
+            "time (pipelined: waits on ready counters; workqueue: the wait for the popped queue slot to fill, the",
+            "item starting when its work-group began to pop); the producer-implied wait is, per GEMM2 item of the",
+            "two one-launch modes, the latest end among the GEMM1 items writing the Z columns it reads minus its",
+            "start (0 when they were done before it started).", ""]
     text = "\n".join(head + lines) + "\n"
     if args.out:
         with open(args.out, "w") as f:
