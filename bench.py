@@ -1,24 +1,28 @@
 #!/usr/bin/env python3
-"""Latency of the two-layer MLP Y = act(X W1) W2 on one MI355X, both modes.
+"""Latency of the two-layer MLP Y = act(X W1) W2 on one MI355X, in each mode.
 
 A step is one ``mlp2_run`` (the whole hot path: GEMM1 + activation + ready
 signals + GEMM2) over one batch of synthetic inputs already resident in HBM.
 W warm-up steps, then exactly K back-to-back steps of the tile-pipelined mode
 timed between a synchronise on each side; ``value`` is that block's mean
-latency per step.  Beside it the line carries the sequential mode's latency
-(same block timing), the workqueue mode's (the paper's scoreboard-and-queue
-scheduling of GEMM2 units, same block timing), cold latencies of both modes (a 1 GiB read evicts the
-L2s and the 256 MB MALL before each timed run, modes interleaved), the
-roofline fraction of the dominant kernel (the pipelined launch, timed with HIP
-events on the stream it is launched on), HBM traffic from committed
-rocprofv3 counter summaries when they match the current kernel sources, a
-table of both modes on every MLP workload (beside eager PyTorch on the same
-inputs, hipBLASLt GEMMs plus an activation kernel, as a reference point), and
-the fp64 CPU oracle timed on a bounded sample of the headline workload.  Two
-more legs guard the comparison: both modes timed run by run in alternating
-order (medians, p10/p90), and what the GPU attains outside the library (a
-4 GiB read-only stream, an 8192^3 hipBLASLt GEMM) as context for the
-roofline fractions, which stay against the published peaks.
+latency per step.  Beside it the line carries:
+
+* the sequential mode's latency: the mean of equal blocks timed just before
+  and just after the pipelined one;
+* the workqueue mode's (the paper's scoreboard-and-queue scheduling of GEMM2
+  units), same block timing;
+* cold latencies of the pipelined and sequential modes (a 1 GiB read evicts
+  the L2s and the 256 MB MALL before each timed run, modes interleaved);
+* both modes timed run by run in alternating order (medians, p10/p90);
+* the roofline fraction of the dominant kernel (the pipelined launch, timed
+  with HIP events on the stream it is launched on), HBM traffic from
+  committed rocprofv3 counter summaries when they match the current kernel
+  sources, and what the GPU attains outside the library (a 4 GiB read-only
+  stream, an 8192^3 hipBLASLt GEMM) as context for the fractions, which stay
+  against the published peaks;
+* a table of the modes on every MLP workload, beside eager PyTorch on the
+  same inputs (hipBLASLt GEMMs plus an activation kernel) as a reference;
+* the fp64 CPU oracle timed on a bounded sample of the headline workload.
 
 Only ``--gpus 1`` is supported: the build targets a single GPU.
 """
@@ -355,16 +359,21 @@ def main():
             r.run(B.MODE_WORKQUEUE)
     torch.cuda.synchronize()
     r.check()
+    seq_before = None if args.only_pipelined else r.block(B.MODE_SEQUENTIAL, args.steps)
     log(f"timing {args.steps} pipelined steps")
     value = r.block(B.MODE_TILE_PIPELINED, args.steps)
     extra = {}
     if not args.only_pipelined:
-        seq_us = r.block(B.MODE_SEQUENTIAL, args.steps)
+        # sequential blocks on both sides of the pipelined one: a drift of the
+        # clocks over the blocks reaches the two modes alike
+        seq_after = r.block(B.MODE_SEQUENTIAL, args.steps)
+        seq_us = (seq_before + seq_after) / 2
         wq_us = r.block(B.MODE_WORKQUEUE, args.steps)
         pipe2 = r.block(B.MODE_TILE_PIPELINED, args.steps)
         log(f"pipelined {value:.2f} us (repeat {pipe2:.2f}), sequential {seq_us:.2f} us, workqueue {wq_us:.2f} us")
         extra = {
             "sequential_us": round(seq_us, 3),
+            "sequential_before_after_us": [round(seq_before, 3), round(seq_after, 3)],
             "workqueue_us": round(wq_us, 3),
             "pipelined_repeat_us": round(pipe2, 3),
             "gain_vs_sequential_pct": round((seq_us - value) / seq_us * 100, 2),
