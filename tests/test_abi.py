@@ -105,3 +105,17 @@ def test_last_error_is_per_thread(lib):
     th.join()
     assert seen == [B.OK]
     assert lib.mlp2_last_error() == B.ERR_INVALID_ARG
+
+
+def test_binding_constants_match_the_header():
+    """Every enum constant the header defines has the same value in the binding
+    (MLP2_MODE_WORKQUEUE -> binding.MODE_WORKQUEUE, MLP2_OK -> binding.OK, ...)."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    consts = {}
+    for body in re.findall(r"enum\s+\w+\s*\{(.*?)\}", text, flags=re.S):
+        for name, value in re.findall(r"\b(MLP2_[A-Z0-9_]+)\s*=\s*(-?\d+)", body):
+            consts[name] = int(value)
+    assert "MLP2_MODE_WORKQUEUE" in consts and len(consts) >= 20
+    for name, value in consts.items():
+        attr = name[len("MLP2_"):]
+        assert getattr(B, attr) == value, name
