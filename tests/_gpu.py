@@ -27,6 +27,14 @@ def run(plan: B.Plan, g: dict, mode: int, Y=None, stream=None):
     return Y
 
 
+def workqueue_mode(plan: B.Plan, g: dict):
+    """Y and Z of a workqueue-mode run (synchronised)."""
+    Yq = run(plan, g, B.MODE_WORKQUEUE)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    return Yq, plan.intermediate()
+
+
 def both_modes(plan: B.Plan, g: dict):
     """Y and Z of a sequential run and of a pipelined run (each synchronised)."""
     Ys = run(plan, g, B.MODE_SEQUENTIAL)

@@ -18,7 +18,7 @@ from oracle import mlp2_oracle as O
 from paper_2607_07862_amd import binding as B
 from paper_2607_07862_amd import inputs as I
 
-from _gpu import assert_bit_equal, assert_matches_oracle, both_modes, bits_of, device_inputs, run
+from _gpu import assert_bit_equal, assert_matches_oracle, both_modes, bits_of, device_inputs, run, workqueue_mode
 
 pytestmark = pytest.mark.gpu
 
@@ -46,11 +46,14 @@ def test_small_shapes_against_full_oracle(lib, M, H, F, act, tuning):
     g = device_inputs(d)
     plan = B.Plan(M, H, F, act, tuning)
     Ys, Zs, Yp, Zp = both_modes(plan, g)
+    Yq, Zq = workqueue_mode(plan, g)
     ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
     assert_matches_oracle(Yp, ref, "pipelined Y")
     assert_matches_oracle(Ys, ref, "sequential Y")
     assert_bit_equal(Ys, Yp, "Y sequential vs pipelined")
     assert_bit_equal(Zs, Zp, "Z sequential vs pipelined")
+    assert_bit_equal(Ys, Yq, "Y sequential vs workqueue")
+    assert_bit_equal(Zs, Zq, "Z sequential vs workqueue")
     zref = O.intermediate(I.bits(d["X"]), I.bits(d["W1"]), M, H, F, act)
     assert_matches_oracle(Zp[:M], zref, "Z")
     plan.close()
@@ -73,6 +76,9 @@ def test_workloads_full_size_sampled_rows(lib, key):
     Ys, Zs, Yp, Zp = both_modes(plan, g)
     assert_bit_equal(Ys, Yp, "Y sequential vs pipelined")
     assert_bit_equal(Zs, Zp, "Z sequential vs pipelined")
+    Yq, Zq = workqueue_mode(plan, g)
+    assert_bit_equal(Ys, Yq, "Y sequential vs workqueue")
+    assert_bit_equal(Zs, Zq, "Z sequential vs workqueue")
     rows = I.sample_rows(w.M, 24, w.seed)
     ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), w.M, w.H, w.F, w.act, rows=rows)
     r = assert_matches_oracle(Yp[torch.as_tensor(rows, device="cuda")], ref, f"{w.name} sampled rows")
