@@ -10,7 +10,9 @@
   bounded wait give up, every kernel still exits, mlp2_check reports the
   timeout and the plan recovers; so does one beyond the first 64 column
   blocks of a consumer whose first 64 are all ready (the wait reads
-  readiness 64 blocks at a time).
+  readiness 64 blocks at a time);
+* the workqueue mode (scoreboards and a device queue) gives the same bits;
+* a run captured into a graph replays with the eager bits, in every mode.
 """
 import pytest
 import torch
@@ -206,6 +208,42 @@ def test_workqueue_dropped_signal_times_out_and_recovers(lib):
     torch.cuda.synchronize()
     assert plan.check() == B.OK
     assert_bit_equal(Ys, Yq, "after recovery")
+    plan.close()
+
+
+@pytest.mark.parametrize("mode", [B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_WORKQUEUE])
+def test_graph_replays_match_eager_runs(lib, mode):
+    """mlp2_run records into a graph (kernel launches only: no memset, no
+    synchronisation), and every replay gives the eager bits: the counters and
+    epochs live on the device and advance once per replay, also with eager
+    runs of the other modes between the replays."""
+    M, H, F, act = 96, 256, 512, 1
+    d = I.make_inputs(M, H, F, act, seed=95)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, {"bm": 32, "splitk1": 2, "splitk2": 2})
+    ref = run(plan, g, B.MODE_SEQUENTIAL).clone()
+    Y = torch.empty(M, H, dtype=torch.bfloat16, device="cuda")
+    side = torch.cuda.Stream()  # default priority
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        plan.run(g["X"], g["W1"], g["W2"], Y, mode, stream=side)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        plan.run(g["X"], g["W1"], g["W2"], Y, mode, stream=torch.cuda.current_stream())
+    outs = []
+    for i in range(6):
+        Y.zero_()
+        graph.replay()
+        torch.cuda.synchronize()
+        outs.append(Y.clone())
+        run(plan, g, (B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_WORKQUEUE)[i % 3])
+        torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    for n, y in enumerate(outs):
+        assert_bit_equal(ref, y, f"mode {mode} replay {n}")
+    del graph
     plan.close()
 
 
