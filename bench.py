@@ -310,6 +310,8 @@ def main():
     ap.add_argument("--interleave-iters", type=int, default=100,
                     help="warm runs per mode timed one by one in alternating order (0 skips; a third of it per table row)")
     ap.add_argument("--no-attainable", action="store_true", help="skip the stream and library-GEMM references")
+    ap.add_argument("--paper-shapes", action="store_true",
+                    help="also time the paper's own workload: 8192x8192 weights, no activation, M = 1024 ... 32768")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
     ap.add_argument("--no-table", action="store_true", help="skip the table of all workloads")
     ap.add_argument("--only-pipelined", action="store_true", help="time the pipelined mode only (profiling runs)")
@@ -462,6 +464,41 @@ def main():
             table[key] = row
             log(f"TABLE {key:12s} {row}")
 
+    paper = {}
+    if args.paper_shapes:
+        for key in I.PAPER_ORDER:
+            wk = I.WORKLOADS[key]
+            gk = device_random_inputs(wk)
+            rr = Runner(B, wk, gk, None, stream)
+            for _ in range(5):
+                rr.run(B.MODE_TILE_PIPELINED)
+                rr.run(B.MODE_SEQUENTIAL)
+                rr.run(B.MODE_WORKQUEUE)
+            steps = max(5, args.steps // 5)
+            s_before = rr.block(B.MODE_SEQUENTIAL, steps)
+            p_us = rr.block(B.MODE_TILE_PIPELINED, steps)
+            s_us = (s_before + rr.block(B.MODE_SEQUENTIAL, steps)) / 2
+            q_us = rr.block(B.MODE_WORKQUEUE, steps)
+            ivk = rr.interleaved(10)
+            rr.check()
+            inf = rr.info
+            rr.close()
+            te = torch_eager_us(wk, gk, steps)
+            del gk
+            torch.cuda.empty_cache()
+            mp, ms = statistics.median(ivk[B.MODE_TILE_PIPELINED]), statistics.median(ivk[B.MODE_SEQUENTIAL])
+            row = {
+                "M": wk.M, "pipelined_us": round(p_us, 2), "sequential_us": round(s_us, 2),
+                "gain_pct": round((s_us - p_us) / s_us * 100, 1), "workqueue_us": round(q_us, 2),
+                "interleaved_median_us": {"pipelined": round(mp, 2), "sequential": round(ms, 2),
+                                          "gain_pct": round((ms - mp) / ms * 100, 1)},
+                "torch_eager_us": round(te, 2),
+                "mfma_frac": round(wk.alg_flops() / (p_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                "tiles": [inf["bm"], inf["bn1"], inf["splitk1"], inf["bn2"], inf["splitk2"], inf["stages"]],
+            }
+            paper[key] = row
+            log(f"PAPER {key:14s} {row}")
+
     att = None
     if not args.no_attainable:
         att = attainable()
@@ -510,6 +547,7 @@ def main():
         "attainable": att,
         "cpu_baseline": cpu,
         "workloads": table,
+        **({"paper_shapes": paper} if paper else {}),
     }
     print(json.dumps(out), flush=True)
 

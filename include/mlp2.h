@@ -83,15 +83,24 @@ enum mlp2_status {
  * worth of tiles (still whole column blocks) is dealt to the 8 XCDs as
  * near-square sub-blocks, so the operand slices a stage reads are shared
  * inside each XCD's L2; the GEMM2 kernel's items are dealt the same way.
- * (Row-block-first halves, which let some GEMM2 items start before GEMM1
- * ends, measured slower at prefill size.) */
+ * With many row blocks whose activation and first weights exceed the 256 MB
+ * last-level cache, the default is MLP2_ORDER_BANDED instead, and the
+ * pipelined launch then places every GEMM2 item after every GEMM1 item
+ * (overlapping only the tail): a band's GEMM2 items could start beside the
+ * next band's GEMM1 items, but both weight matrices streaming at once no
+ * longer fit that cache.  (Row-block-first halves, which let some GEMM2
+ * items start before GEMM1 ends, measured slower at prefill size.) */
 enum mlp2_order {
-  MLP2_ORDER_AUTO = 0,         /* the default: XCD-grouped column-first with several row
-                                  blocks and no split-K, else column-first                     */
+  MLP2_ORDER_AUTO = 0,         /* the default: row bands for many row blocks whose X and W1
+                                  exceed the last-level cache; else XCD-grouped column-first
+                                  with several row blocks and no split-K; else column-first    */
   MLP2_ORDER_COLUMN_FIRST = 1, /* every row block of column block 0, then column block 1, ... */
   MLP2_ORDER_ROW_FIRST = 2,    /* every column block of row block 0, then row block 1, ...    */
   MLP2_ORDER_REVERSED = 3,     /* column-first, last column block first (stress order)         */
-  MLP2_ORDER_SHUFFLED = 4      /* a seeded permutation (stress order)                          */
+  MLP2_ORDER_SHUFFLED = 4,     /* a seeded permutation (stress order)                          */
+  MLP2_ORDER_BANDED = 5        /* bands of about a grid's worth of row blocks, all column blocks
+                                  of a band before the next (both kernels); for many row blocks,
+                                  where a wave of whole column blocks reads all of X             */
 };
 
 /* Optional tuning for mlp2_plan_ex; a zero field means "choose automatically". */

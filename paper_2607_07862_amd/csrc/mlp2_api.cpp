@@ -126,6 +126,38 @@ std::vector<uint32_t> xcd_grouped(int Mb, int N, int wave) {
   return out;
 }
 
+// Row bands: `band` consecutive row blocks with all their column blocks,
+// band after band, each band dealt to the XCDs as xcd_grouped deals a grid.
+// A band reads its rows of the activation once while the weights stay in the
+// last-level cache, and the GEMM2 items of a band depend on that band only.
+std::vector<uint32_t> banded(int Mb, int N, int wave, int band) {
+  std::vector<uint32_t> out;
+  out.reserve((size_t)Mb * N);
+  for (int r0 = 0; r0 < Mb; r0 += band) {
+    const int rb = std::min(band, Mb - r0);
+    for (uint32_t t : xcd_grouped(rb, N, wave)) {
+      const int nb = (int)t / rb, mb = (int)t % rb;
+      out.push_back((uint32_t)(nb * Mb + r0 + mb));
+    }
+  }
+  return out;
+}
+
+// Row blocks per band: about one wave of the grid's tiles.
+int band_rows(int N, int wave) { return std::max(1, wave / std::max(1, N)); }
+
+// Whether the plan's GEMM1 order is row bands: explicitly, or by default once
+// X and W1 together exceed the 256 MB last-level cache with many row blocks
+// (measured at 8192 x 8192 weights: from 16384 rows on; at 32768 rows bands
+// take the sequential mode from 12.7 to 9.0 ms).
+bool uses_bands(const mlp2_plan_s* p) {
+  if (p->S1 != 1) return false;
+  if (p->order == MLP2_ORDER_BANDED) return true;
+  const int64_t nb = p->act == MLP2_ACT_SWIGLU ? 2 : 1;
+  const int64_t x_w1 = (int64_t)p->M * p->H * 2 + nb * p->H * p->F * 2;
+  return p->order == MLP2_ORDER_AUTO && p->Mb >= 32 && x_w1 > (int64_t)256 << 20;
+}
+
 // GEMM1 item order (the rank order of the GEMM1 kernel, and of the GEMM1
 // items within the pipelined kernel).  Items are id = tile * S1 + s with
 // tile = nb * Mb + mb; every policy orders tiles and keeps the S1 parts of a
@@ -144,8 +176,13 @@ void build_order(mlp2_plan_s* p, std::vector<uint32_t>& out) {
       for (int nb = p->Nb1 - 1; nb >= 0; --nb)
         for (int mb = 0; mb < p->Mb; ++mb) tile(nb, mb);
       break;
+    case MLP2_ORDER_BANDED:
     case MLP2_ORDER_AUTO:
-      if (p->Mb > 1 && p->S1 == 1) {
+      if (uses_bands(p)) {
+        tiles = banded(p->Mb, p->Nb1, p->grid1, band_rows(p->Nb1, p->grid1));
+        break;
+      }
+      if (p->Mb > 1 && p->S1 == 1 && p->order == MLP2_ORDER_AUTO) {
         tiles = xcd_grouped(p->Mb, p->Nb1, p->grid1);
         break;
       }
@@ -171,6 +208,11 @@ void build_order(mlp2_plan_s* p, std::vector<uint32_t>& out) {
 // (q = tile * S2 + s, tile = nb * Mb + mb).  No GEMM2 item waits in the
 // GEMM2 kernel, so any order is valid there.
 void build_order2(const mlp2_plan_s* p, std::vector<uint32_t>& out) {
+  if (uses_bands(p) && p->S2 == 1) {  // the GEMM1 bands' rows, band by band
+    const std::vector<uint32_t> t = banded(p->Mb, p->Nb2, p->grid2, band_rows(p->Nb1, p->grid1));
+    out.assign(t.begin(), t.end());
+    return;
+  }
   if (p->order == MLP2_ORDER_AUTO && p->Mb > 1 && p->S2 == 1) {
     out = xcd_grouped(p->Mb, p->Nb2, p->grid2);
     return;
@@ -180,8 +222,9 @@ void build_order2(const mlp2_plan_s* p, std::vector<uint32_t>& out) {
 }
 
 // Rank table of the pipelined kernel: the GEMM1 items keep their order; GEMM2
-// item q = tile * S2 + s goes right after rank h(q) + lag, where h(q) is the
-// highest GEMM1 rank among the tiles its K range reads.  Every GEMM2 item thus
+// item q = tile * S2 + s goes right after rank h(q) + lag (after every GEMM1
+// item, in the GEMM2 order table's sequence, when lag >= items1), where h(q)
+// is the highest GEMM1 rank among the tiles its K range reads.  Every GEMM2 item thus
 // ranks above every GEMM1 item it waits for (what the deadlock argument
 // needs), and is claimed about `lag` claims after its last producer.
 void build_merged(const mlp2_plan_s* p, const std::vector<uint32_t>& order1, const std::vector<uint32_t>& order2, int lag,
@@ -206,7 +249,14 @@ void build_merged(const mlp2_plan_s* p, const std::vector<uint32_t>& order1, con
     const int64_t kbeg = (int64_t)s * p->kc2, kend = std::min<int64_t>(p->F, kbeg + p->kc2);
     int64_t h = -1;
     for (int64_t kb = kbeg / p->kc.bn1; kb <= (kend - 1) / p->kc.bn1; ++kb) h = std::max(h, last_rank[kb * p->Mb + mb]);
-    keys.push_back({h + lag, 1, (uint32_t)q});
+    // With a lag of the whole GEMM1 list (row bands) every GEMM2 item gets the
+    // key items1: they all follow GEMM1 in the GEMM2 order table's sequence
+    // (its bands and XCD deal) instead of being sorted by their last
+    // producer.  Otherwise the key keeps the order in which producers finish
+    // (e.g. split-K parts whose producers end a round apart).  Every item
+    // still ranks above its producers.
+    const int64_t n1 = (int64_t)order1.size();
+    keys.push_back({lag >= n1 ? n1 : h + lag, 1, (uint32_t)q});
   }
   std::stable_sort(keys.begin(), keys.end(), [](const Key& a, const Key& b) {
     return a.key != b.key ? a.key < b.key : a.kind < b.kind;
@@ -231,7 +281,13 @@ int upload_order(mlp2_plan_s* p) {
   std::vector<uint32_t> ord, ord2, merged;
   build_order(p, ord);
   build_order2(p, ord2);
-  build_merged(p, ord, ord2, p->grid_override ? p->grid_override : p->grid, merged);
+  // With row bands every GEMM2 item goes after every GEMM1 item: bands would
+  // let a band's GEMM2 items start beside the next band's GEMM1 items, but
+  // then W1 and W2 stream at once and no longer fit the last-level cache
+  // together (measured: 30-37 % slower than the sequential mode at 4096 to
+  // 32768 rows); the launch then overlaps only the tail of GEMM1.
+  const int lag = uses_bands(p) ? p->items1 : (p->grid_override ? p->grid_override : p->grid);
+  build_merged(p, ord, ord2, lag, merged);
   p->lead1 = 0;
   while (p->lead1 < (int64_t)merged.size() && !(merged[p->lead1] & 0x80000000u)) ++p->lead1;
   if (hipMemcpy(p->order1, ord.data(), ord.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess ||
@@ -274,7 +330,7 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   std::memset(&tz, 0, sizeof(tz));
   if (t) tz = *t;
   if (tz.bm < 0 || tz.bn1 < 0 || tz.bn2 < 0 || tz.splitk1 < 0 || tz.splitk2 < 0 || tz.grid < 0 || tz.order < 0 || tz.stages < 0 ||
-      tz.order > MLP2_ORDER_SHUFFLED) {
+      tz.order > MLP2_ORDER_BANDED) {
     fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
   }
@@ -589,7 +645,7 @@ int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
       p->drop_signal = (int)value;
       return MLP2_OK;
     case MLP2_OPT_ORDER:
-      if (value < MLP2_ORDER_AUTO || value > MLP2_ORDER_SHUFFLED) return fail(MLP2_ERR_INVALID_ARG);
+      if (value < MLP2_ORDER_AUTO || value > MLP2_ORDER_BANDED) return fail(MLP2_ERR_INVALID_ARG);
       p->order = (int)value;
       if (hipDeviceSynchronize() != hipSuccess || upload_order(p) != MLP2_OK) return fail(MLP2_ERR_HIP);
       return MLP2_OK;

@@ -621,11 +621,11 @@ struct ReadyWait {
   uint32_t target;
   uint32_t spin_limit;
   int* s_known;   // LDS broadcast slot
-  int known;      // highest column block acquired by this work-group (uniform)
+  int k_ready;    // K offsets below this are in column blocks this work-group has acquired (uniform)
   TraceAcc* tr;
   __device__ __forceinline__ void operator()(int k) {
+    if (k < k_ready) return;  // one compare per stage; the division below only on a miss
     const int kb = k / bn1;
-    if (kb <= known) return;
     const uint64_t t0 = trace_now();
     if (uniform((int)(threadIdx.x >> 6)) == 0) {  // wave 0, as a scalar branch
       const int lane = threadIdx.x & 63;
@@ -659,7 +659,8 @@ struct ReadyWait {
       if (lane == 0) *s_known = hi >= 0 ? hi : 0x7fffffff;
     }
     __syncthreads();
-    known = uniform(*s_known);
+    const int known = uniform(*s_known);
+    k_ready = known >= kb_last ? 0x7fffffff : (known + 1) * bn1;
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     // Every wave has read *s_known before wave 0 may write it again: the
     // pipeline prologue calls this back to back, with no other barrier between.

@@ -200,7 +200,7 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
   const int zlast = a.Mb * T::BM - 1;
   if constexpr (WAIT) {
     ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1, epoch + 1u, a.spin_limit, s_slot,
-                -1, &tr};
+                0, &tr};
     ClaimAtLastStage<ReadyWait, C> hook{w, &next, kend - kBK};
     mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   } else {

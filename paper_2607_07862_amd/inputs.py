@@ -74,6 +74,14 @@ WORKLOADS = {
 }
 WORKLOAD_ORDER = ["tiny", "l8b_decode", "l8b_prefill", "l70b_gated", "l70b_shard8"]
 
+# The paper's own workload (Sec. IV): Y = X A B with both weight matrices
+# fixed at 8192 x 8192, no activation between the layers, and the row count
+# of X swept over 1024 ... 32768.  A shape study beside the five workloads.
+PAPER_ORDER = []
+for _i, _m in enumerate((1024, 2048, 4096, 8192, 16384, 32768)):
+    WORKLOADS[f"paper_m{_m}"] = Workload(f"paper-{_m}x8192x8192-identity", _m, 8192, 8192, ACT_IDENTITY, 10 + _i)
+    PAPER_ORDER.append(f"paper_m{_m}")
+
 
 def _randn_bf16(gen: torch.Generator, shape, std: float) -> torch.Tensor:
     t = torch.randn(*shape, generator=gen, dtype=torch.float32)

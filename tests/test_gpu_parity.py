@@ -60,7 +60,8 @@ def test_small_shapes_against_full_oracle(lib, M, H, F, act, tuning):
 
 
 def _workload_params():
-    return [pytest.param(k, id=k) for k in I.WORKLOAD_ORDER]
+    # the five workloads, and the smallest of the paper's own shapes
+    return [pytest.param(k, id=k) for k in I.WORKLOAD_ORDER + ["paper_m1024"]]
 
 
 _cache = {}

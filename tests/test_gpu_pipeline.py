@@ -27,21 +27,27 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("order", [B.ORDER_AUTO, B.ORDER_ROW_FIRST, B.ORDER_REVERSED, B.ORDER_SHUFFLED,
-                                   B.ORDER_COLUMN_FIRST])
+                                   B.ORDER_COLUMN_FIRST, B.ORDER_BANDED])
 @pytest.mark.parametrize("grid", [1, 2, 3, 4, 17, 0])
 def test_orders_and_grids_match_sequential_bits(lib, order, grid):
     M, H, F, act = 160, 256, 768, 1
     d = I.make_inputs(M, H, F, act, seed=40 + order)
     g = device_inputs(d)
-    plan = B.Plan(M, H, F, act, {"bm": 64, "splitk1": 2, "splitk2": 3})
-    Ys = run(plan, g, B.MODE_SEQUENTIAL)
+    # split-K 1 for the banded order (bands apply to unsplit GEMM1 tiles), else 2 and 3
+    tun = {"bm": 32, "splitk1": 1, "splitk2": 1} if order == B.ORDER_BANDED else {"bm": 64, "splitk1": 2, "splitk2": 3}
+    plan = B.Plan(M, H, F, act, tun)
+    Ys = run(plan, g, B.MODE_SEQUENTIAL).clone()
     plan.set_option(B.OPT_ORDER, order)
     if grid:
         plan.set_option(B.OPT_GRID, grid)
-    Yp = run(plan, g, B.MODE_TILE_PIPELINED)
+    Yp = run(plan, g, B.MODE_TILE_PIPELINED).clone()
+    Yq = run(plan, g, B.MODE_WORKQUEUE)
+    Ys2 = run(plan, g, B.MODE_SEQUENTIAL)
     torch.cuda.synchronize()
     assert plan.check() == B.OK
     assert_bit_equal(Ys, Yp, f"order {order} grid {grid}")
+    assert_bit_equal(Ys, Yq, f"order {order} grid {grid} workqueue")
+    assert_bit_equal(Ys, Ys2, f"order {order} grid {grid} sequential after the order change")
     plan.close()
 
 

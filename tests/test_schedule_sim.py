@@ -39,9 +39,21 @@ def xcd_grouped(Mb, N, wave):
     return out
 
 
+def banded(Mb, N, wave, band):
+    """The host's row bands: `band` row blocks with all their column blocks,
+    band after band, each dealt like xcd_grouped."""
+    out = []
+    for r0 in range(0, Mb, band):
+        rb = min(band, Mb - r0)
+        out += [(t // rb) * Mb + r0 + t % rb for t in xcd_grouped(rb, N, wave)]
+    return out
+
+
 def column_first_tiles(Mb, Nb1, order, seed=12345, S2=1, wave=16):
     if order == "xcd":
         return xcd_grouped(Mb, Nb1, wave)
+    if order == "banded":
+        return banded(Mb, Nb1, wave, max(1, wave // Nb1))
     if order == "halves":  # column-first over each half of the row blocks (a stress order)
         per = -(-Mb // 2)
         return [nb * Mb + mb for g0 in range(0, Mb, per) for nb in range(Nb1) for mb in range(g0, min(Mb, g0 + per))]
@@ -58,7 +70,8 @@ def column_first_tiles(Mb, Nb1, order, seed=12345, S2=1, wave=16):
 def items(Mb, Nb1, Nb2, S1, S2, order, consumers_first=False, merged_lag=None):
     """Rank-ordered items: (kind, tile, s, needs) with needs = GEMM1 tiles a GEMM2 part reads.
 
-    merged_lag: place each GEMM2 item right after rank (last producer rank + lag), as the
+    merged_lag: place each GEMM2 item right after rank (last producer rank + lag), or after
+    every GEMM1 item in GEMM2 order when lag >= the GEMM1 count, as the
     pipelined kernel's merged table does, instead of after every GEMM1 item."""
     g1 = [("g1", t, s, []) for t in column_first_tiles(Mb, Nb1, order, S2=S2) for s in range(S1)]
     per = -(-Nb1 // S2)
@@ -74,7 +87,8 @@ def items(Mb, Nb1, Nb2, S1, S2, order, consumers_first=False, merged_lag=None):
         for r, it in enumerate(g1):
             last[it[1]] = r
         keyed = [(r, 0, it) for r, it in enumerate(g1)]
-        keyed += [(max((last[n] for n in it[3]), default=-1) + merged_lag, 1, it) for it in g2]
+        keyed += [(len(g1) if merged_lag >= len(g1) else max((last[n] for n in it[3]), default=-1) + merged_lag, 1, it)
+                  for it in g2]
         keyed.sort(key=lambda k: (k[0], k[1]))
         return [k[2] for k in keyed]
     return g2 + g1 if consumers_first else g1 + g2
@@ -181,10 +195,10 @@ def test_pipelined_schedule_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
             assert simulate(lst, S1, S2, grid, seed), (order, grid, seed)
 
 
-@pytest.mark.parametrize("order", ["auto", "xcd", "row", "shuffled", "halves"])
+@pytest.mark.parametrize("order", ["auto", "xcd", "banded", "row", "shuffled", "halves"])
 @pytest.mark.parametrize("Mb,Nb1,Nb2,S1,S2", CASES)
 def test_merged_rank_table_finishes_for_any_grid(order, Mb, Nb1, Nb2, S1, S2):
-    for lag in (0, 1, 5, 40):
+    for lag in (0, 1, 5, 40, Mb * Nb1 * S1):  # the last: every GEMM2 item after every GEMM1 item
         lst = items(Mb, Nb1, Nb2, S1, S2, order, merged_lag=lag)
         rank = {id(it): r for r, it in enumerate(lst)}
         g1_rank = {(it[1]): r for r, it in enumerate(lst) if it[0] == "g1"}
@@ -380,3 +394,11 @@ def test_counter_targets_hold_across_any_sequence_of_modes(seed):
             assert (arrivals == (epoch + 1) * S) == (s == S - 1)
         epoch += 1
         wq += mode == "workqueue"
+
+
+@pytest.mark.parametrize("Mb,N,wave,band", [(128, 64, 512, 8), (16, 112, 512, 4), (5, 7, 8, 2), (3, 10, 17, 1), (40, 3, 64, 21)])
+def test_banded_deal_is_a_permutation_band_by_band(Mb, N, wave, band):
+    order = banded(Mb, N, wave, band)
+    assert sorted(order) == list(range(Mb * N))
+    bands = [(t % Mb) // band for t in order]
+    assert bands == sorted(bands)  # every tile of a band before the next band
