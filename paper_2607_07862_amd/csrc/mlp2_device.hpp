@@ -323,29 +323,60 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     b_frag[tp] = T::A_BYTES + brow * (2 * T::BN) + ((q ^ swz_b<T::BN>(brow)) << 4);
   }
 
+  // Two K halves of 32 per stage.  With a two-stage ring every fragment of
+  // the stage is read before its first product: the reads of the second
+  // half and of the later column pairs then overlap the first products in
+  // whatever code the mainloop is inlined into (the one-launch kernels' item
+  // loop otherwise schedules one read pair ahead of its four products).
+  // Deeper rings keep each half's reads next to its products.  Both orders
+  // accumulate every output in the same sequence (first half, then second).
+  auto weight_frag = [&](const char* base, int ks, int b, int i) {
+    const char* p = base + b * T::B_BYTES + b_frag[i / 2] + ks * 32 * (2 * T::BN) + (i % 2) * 8;
+    bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p));
+    bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p + 4 * (2 * T::BN)));
+    return (bf16x8)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  };
+  auto act_frag = [&](const char* base, int ks, int tm) {
+    return *reinterpret_cast<const bf16x8*>(base + (ks ? a_frag1 : a_frag0) + tm * 16 * 128);
+  };
   auto compute = [&](int st) {
     const char* base = lds + (st % T::NS) * SB;
+    if constexpr (T::NS == 2) {
+      bf16x8 xf[kBK / 32][T::TM];
+      bf16x8 wf[kBK / 32][NB][T::TN];
 #pragma unroll
-    for (int ks = 0; ks < kBK / 32; ++ks) {
-      bf16x8 xf[T::TM];
+      for (int ks = 0; ks < kBK / 32; ++ks) {
 #pragma unroll
-      for (int tm = 0; tm < T::TM; ++tm)
-        xf[tm] = *reinterpret_cast<const bf16x8*>(base + (ks ? a_frag1 : a_frag0) + tm * 16 * 128);
+        for (int tm = 0; tm < T::TM; ++tm) xf[ks][tm] = act_frag(base, ks, tm);
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int tp = 0; tp < T::TN / 2; ++tp) {
+          for (int i = 0; i < T::TN; ++i) wf[ks][b][i] = weight_frag(base, ks, b, i);
+      }
 #pragma unroll
-          for (int t2 = 0; t2 < 2; ++t2) {
-            const char* p = base + b * T::B_BYTES + b_frag[tp] + ks * 32 * (2 * T::BN) + t2 * 8;
-            bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p));
-            bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(p + 4 * (2 * T::BN)));
-            bf16x8 wf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      for (int ks = 0; ks < kBK / 32; ++ks)
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int i = 0; i < T::TN; ++i)
 #pragma unroll
             for (int tm = 0; tm < T::TM; ++tm)
-              acc[b][2 * tp + t2][tm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xf[tm], acc[b][2 * tp + t2][tm], 0, 0, 0);
+              acc[b][i][tm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[ks][b][i], xf[ks][tm], acc[b][i][tm], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < kBK / 32; ++ks) {
+        bf16x8 xf[T::TM];
+#pragma unroll
+        for (int tm = 0; tm < T::TM; ++tm) xf[tm] = act_frag(base, ks, tm);
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int i = 0; i < T::TN; ++i) {
+            const bf16x8 wf = weight_frag(base, ks, b, i);
+#pragma unroll
+            for (int tm = 0; tm < T::TM; ++tm)
+              acc[b][i][tm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, xf[tm], acc[b][i][tm], 0, 0, 0);
           }
-        }
       }
     }
   };
