@@ -203,8 +203,10 @@ int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
  * real-time counter; the marks are: for a GEMM1 tile that signals, its Z
  * stores complete and its ready counter released; for a split-K part that
  * does not complete its tile, its partial stored and its arrival counted;
- * 0 and 0 otherwise), ticks waiting for the tile loads of the work-group's own ring,
- * ticks waiting for ready counters and split-K siblings.  Items beyond records_per_group are counted, not stored.
+ * 0 and 0 otherwise), the item's core clock cycles (shader-clock counter,
+ * high 32 bits) above its ticks waiting for the tile loads of the
+ * work-group's own ring (low 32 bits), ticks waiting for ready counters and
+ * split-K siblings.  Items beyond records_per_group are counted, not stored.
  * G is the largest of the plan's grids (grid_pipelined, grid_gemm1,
  * grid_gemm2 of mlp2_plan_info); the buffer must hold
  * 2 * G * (1 + 8 * records_per_group) words.  Returns MLP2_OK, MLP2_ERR_INVALID_ARG

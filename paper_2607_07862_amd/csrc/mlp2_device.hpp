@@ -99,10 +99,18 @@ constexpr int kTraceWords = 8;
 
 struct TraceAcc {
   uint64_t ring = 0, flag = 0, t_main = 0, t_rel = 0, t_wait = 0;
+  uint64_t c_start = 0;  // shader-clock counter at the item's start
 };
 
 __device__ __forceinline__ uint64_t trace_now() {
   if constexpr (kTrace) return __builtin_amdgcn_s_memrealtime();
+  return 0;
+}
+
+// Shader-clock counter (core clock cycles): beside the real-time counter it
+// gives the clock an item ran at.
+__device__ __forceinline__ uint64_t trace_clock() {
+  if constexpr (kTrace) return __builtin_amdgcn_s_memtime();
   return 0;
 }
 

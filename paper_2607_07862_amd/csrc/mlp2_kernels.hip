@@ -88,7 +88,7 @@ __device__ __forceinline__ void tr_record(const Args& a, int section, int n, int
   r[3] = tr.t_rel;
   r[4] = tr.t_wait;
   r[5] = trace_now();
-  r[6] = tr.ring;
+  r[6] = ((trace_clock() - tr.c_start) << 32) | (uint32_t)tr.ring;  // core cycles | ring-wait ticks
   r[7] = tr.flag;
 }
 
@@ -340,6 +340,7 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
     if (p >= total) break;
     __syncthreads();  // every wave has read s_item before the item's claim rewrites it
     TraceAcc tr;
+    if constexpr (kTrace) tr.c_start = trace_clock();
     const uint64_t t_start = trace_now();
     Claim next = make_claim(a);
     uint32_t e;  // order-table entry: item id, bit 31 set for a GEMM2 item
@@ -364,14 +365,17 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
   if constexpr (PHASE == PHASE_WORKQUEUE) {
     __syncthreads();  // every wave is done with s_item before pop_ready rewrites it
     uint64_t t_pop = trace_now();  // a unit's trace starts when its work-group begins to pop it
+    uint64_t c_pop = trace_clock();
     for (int q = pop_ready(a, wq_epoch, &s_item); q >= 0; q = pop_ready(a, wq_epoch, &s_item)) {
       TraceAcc tr;
+      if constexpr (kTrace) tr.c_start = c_pop;
       if constexpr (kTrace) tr.flag = trace_now() - t_pop;  // waiting for the queue slot to fill
       NoClaim none;
       gemm2_item<T2, HV, false, NoClaim>(a, q, epoch, lds, &s_slot, none, &s_item, tr);
       if constexpr (kTrace) tr_record(a, 0, n_items++, -1, 0x80000000u | (uint32_t)q, t_pop, tr);
       __syncthreads();  // the item's divergent stores close, and s_item is free again
       t_pop = trace_now();
+      c_pop = trace_clock();
     }
   }
   finish_kernel(a, epoch, PHASE != PHASE_GEMM1, PHASE == PHASE_WORKQUEUE, wq_epoch);

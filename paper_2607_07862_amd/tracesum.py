@@ -8,10 +8,12 @@ then one traced warm run per mode.  Per item kind it reports the mean item
 time split into mainloop, waits for the work-group's own ring loads, flag
 waits (ready counters in the pipelined mode; in the workqueue mode the wait
 for the popped queue slot to fill, counted from when the work-group began to
-pop) and epilogue, and for the GEMM2 items of the two one-launch modes the
-share of their time spent in flag waits beside the wait their producers'
+pop) and epilogue, the item's core clock cycles and the clock they imply
+(cycles over real time), and for the GEMM2 items of the two one-launch modes
+the share of their time spent in flag waits beside the wait their producers'
 completion times imply (the latest end among the GEMM1 items that write the
-Z columns the item reads, minus the item's start).
+Z columns the item reads, minus the item's start).  A second table gives each
+mode's clock over eighths of its run.
 """
 from __future__ import annotations
 
@@ -24,11 +26,11 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 
 TICK_US = 0.01  # 100 MHz device real-time counter
-CAP = 64        # records per work-group
+CAP = 128       # records per work-group
 
 
 def _records(buf, G):
-    """(kind, item, rank, start, main, end, ring, flag) per recorded item, sections merged."""
+    """(kind, item, rank, start, main, end, ring, flag, cycles) per recorded item, sections merged."""
     import numpy as np
 
     a = buf.cpu().numpy().reshape(2, G, 1 + 8 * CAP)
@@ -41,7 +43,8 @@ def _records(buf, G):
                 w0 = int(r[0])
                 entry, rank = w0 & 0xFFFFFFFF, w0 >> 32
                 kind = 1 if entry & 0x80000000 else 0
-                out.append((kind, entry & 0x7FFFFFFF, rank, int(r[1]), int(r[2]), int(r[5]), int(r[6]), int(r[7])))
+                ring, cycles = int(r[6]) & 0xFFFFFFFF, int(r[6]) >> 32
+                out.append((kind, entry & 0x7FFFFFFF, rank, int(r[1]), int(r[2]), int(r[5]), ring, int(r[7]), cycles))
     return out
 
 
@@ -73,7 +76,7 @@ def summarise(B, I, bench, key):
         r.run(B.MODE_TILE_PIPELINED)
         r.run(B.MODE_SEQUENTIAL)
     torch.cuda.synchronize()
-    rows = []
+    rows, clocks = [], []
     for mode, name in ((B.MODE_SEQUENTIAL, "sequential"), (B.MODE_TILE_PIPELINED, "pipelined"),
                        (B.MODE_WORKQUEUE, "workqueue")):
         buf.zero_()
@@ -84,11 +87,12 @@ def summarise(B, I, bench, key):
         recs = _records(buf, G)
         t0 = min(x[3] for x in recs)
         span = (max(x[5] for x in recs) - t0) * TICK_US
+        clocks.append((name, span, clock_by_eighth(recs, t0)))
         for kind in (0, 1):
             K = [x for x in recs if x[0] == kind]
             if not K:
                 continue
-            R = np.array([x[3:] for x in K], dtype=np.float64)  # start, main, end, ring, flag
+            R = np.array([x[3:] for x in K], dtype=np.float64)  # start, main, end, ring, flag, cycles
             item = (R[:, 2] - R[:, 0]) * TICK_US
             main = (R[:, 1] - R[:, 0]) * TICK_US
             ring, flag = R[:, 3] * TICK_US, R[:, 4] * TICK_US
@@ -96,6 +100,7 @@ def summarise(B, I, bench, key):
                 "mode": name, "kind": "GEMM1" if kind == 0 else "GEMM2", "n": len(K), "span": span,
                 "item": item.mean(), "main": main.mean(), "ring": ring.mean(), "flag": flag.mean(),
                 "epi": (item - main).mean(), "flag_share": flag.sum() / item.sum(),
+                "kcycles": R[:, 5].mean() / 1e3, "mhz": R[:, 5].sum() / item.sum(),
             }
             if kind == 1 and name != "sequential":
                 S1 = info["splitk1"]
@@ -113,7 +118,19 @@ def summarise(B, I, bench, key):
     del g
     torch.cuda.empty_cache()
     tiles = [info[k] for k in ("bm", "bn1", "splitk1", "bn2", "splitk2", "stages")]
-    return w, tiles, rows
+    return w, tiles, rows, clocks
+
+
+def clock_by_eighth(recs, t0):
+    """Mean clock (MHz) of the items ending in each eighth of the run (cycles over real time)."""
+    end = max(x[5] for x in recs)
+    width = (end - t0) / 8 or 1
+    out = []
+    for e in range(8):
+        sel = [x for x in recs if t0 + e * width <= x[5] < t0 + (e + 1) * width or (e == 7 and x[5] == end)]
+        ticks = sum(x[5] - x[3] for x in sel)
+        out.append(sum(x[8] for x in sel) / (ticks * TICK_US) if ticks else float("nan"))
+    return out
 
 
 def main():
@@ -126,14 +143,18 @@ def main():
     import bench
 
     B.load()
-    lines = ["| workload | mode | launch µs | kind | items | item µs | mainloop µs | ring wait µs | flag wait µs | epilogue µs | flag share | producer-implied wait µs |",
-             "|---|---|---:|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    lines = ["| workload | mode | launch µs | kind | items | item µs | mainloop µs | ring wait µs | flag wait µs | epilogue µs | flag share | producer-implied wait µs | k cycles / item | clock MHz |",
+             "|---|---|---:|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    clock_lines = ["| workload | mode | launch µs | clock MHz in each eighth of the run |", "|---|---|---:|---|"]
     for key in args.workloads.split(","):
-        w, tiles, rows = summarise(B, I, bench, key)
+        w, tiles, rows, clocks = summarise(B, I, bench, key)
         for x in rows:
             implied = f"{x['implied']:.1f}" if "implied" in x else ""
             lines.append(f"| {key} {tiles} | {x['mode']} | {x['span']:.1f} | {x['kind']} | {x['n']} | {x['item']:.1f} | "
-                         f"{x['main']:.1f} | {x['ring']:.1f} | {x['flag']:.1f} | {x['epi']:.2f} | {100 * x['flag_share']:.1f} % | {implied} |")
+                         f"{x['main']:.1f} | {x['ring']:.1f} | {x['flag']:.1f} | {x['epi']:.2f} | {100 * x['flag_share']:.1f} % | {implied} | "
+                         f"{x['kcycles']:.1f} | {x['mhz']:.0f} |")
+        for name, span, c in clocks:
+            clock_lines.append(f"| {key} | {name} | {span:.1f} | " + " ".join(f"{v:.0f}" for v in c) + " |")
         print(lines[-1] if rows else key, flush=True)
     cmd = " ".join(["python -m paper_2607_07862_amd.tracesum"] + sys.argv[1:])
     head = ["# Flag waits and where item time goes (timing-trace build, one warm run per mode)", "",
@@ -143,8 +164,9 @@ def main():
             "time (pipelined: waits on ready counters; workqueue: the wait for the popped queue slot to fill, the",
             "item starting when its work-group began to pop); the producer-implied wait is, per GEMM2 item of the",
             "two one-launch modes, the latest end among the GEMM1 items writing the Z columns it reads minus its",
-            "start (0 when they were done before it started).", ""]
-    text = "\n".join(head + lines) + "\n"
+            "start (0 when they were done before it started).  Cycles are the item's core clock cycles",
+            "(shader-clock counter); the clock is cycles over the item's real time.", ""]
+    text = "\n".join(head + lines + ["", "Clock over the run (items grouped by the eighth of the run they end in):", ""] + clock_lines) + "\n"
     if args.out:
         with open(args.out, "w") as f:
             f.write(text)
