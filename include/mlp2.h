@@ -114,7 +114,10 @@ typedef struct mlp2_tuning {
                     device at once)                                                      */
   int order;     /* enum mlp2_order (0 = MLP2_ORDER_AUTO)                                 */
   int stages;    /* LDS ring depth of the tile mainloop (2, 3 or 4, as built for the shape)*/
-  int reserved[6];
+  int row_group; /* rows per launch group: 0 = automatic (groups once Z of all rows exceeds
+                    the 256 MB last-level cache), -1 = one launch over all rows, else a
+                    multiple of 256 (groups of that many rows, the last one shorter)      */
+  int reserved[5];
 } mlp2_tuning_t;
 
 /* What a plan chose, for reports and tests. */
@@ -135,7 +138,9 @@ typedef struct mlp2_info {
   int stages;            /* LDS ring depth                                  */
   int grid_gemm1;        /* persistent work-groups of the GEMM1 launch      */
   int grid_gemm2;        /* persistent work-groups of the GEMM2 launch      */
-  int reserved[5];
+  int row_group;         /* rows per launch group (0: one launch over all rows);
+                            the tile fields above are those of a whole group */
+  int reserved[4];
 } mlp2_info_t;
 
 /* Create a plan for Y[M,H] = act(X[M,H] . W1) . W2 on the current HIP device.
@@ -154,7 +159,10 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
  * stream) in `mode`.  Asynchronous: no host synchronisation, no allocation.
  * X, W1, W2, Y are device pointers laid out as described above; Y must not
  * overlap any input.  Runs of one plan on one stream are ordered; the plan
- * keeps its counters consistent across runs and modes without host resets. */
+ * keeps its counters consistent across runs and modes without host resets.
+ * A plan with row groups (mlp2_info_t.row_group > 0) enqueues the mode's
+ * launches once per group of rows, in row order; rows do not interact, and
+ * every mode uses the same groups, so the modes still agree bit for bit. */
 int mlp2_run(mlp2_plan_t plan, const void* X, const void* W1, const void* W2, void* Y, void* stream, int mode);
 
 /* Free the plan and its workspace (synchronises the device first).  NULL-safe. */
@@ -175,7 +183,8 @@ int mlp2_check(mlp2_plan_t plan);
 int mlp2_plan_info(mlp2_plan_t plan, mlp2_info_t* out);
 
 /* Device pointer to the plan's bf16 intermediate Z, laid out [row_blocks*bm, F]
- * row-major (rows >= M are padding).  Valid until mlp2_destroy.  For tests and
+ * row-major (rows >= M are padding; with row groups, Z of every group at its
+ * rows).  Valid until mlp2_destroy.  For tests and
  * diagnostics; NULL on a NULL plan. */
 const void* mlp2_intermediate(mlp2_plan_t plan);
 
@@ -208,7 +217,8 @@ int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
  * work-group's own ring (low 32 bits), ticks waiting for ready counters and
  * split-K siblings.  Items beyond records_per_group are counted, not stored.
  * G is the largest of the plan's grids (grid_pipelined, grid_gemm1,
- * grid_gemm2 of mlp2_plan_info); the buffer must hold
+ * grid_gemm2 of mlp2_plan_info; with row groups the records are those of
+ * the last whole group's launches, the shorter last group records nothing); the buffer must hold
  * 2 * G * (1 + 8 * records_per_group) words.  Returns MLP2_OK, MLP2_ERR_INVALID_ARG
  * or MLP2_ERR_UNSUPPORTED. */
 int mlp2_trace_attach(mlp2_plan_t plan, void* buffer, int records_per_group);

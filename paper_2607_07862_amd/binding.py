@@ -49,7 +49,8 @@ class Tuning(ctypes.Structure):
         ("grid", ctypes.c_int),
         ("order", ctypes.c_int),
         ("stages", ctypes.c_int),
-        ("reserved", ctypes.c_int * 6),
+        ("row_group", ctypes.c_int),
+        ("reserved", ctypes.c_int * 5),
     ]
 
 
@@ -79,7 +80,8 @@ class Info(ctypes.Structure):
         ("stages", ctypes.c_int),
         ("grid_gemm1", ctypes.c_int),
         ("grid_gemm2", ctypes.c_int),
-        ("reserved", ctypes.c_int * 5),
+        ("row_group", ctypes.c_int),
+        ("reserved", ctypes.c_int * 4),
     ]
 
 

@@ -54,6 +54,13 @@ struct mlp2_plan_s {
   uint32_t* orderp = nullptr;
   int64_t lead1 = 0;  // leading ranks of the pipelined table that are GEMM1 items (they never wait)
   size_t counters_off = 0, counters_bytes = 0;
+  // Row groups (group_rows_for): a grouped plan runs as back-to-back launches
+  // of `group` over whole groups of group_rows rows and of `tail` over the
+  // remaining rows; every launch writes its rows of this plan's Z.
+  int64_t group_rows = 0;
+  mlp2_plan_s* group = nullptr;
+  mlp2_plan_s* tail = nullptr;
+  bool z_external = false;  // a group's plan: Z belongs to the grouped plan
 };
 
 namespace {
@@ -316,6 +323,20 @@ const char* mlp2_strerror(int code) {
   }
 }
 
+}  // extern "C"
+
+namespace {
+
+mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuning_t& tz, int dev,
+                       const hipDeviceProp_t& prop, uint16_t* z_ext);
+mlp2_plan_s* make_grouped(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuning_t& tz, int dev,
+                          const hipDeviceProp_t& prop, int64_t rows);
+int64_t group_rows_for(int64_t M, int64_t F, const mlp2_tuning_t& tz);
+
+}  // namespace
+
+extern "C" {
+
 mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, const mlp2_tuning_t* t) {
   g_last_error = MLP2_OK;
   if (M < 1 || H < 1 || F < 1) { fail(MLP2_ERR_INVALID_ARG); return nullptr; }
@@ -325,12 +346,11 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
     fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
   }
-  const int nb = act == MLP2_ACT_SWIGLU ? 2 : 1;
   mlp2_tuning_t tz;
   std::memset(&tz, 0, sizeof(tz));
   if (t) tz = *t;
   if (tz.bm < 0 || tz.bn1 < 0 || tz.bn2 < 0 || tz.splitk1 < 0 || tz.splitk2 < 0 || tz.grid < 0 || tz.order < 0 || tz.stages < 0 ||
-      tz.order > MLP2_ORDER_BANDED) {
+      tz.order > MLP2_ORDER_BANDED || tz.row_group < -1 || (tz.row_group > 0 && tz.row_group % 256)) {
     fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
   }
@@ -339,7 +359,65 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   if (hipGetDevice(&dev) != hipSuccess || !is_gfx950(dev)) { fail(MLP2_ERR_DEVICE); return nullptr; }
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, dev) != hipSuccess) { fail(MLP2_ERR_HIP); return nullptr; }
+  const int64_t rows = group_rows_for(M, F, tz);
+  return rows ? make_grouped(M, H, F, act, tz, dev, prop, rows) : make_plan(M, H, F, act, tz, dev, prop, nullptr);
+}
 
+}  // extern "C"
+
+namespace {
+
+// Rows per launch group: 0 runs the plan as one launch of each kernel.
+// Automatic: once the bf16 Z of all rows exceeds the 256 MB last-level
+// cache, groups of the most rows whose Z fits (a multiple of 256), at least
+// 8192 of them.  Measured with 8192 x 8192 weights: at 32768 rows two
+// groups of 16384 take the sequential mode from 9.4 to 8.2 ms and the
+// pipelined one from 10.4 to 8.0 ms (one launch of the pipelined kernel
+// over all rows loses its clock), while at 16384 rows one launch is best.
+int64_t group_rows_for(int64_t M, int64_t F, const mlp2_tuning_t& tz) {
+  if (tz.row_group == -1) return 0;
+  if (tz.row_group > 0) return tz.row_group < M ? tz.row_group : 0;
+  const int64_t fit = ((int64_t)256 << 20) / (F * 2) / 256 * 256;
+  return fit >= 8192 && M > fit ? fit : 0;
+}
+
+// A plan over whole groups of `rows` rows plus one over the rest, sharing
+// one Z of every row (with room for the last group's tile padding: groups
+// of a multiple of 256 rows hold whole row blocks, so only the last one pads).
+mlp2_plan_s* make_grouped(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuning_t& tz, int dev,
+                          const hipDeviceProp_t& prop, int64_t rows) {
+  auto* p = new mlp2_plan_s();
+  p->M = M; p->H = H; p->F = F; p->act = act; p->device = dev;
+  p->num_cus = prop.multiProcessorCount;
+  p->order = tz.order;
+  p->group_rows = rows;
+  p->ws_bytes = align_up((size_t)(M + 256) * F * 2, 256);
+  if (hipMalloc(&p->ws, p->ws_bytes) != hipSuccess) {
+    delete p;
+    fail(MLP2_ERR_HIP);
+    return nullptr;
+  }
+  p->Z = (uint16_t*)p->ws;
+  const int64_t rest = M % rows;
+  if (hipMemset(p->Z, 0, p->ws_bytes) != hipSuccess ||
+      !(p->group = make_plan(rows, H, F, act, tz, dev, prop, p->Z)) ||
+      (rest && !(p->tail = make_plan(rest, H, F, act, tz, dev, prop, p->Z)))) {
+    const int code = g_last_error != MLP2_OK ? g_last_error : MLP2_ERR_HIP;
+    mlp2_destroy(p);
+    fail(code);
+    return nullptr;
+  }
+  if (p->group->kc.bm > 256 || rows % p->group->kc.bm) {  // whole row blocks per group
+    mlp2_destroy(p);
+    fail(MLP2_ERR_UNSUPPORTED);
+    return nullptr;
+  }
+  return p;
+}
+
+mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuning_t& tz, int dev,
+                       const hipDeviceProp_t& prop, uint16_t* z_ext) {
+  const int nb = act == MLP2_ACT_SWIGLU ? 2 : 1;
   auto* p = new mlp2_plan_s();
   p->M = M; p->H = H; p->F = F; p->act = act; p->device = dev;
   p->num_cus = prop.multiProcessorCount;
@@ -437,7 +515,7 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   const int64_t Mpad = (int64_t)p->Mb * bm;
   size_t off = 0;
   const size_t z_off = off;
-  off = align_up(off + (size_t)Mpad * F * 2, 256);
+  if (!z_ext) off = align_up(off + (size_t)Mpad * F * 2, 256);
   const size_t p1_off = off;
   if (p->S1 > 1) off = align_up(off + (size_t)p->items1 * nb * bm * bn1 * 4, 256);
   const size_t p2_off = off;
@@ -470,7 +548,8 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
     return nullptr;
   }
   char* b = (char*)p->ws;
-  p->Z = (uint16_t*)(b + z_off);
+  p->Z = z_ext ? z_ext : (uint16_t*)(b + z_off);
+  p->z_external = z_ext != nullptr;
   p->part1 = p->S1 > 1 ? (float*)(b + p1_off) : nullptr;
   p->part2 = p->S2 > 1 ? (float*)(b + p2_off) : nullptr;
   p->cnt1 = (uint32_t*)(b + c1_off);
@@ -484,7 +563,8 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   p->orderp = (uint32_t*)(b + ordp_off);
   p->counters_off = cnt_off;
   p->counters_bytes = cnt_end - cnt_off;
-  if (hipMemset(b + cnt_off, 0, cnt_end - cnt_off) != hipSuccess || hipMemset(p->Z, 0, (size_t)Mpad * F * 2) != hipSuccess ||
+  if (hipMemset(b + cnt_off, 0, cnt_end - cnt_off) != hipSuccess ||
+      (!z_ext && hipMemset(p->Z, 0, (size_t)Mpad * F * 2) != hipSuccess) ||
       upload_order(p) != MLP2_OK || hipDeviceSynchronize() != hipSuccess) {
     (void)hipFree(p->ws);
     delete p;
@@ -494,27 +574,28 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   return p;
 }
 
+}  // namespace
+
+extern "C" {
+
 mlp2_plan_t mlp2_plan(int64_t M, int64_t H, int64_t F, int act, int dtype) {
   return mlp2_plan_ex(M, H, F, act, dtype, nullptr);
 }
 
-int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void* Y, void* stream, int mode) {
-  if (!p || !X || !W1 || !W2 || !Y) return fail(MLP2_ERR_INVALID_ARG);
-  if (mode != MLP2_MODE_SEQUENTIAL && mode != MLP2_MODE_TILE_PIPELINED && mode != MLP2_MODE_WORKQUEUE)
-    return fail(MLP2_ERR_INVALID_ARG);
-  if (((uintptr_t)X | (uintptr_t)W1 | (uintptr_t)W2 | (uintptr_t)Y) & 15u) return fail(MLP2_ERR_ALIGNMENT);
-  const int nb = p->act == MLP2_ACT_SWIGLU ? 2 : 1;
-  const size_t xb = (size_t)p->M * p->H * 2, w1b = (size_t)nb * p->H * p->F * 2, w2b = (size_t)p->F * p->H * 2;
-  if (overlaps(Y, xb, X, xb) || overlaps(Y, xb, W1, w1b) || overlaps(Y, xb, W2, w2b)) return fail(MLP2_ERR_INVALID_ARG);
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev != p->device) return fail(MLP2_ERR_DEVICE);
+}  // extern "C"
 
+namespace {
+
+// One evaluation of a single-launch plan (each kernel launched once) with
+// its Z rows at Z.
+int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void* W2, void* Y, uint16_t* Z, hipStream_t s,
+                int mode) {
   Args a;
   a.X = (const uint16_t*)X;
   a.W1 = (const uint16_t*)W1;
   a.W2 = (const uint16_t*)W2;
   a.Y = (uint16_t*)Y;
-  a.Z = p->Z;
+  a.Z = Z;
   a.part1 = p->part1;
   a.part2 = p->part2;
   a.cnt1 = p->cnt1;
@@ -545,7 +626,6 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   a.trace = p->trace;
   a.trace_cap = p->trace_cap;
 
-  hipStream_t s = (hipStream_t)stream;
   const int go = p->grid_override;
   const int grids[2] = {go ? go : p->grid1, go ? go : p->grid2};
   const int gridp = go ? go : p->grid;
@@ -579,8 +659,39 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   return MLP2_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void* Y, void* stream, int mode) {
+  if (!p || !X || !W1 || !W2 || !Y) return fail(MLP2_ERR_INVALID_ARG);
+  if (mode != MLP2_MODE_SEQUENTIAL && mode != MLP2_MODE_TILE_PIPELINED && mode != MLP2_MODE_WORKQUEUE)
+    return fail(MLP2_ERR_INVALID_ARG);
+  if (((uintptr_t)X | (uintptr_t)W1 | (uintptr_t)W2 | (uintptr_t)Y) & 15u) return fail(MLP2_ERR_ALIGNMENT);
+  const int nb = p->act == MLP2_ACT_SWIGLU ? 2 : 1;
+  const size_t xb = (size_t)p->M * p->H * 2, w1b = (size_t)nb * p->H * p->F * 2, w2b = (size_t)p->F * p->H * 2;
+  if (overlaps(Y, xb, X, xb) || overlaps(Y, xb, W1, w1b) || overlaps(Y, xb, W2, w2b)) return fail(MLP2_ERR_INVALID_ARG);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != p->device) return fail(MLP2_ERR_DEVICE);
+
+  hipStream_t s = (hipStream_t)stream;
+  if (!p->group) return launch_plan(p, X, W1, W2, Y, p->Z, s, mode);
+  // Row groups, in order on the stream: each group's launches read its rows
+  // of X and write its rows of Z and Y.
+  const int64_t R = p->group_rows;
+  int64_t r0 = 0;
+  for (; r0 + R <= p->M; r0 += R) {
+    const int rc = launch_plan(p->group, (const uint16_t*)X + r0 * p->H, W1, W2, (uint16_t*)Y + r0 * p->H, p->Z + r0 * p->F, s, mode);
+    if (rc != MLP2_OK) return rc;
+  }
+  if (p->tail) return launch_plan(p->tail, (const uint16_t*)X + r0 * p->H, W1, W2, (uint16_t*)Y + r0 * p->H, p->Z + r0 * p->F, s, mode);
+  return MLP2_OK;
+}
+
 void mlp2_destroy(mlp2_plan_t p) {
   if (!p) return;
+  mlp2_destroy(p->group);
+  mlp2_destroy(p->tail);
   int cur = -1;
   (void)hipGetDevice(&cur);
   if (cur != p->device) (void)hipSetDevice(p->device);
@@ -592,6 +703,11 @@ void mlp2_destroy(mlp2_plan_t p) {
 
 int mlp2_check(mlp2_plan_t p) {
   if (!p) return fail(MLP2_ERR_INVALID_ARG);
+  if (p->group) {  // every group's plan is checked (and recovered) in turn
+    const int a = mlp2_check(p->group);
+    const int b = p->tail ? mlp2_check(p->tail) : MLP2_OK;
+    return a != MLP2_OK ? fail(a) : b != MLP2_OK ? fail(b) : MLP2_OK;
+  }
   uint32_t ctrl[mlp2::CTRL_WORDS];
   if (hipMemcpy(ctrl, p->ctrl, sizeof(ctrl), hipMemcpyDeviceToHost) != hipSuccess) return fail(MLP2_ERR_HIP);
   if (ctrl[mlp2::CTRL_ERROR] == 0) return MLP2_OK;
@@ -603,6 +719,16 @@ int mlp2_check(mlp2_plan_t p) {
 
 int mlp2_plan_info(mlp2_plan_t p, mlp2_info_t* out) {
   if (!p || !out) return fail(MLP2_ERR_INVALID_ARG);
+  if (p->group) {  // what a whole group's launch chose, over this plan's rows
+    const int rc = mlp2_plan_info(p->group, out);
+    if (rc != MLP2_OK) return rc;
+    out->M = p->M;
+    out->row_blocks = (int)ceil_div(p->M, out->bm);
+    out->order = p->order;
+    out->workspace_bytes = (int64_t)(p->ws_bytes + p->group->ws_bytes + (p->tail ? p->tail->ws_bytes : 0));
+    out->row_group = (int)p->group_rows;
+    return MLP2_OK;
+  }
   std::memset(out, 0, sizeof(*out));
   out->M = p->M;
   out->H = p->H;
@@ -635,6 +761,12 @@ const void* mlp2_intermediate(mlp2_plan_t p) { return p ? p->Z : nullptr; }
 
 int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
   if (!p) return fail(MLP2_ERR_INVALID_ARG);
+  if (p->group) {  // every group's plan takes the option (a dropped signal: the whole groups')
+    int rc = mlp2_set_option(p->group, key, value);
+    if (rc == MLP2_OK && p->tail && key != MLP2_OPT_DROP_SIGNAL) rc = mlp2_set_option(p->tail, key, value);
+    if (rc == MLP2_OK && key == MLP2_OPT_ORDER) p->order = (int)value;
+    return rc;
+  }
   switch (key) {
     case MLP2_OPT_SPIN_LIMIT:
       if (value < 1 || value > 0xFFFFFFFFLL) return fail(MLP2_ERR_INVALID_ARG);
@@ -665,6 +797,7 @@ int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
 int mlp2_trace_attach(mlp2_plan_t p, void* buffer, int records_per_group) {
   if (!p || (buffer && records_per_group < 1) || ((uintptr_t)buffer & 7u)) return fail(MLP2_ERR_INVALID_ARG);
   if (!mlp2::kTrace) return fail(MLP2_ERR_UNSUPPORTED);
+  if (p->group) return mlp2_trace_attach(p->group, buffer, records_per_group);  // the whole groups' launches
   p->trace = (uint64_t*)buffer;
   p->trace_cap = buffer ? records_per_group : 0;
   return MLP2_OK;

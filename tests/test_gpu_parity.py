@@ -60,9 +60,10 @@ def test_small_shapes_against_full_oracle(lib, M, H, F, act, tuning):
 
 
 def _workload_params():
-    # the five workloads, the smallest of the paper's own shapes, and one
-    # large enough for the default row-band order (X + W1 above 256 MB)
-    return [pytest.param(k, id=k) for k in I.WORKLOAD_ORDER + ["paper_m1024", "paper_m16384"]]
+    # the five workloads, the smallest of the paper's own shapes, one large
+    # enough for the default row-band order (X + W1 above 256 MB) and one run
+    # in row groups by default (Z of all rows above 256 MB)
+    return [pytest.param(k, id=k) for k in I.WORKLOAD_ORDER + ["paper_m1024", "paper_m16384", "paper_m32768"]]
 
 
 _cache = {}
