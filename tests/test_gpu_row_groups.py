@@ -8,8 +8,11 @@
   one launch at 16384 rows);
 * a dropped producer signal in the whole groups' plan times out, mlp2_check
   reports it and the grouped plan recovers;
-* a grouped run captured into a graph replays with the eager bits.
+* a grouped run captured into a graph replays with the eager bits;
+* at full size (20000 rows of 8192 x 8192) the automatic groups, a shorter
+  last one included, match the oracle on rows around the group boundary.
 """
+import numpy as np
 import pytest
 import torch
 
@@ -123,4 +126,26 @@ def test_grouped_graph_replays_match_eager_runs(lib, mode):
     for n, y in enumerate(outs):
         assert_bit_equal(ref, y, f"mode {mode} replay {n}")
     del graph
+    plan.close()
+
+
+def test_full_size_groups_with_a_shorter_last_group(lib):
+    """20000 rows of the paper's 8192 x 8192 shape: one automatic group of
+    16384 rows and a last group of 3616, every mode bit-exact; the sampled
+    rows straddle the group boundary and include the last row."""
+    M, H, F, act = 20000, 8192, 8192, 0
+    d = I.make_inputs(M, H, F, act, seed=96)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act)
+    assert plan.info()["row_group"] == 16384
+    Ys, Zs, Yp, Zp = both_modes(plan, g)
+    assert_bit_equal(Ys, Yp, "Y sequential vs pipelined")
+    assert_bit_equal(Zs, Zp, "Z sequential vs pipelined")
+    Yq, _ = workqueue_mode(plan, g)
+    assert_bit_equal(Ys, Yq, "Y sequential vs workqueue")
+    rows = np.unique(np.concatenate([I.sample_rows(M, 12, 96), [16382, 16383, 16384, 16385, 19999]]))
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act, rows=rows)
+    assert_matches_oracle(Yp[torch.as_tensor(rows, device="cuda")], ref, "rows around the group boundary")
+    zref = O.intermediate(I.bits(d["X"]), I.bits(d["W1"]), M, H, F, act, rows=rows)
+    assert_matches_oracle(Zp[torch.as_tensor(rows, device="cuda")], zref, "Z rows around the group boundary")
     plan.close()
