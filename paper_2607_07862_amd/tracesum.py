@@ -49,8 +49,12 @@ def _records(buf, G):
 
 
 def _dependencies(info, F):
-    """GEMM2 item -> GEMM1 tiles whose Z columns it reads (closed form of the plan)."""
-    Mb, S2, bn1 = info["row_blocks"], info["splitk2"], info["bn1"]
+    """GEMM2 item -> GEMM1 tiles whose Z columns it reads (closed form of the plan).
+
+    A plan run in row groups records the launches of a whole group, whose
+    row blocks are the group's."""
+    Mb = info["row_group"] // info["bm"] if info.get("row_group") else info["row_blocks"]
+    S2, bn1 = info["splitk2"], info["bn1"]
     per = -(-F // S2)              # ceil(F / S2), as the plan splits K ...
     kc2 = -(-per // 64) * 64       # ... rounded up to whole 64-deep stages
     deps = {}

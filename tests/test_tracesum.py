@@ -48,3 +48,11 @@ def test_clock_by_eighth_is_cycles_over_real_time():
     c = T.clock_by_eighth(recs, 0)
     assert [round(v) for v in c[1:4]] == [1900] * 3
     assert [round(v) for v in c[5:]] == [1400] * 3
+
+
+def test_dependencies_of_a_grouped_plan_use_the_groups_row_blocks():
+    # one launch: 4 row blocks; grouped: the records are a 2-row-block group's
+    base = {"row_blocks": 4, "bm": 128, "splitk2": 1, "bn1": 128, "items2": 2, "row_group": 0}
+    assert T._dependencies(base, 256) == {0: [0, 4], 1: [1, 5]}
+    grouped = dict(base, row_group=256)
+    assert T._dependencies(grouped, 256) == {0: [0, 2], 1: [1, 3]}
