@@ -100,6 +100,35 @@ def mlp2(X_bits, W1_bits, W2_bits, M: int, H: int, F: int, act: int, rows=None) 
     return Z @ W2
 
 
+def chain(X_bits, W_bits: list, M: int, dims: list, act: int, rows=None) -> np.ndarray:
+    """An L-layer GEMM chain in fp64: Z_0 = X, Z_l = act(Z_{l-1} @ W_l) for
+    l < L and Y = Z_{L-1} @ W_L (rows: optional subset of output rows).
+
+    The paper's pipelining carries over to a chain of GEMMs whose middle
+    kernels both consume the previous output and produce the next (Sec.
+    III-A, the producer/consumer relation applied at every boundary); as for
+    two layers it changes only when a tile runs, so the result is the plain
+    product, with the activation after every layer but the last (identity or
+    GELU, tanh form).  dims = [D_0, ..., D_L]: X is [M, D_0], W_l is
+    [D_{l-1}, D_l] (bf16 bit patterns); the intermediates stay fp64.
+    """
+    L = len(W_bits)
+    if L < 1 or len(dims) != L + 1 or act not in (ACT_IDENTITY, ACT_GELU_TANH):
+        raise ValueError("chain: need L >= 1 weights, L + 1 widths and an identity or GELU activation")
+    if np.asarray(X_bits).size != M * dims[0]:
+        raise ValueError("chain: X size does not match M x D_0")
+    Z = bf16_bits_to_f64(X_bits).reshape(M, dims[0])
+    if rows is not None:
+        Z = Z[np.asarray(rows, dtype=np.int64)]
+    for l, Wb in enumerate(W_bits):
+        if np.asarray(Wb).size != dims[l] * dims[l + 1]:
+            raise ValueError(f"chain: W_{l + 1} size does not match D_{l} x D_{l + 1}")
+        Z = Z @ bf16_bits_to_f64(Wb).reshape(dims[l], dims[l + 1])
+        if l < L - 1 and act == ACT_GELU_TANH:
+            Z = gelu_tanh(Z)
+    return Z
+
+
 def tolerance_bound(Y_ref: np.ndarray) -> float:
     """The elementwise acceptance bound REL_OF_MAX * max|Y_ref| + ABS_FLOOR."""
     m = float(np.max(np.abs(Y_ref))) if Y_ref.size else 0.0
