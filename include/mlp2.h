@@ -223,6 +223,46 @@ int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
  * or MLP2_ERR_UNSUPPORTED. */
 int mlp2_trace_attach(mlp2_plan_t plan, void* buffer, int records_per_group);
 
+/* ---- GEMM chain: the producer / consumer relation at every layer boundary
+ * (Sec. III-A applied to a chain of GEMMs whose middle kernels both consume
+ * and produce).  Z_0 = X [M, D_0]; Z_l = act(Z_{l-1} . W_l) for l < L;
+ * Y = Z_{L-1} . W_L [M, D_L].  W_l is [D_{l-1}, D_l] row-major bf16; fp32
+ * accumulation; the intermediates are stored as bf16 in the plan's
+ * workspace.  Items are 128 x 128 output tiles over their whole K. */
+typedef struct mlp2_chain_s* mlp2_chain_t; /* opaque; created by mlp2_chain_plan, freed by mlp2_chain_destroy */
+
+/* Plan an L-layer chain on the current device.  dims holds L + 1 widths
+ * D_0 .. D_L (host array, read during the call), each a multiple of 128 in
+ * [128, 65536]; 1 <= L <= 8; 1 <= M <= 1<<20; act is MLP2_ACT_IDENTITY or
+ * MLP2_ACT_GELU_TANH (applied after every layer but the last); dtype
+ * MLP2_DTYPE_BF16.  Allocates the intermediates, ready counters and rank
+ * tables.  NULL on failure (mlp2_last_error: MLP2_ERR_INVALID_ARG for null or
+ * non-positive arguments and other activations, MLP2_ERR_UNSUPPORTED for
+ * sizes outside the ranges, MLP2_ERR_DEVICE, MLP2_ERR_HIP). */
+mlp2_chain_t mlp2_chain_plan(int64_t M, int layers, const int64_t* dims, int act, int dtype);
+
+/* Enqueue one evaluation on `stream` (a hipStream_t; NULL = the default
+ * stream).  X, Y: device pointers ([M, D_0] and [M, D_L], 16-byte aligned; Y
+ * must not overlap X or a weight); W: host array of L device pointers to the
+ * weights (read during the call).  MLP2_MODE_SEQUENTIAL launches each
+ * layer's items after the previous layer's launch; MLP2_MODE_TILE_PIPELINED
+ * runs every layer in one persistent launch, each tile starting once the
+ * tiles of the layer below that it reads have signalled.  Both modes give
+ * the same bits.  Asynchronous; no allocation; runs of one plan on one
+ * stream are ordered.  Returns MLP2_OK or MLP2_ERR_INVALID_ARG (also for
+ * MLP2_MODE_WORKQUEUE), MLP2_ERR_ALIGNMENT, MLP2_ERR_DEVICE, MLP2_ERR_HIP. */
+int mlp2_chain_run(mlp2_chain_t plan, const void* X, const void* const* W, void* Y, void* stream, int mode);
+
+/* As mlp2_check, for a chain plan (after the caller has synchronised). */
+int mlp2_chain_check(mlp2_chain_t plan);
+
+/* Polls before a flag wait of a later run gives up (tests of the failure
+ * path); MLP2_ERR_INVALID_ARG outside 1 .. 2^32 - 1. */
+int mlp2_chain_set_spin_limit(mlp2_chain_t plan, int64_t polls);
+
+/* Free the chain plan and its workspace (synchronises the device first).  NULL-safe. */
+void mlp2_chain_destroy(mlp2_chain_t plan);
+
 #ifdef __cplusplus
 }
 #endif

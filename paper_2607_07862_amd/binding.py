@@ -36,6 +36,11 @@ EXPORTS = (
     "mlp2_intermediate",
     "mlp2_set_option",
     "mlp2_trace_attach",
+    "mlp2_chain_plan",
+    "mlp2_chain_run",
+    "mlp2_chain_check",
+    "mlp2_chain_set_spin_limit",
+    "mlp2_chain_destroy",
 )
 
 
@@ -131,6 +136,16 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.mlp2_set_option.argtypes = [P, ctypes.c_int, ctypes.c_int64]
     lib.mlp2_trace_attach.restype = ctypes.c_int
     lib.mlp2_trace_attach.argtypes = [P, P, ctypes.c_int]
+    lib.mlp2_chain_plan.restype = P
+    lib.mlp2_chain_plan.argtypes = [ctypes.c_int64, ctypes.c_int, ctypes.POINTER(ctypes.c_int64), ctypes.c_int, ctypes.c_int]
+    lib.mlp2_chain_run.restype = ctypes.c_int
+    lib.mlp2_chain_run.argtypes = [P, P, ctypes.POINTER(P), P, P, ctypes.c_int]
+    lib.mlp2_chain_check.restype = ctypes.c_int
+    lib.mlp2_chain_check.argtypes = [P]
+    lib.mlp2_chain_set_spin_limit.restype = ctypes.c_int
+    lib.mlp2_chain_set_spin_limit.argtypes = [P, ctypes.c_int64]
+    lib.mlp2_chain_destroy.restype = None
+    lib.mlp2_chain_destroy.argtypes = [P]
     _lib = lib
     return lib
 
@@ -256,3 +271,58 @@ def _hip_memcpy_d2d(dst: int, src: int, nbytes: int) -> None:
     rc = _hip.hipMemcpy(dst, src, nbytes, 3)  # hipMemcpyDeviceToDevice
     if rc != 0:
         raise RuntimeError(f"hipMemcpy failed ({rc})")
+
+
+class ChainPlan:
+    """A plan for the GEMM chain ``Z_l = act(Z_{l-1} @ W_l)``, ``Y = Z_{L-1} @ W_L`` (dims = [D_0, ..., D_L])."""
+
+    def __init__(self, M: int, dims, act: int):
+        import torch
+
+        self.lib = load()
+        self.M, self.dims, self.act = int(M), [int(d) for d in dims], int(act)
+        self.L = len(self.dims) - 1
+        self.device = torch.device("cuda", torch.cuda.current_device())
+        arr = (ctypes.c_int64 * len(self.dims))(*self.dims)
+        h = self.lib.mlp2_chain_plan(self.M, self.L, arr, self.act, DTYPE_BF16)
+        if not h:
+            raise Mlp2Error(self.lib.mlp2_last_error(), "mlp2_chain_plan")
+        self.handle = ctypes.c_void_p(h)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.mlp2_chain_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):  # pragma: no cover - best effort
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def run(self, X, Ws, Y, mode, stream=None) -> None:
+        """Enqueue one evaluation on ``stream`` (default: torch's current stream)."""
+        import torch
+
+        if len(Ws) != self.L:
+            raise ValueError(f"expected {self.L} weights")
+        _check_tensor(X, "X", self.M * self.dims[0], self.device)
+        for l, W in enumerate(Ws):
+            _check_tensor(W, f"W{l + 1}", self.dims[l] * self.dims[l + 1], self.device)
+        _check_tensor(Y, "Y", self.M * self.dims[-1], self.device)
+        mode = MODES.get(mode, mode)
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device)
+        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        ptrs = (ctypes.c_void_p * self.L)(*[_ptr(W) for W in Ws])
+        rc = self.lib.mlp2_chain_run(self.handle, _ptr(X), ptrs, _ptr(Y), sp, int(mode))
+        if rc != OK:
+            raise Mlp2Error(rc, "mlp2_chain_run")
+
+    def check(self) -> int:
+        return self.lib.mlp2_chain_check(self.handle)
+
+    def set_spin_limit(self, polls: int) -> None:
+        rc = self.lib.mlp2_chain_set_spin_limit(self.handle, int(polls))
+        if rc != OK:
+            raise Mlp2Error(rc, "mlp2_chain_set_spin_limit")

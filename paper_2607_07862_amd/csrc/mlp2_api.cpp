@@ -63,6 +63,29 @@ struct mlp2_plan_s {
   bool z_external = false;  // a group's plan: Z belongs to the grouped plan
 };
 
+struct mlp2_chain_s {
+  int64_t M = 0;
+  int L = 0;
+  int64_t dims[mlp2::kChainMaxLayers + 1] = {};
+  int act = 0;
+  int device = -1;
+  int num_cus = 0;
+  int Mb = 0;
+  int items[mlp2::kChainMaxLayers] = {};  // tiles per layer: Mb * D_l / 128
+  int total = 0;
+  int grid = 0;
+  uint32_t spin_limit = 1u << 20;
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  uint16_t* Z[mlp2::kChainMaxLayers] = {};        // output of layer l < L - 1, [Mb * 128, D_{l+1}]
+  uint32_t* ready[mlp2::kChainMaxLayers] = {};    // ready counters of layer l < L - 1
+  uint32_t* ctrl = nullptr;
+  uint32_t* order_seq = nullptr;  // layer l's tiles at offset seq_off[l], column blocks first
+  uint32_t* order_pipe = nullptr; // every item of every layer, after its producers
+  int seq_off[mlp2::kChainMaxLayers] = {};
+  size_t counters_off = 0, counters_bytes = 0;
+};
+
 namespace {
 
 thread_local int g_last_error = MLP2_OK;
@@ -808,6 +831,218 @@ int mlp2_trace_attach(mlp2_plan_t p, void* buffer, int records_per_group) {
   p->trace = (uint64_t*)buffer;
   p->trace_cap = buffer ? records_per_group : 0;
   return MLP2_OK;
+}
+
+
+}  // extern "C"
+
+namespace {
+
+// Rank table of the chain's one-launch mode.  Layer 0's tiles come column
+// blocks first; each later layer is merged in layer by layer: the item of
+// tile (mb, nb) goes right after rank h + lag of the table built so far,
+// where h is the highest rank among the tiles of the layer below in row
+// block mb (it reads all of them), and items of equal key keep their column
+// order.  Every item therefore ranks above all of its producers.
+std::vector<uint32_t> chain_rank_table(const mlp2_chain_s* p, int lag) {
+  std::vector<uint32_t> list;
+  for (int t = 0; t < p->items[0]; ++t) list.push_back((uint32_t)t);
+  for (int l = 1; l < p->L; ++l) {
+    std::vector<int64_t> row_last((size_t)p->Mb, -1);  // highest rank of layer l - 1 per row block
+    for (size_t r = 0; r < list.size(); ++r)
+      if ((int)(list[r] >> 24) == l - 1) {
+        const int mb = (int)(list[r] & 0xffffffu) % p->Mb;
+        row_last[(size_t)mb] = std::max<int64_t>(row_last[(size_t)mb], (int64_t)r);
+      }
+    std::vector<std::pair<int64_t, uint32_t>> add;
+    for (int t = 0; t < p->items[l]; ++t) {
+      const int64_t key = std::min<int64_t>(row_last[(size_t)(t % p->Mb)] + lag, (int64_t)list.size() - 1);
+      add.push_back({key, ((uint32_t)l << 24) | (uint32_t)t});
+    }
+    std::stable_sort(add.begin(), add.end(), [](const std::pair<int64_t, uint32_t>& x, const std::pair<int64_t, uint32_t>& y) {
+      return x.first < y.first;
+    });
+    std::vector<uint32_t> merged;
+    merged.reserve(list.size() + add.size());
+    size_t k = 0;
+    for (size_t r = 0; r < list.size(); ++r) {
+      merged.push_back(list[r]);
+      while (k < add.size() && add[k].first == (int64_t)r) merged.push_back(add[k++].second);
+    }
+    list.swap(merged);
+  }
+  return list;
+}
+
+}  // namespace
+
+extern "C" {
+
+mlp2_chain_t mlp2_chain_plan(int64_t M, int layers, const int64_t* dims, int act, int dtype) {
+  g_last_error = MLP2_OK;
+  if (M < 1 || layers < 1 || !dims || (act != MLP2_ACT_IDENTITY && act != MLP2_ACT_GELU_TANH) || dtype != MLP2_DTYPE_BF16) {
+    fail(MLP2_ERR_INVALID_ARG);
+    return nullptr;
+  }
+  if (layers > mlp2::kChainMaxLayers || M > (1 << 20)) { fail(MLP2_ERR_UNSUPPORTED); return nullptr; }
+  for (int l = 0; l <= layers; ++l)
+    if (dims[l] < mlp2::kChainTile || dims[l] % mlp2::kChainTile || dims[l] > (1 << 16)) {
+      fail(dims[l] < 1 ? MLP2_ERR_INVALID_ARG : MLP2_ERR_UNSUPPORTED);
+      return nullptr;
+    }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || !is_gfx950(dev)) { fail(MLP2_ERR_DEVICE); return nullptr; }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) { fail(MLP2_ERR_HIP); return nullptr; }
+  int occ = 0;
+  if (mlp2::chain_occupancy(&occ) != hipSuccess || occ < 1) { fail(MLP2_ERR_HIP); return nullptr; }
+
+  auto* p = new mlp2_chain_s();
+  p->M = M; p->L = layers; p->act = act; p->device = dev; p->num_cus = prop.multiProcessorCount;
+  for (int l = 0; l <= layers; ++l) p->dims[l] = dims[l];
+  p->Mb = ceil_div(M, mlp2::kChainTile);
+  for (int l = 0; l < layers; ++l) {
+    p->items[l] = (int)(p->Mb * (dims[l + 1] / mlp2::kChainTile));
+    p->seq_off[l] = p->total;
+    p->total += p->items[l];
+  }
+  if (p->Mb > (1 << 16) || p->total >= (1 << 24)) { delete p; fail(MLP2_ERR_UNSUPPORTED); return nullptr; }
+  p->grid = std::min(occ * p->num_cus, p->total);
+
+  // workspace: intermediates, then ready counters and control words (zeroed), then rank tables
+  const int64_t Mpad = (int64_t)p->Mb * mlp2::kChainTile;
+  const size_t line = mlp2::kLine * 4;
+  size_t off = 0, z_off[mlp2::kChainMaxLayers] = {}, r_off[mlp2::kChainMaxLayers] = {};
+  for (int l = 0; l + 1 < layers; ++l) {
+    z_off[l] = off;
+    off = align_up(off + (size_t)Mpad * dims[l + 1] * 2, 256);
+  }
+  const size_t cnt_off = off;
+  for (int l = 0; l + 1 < layers; ++l) {
+    r_off[l] = off;
+    off = align_up(off + (size_t)p->items[l] * line, 256);
+  }
+  const size_t ctrl_off = off;
+  off = align_up(off + mlp2::CTRL_WORDS * 4, 256);
+  const size_t cnt_end = off;
+  const size_t seq_off = off;
+  off = align_up(off + (size_t)p->total * 4, 256);
+  const size_t pipe_off = off;
+  off = align_up(off + (size_t)p->total * 4, 256);
+  p->ws_bytes = off;
+  if (hipMalloc(&p->ws, p->ws_bytes) != hipSuccess) { delete p; fail(MLP2_ERR_HIP); return nullptr; }
+  char* b = (char*)p->ws;
+  for (int l = 0; l + 1 < layers; ++l) {
+    p->Z[l] = (uint16_t*)(b + z_off[l]);
+    p->ready[l] = (uint32_t*)(b + r_off[l]);
+  }
+  p->ctrl = (uint32_t*)(b + ctrl_off);
+  p->order_seq = (uint32_t*)(b + seq_off);
+  p->order_pipe = (uint32_t*)(b + pipe_off);
+  p->counters_off = cnt_off;
+  p->counters_bytes = cnt_end - cnt_off;
+  std::vector<uint32_t> seq;
+  for (int l = 0; l < layers; ++l)
+    for (int t = 0; t < p->items[l]; ++t) seq.push_back(((uint32_t)l << 24) | (uint32_t)t);
+  const std::vector<uint32_t> pipe = chain_rank_table(p, p->grid);
+  if (hipMemset(b, 0, cnt_end) != hipSuccess ||
+      hipMemcpy(p->order_seq, seq.data(), seq.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(p->order_pipe, pipe.data(), pipe.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
+      hipDeviceSynchronize() != hipSuccess) {
+    (void)hipFree(p->ws);
+    delete p;
+    fail(MLP2_ERR_HIP);
+    return nullptr;
+  }
+  return p;
+}
+
+int mlp2_chain_run(mlp2_chain_t p, const void* X, const void* const* W, void* Y, void* stream, int mode) {
+  if (!p || !X || !W || !Y) return fail(MLP2_ERR_INVALID_ARG);
+  if (mode != MLP2_MODE_SEQUENTIAL && mode != MLP2_MODE_TILE_PIPELINED) return fail(MLP2_ERR_INVALID_ARG);
+  uintptr_t bits = (uintptr_t)X | (uintptr_t)Y;
+  for (int l = 0; l < p->L; ++l) {
+    if (!W[l]) return fail(MLP2_ERR_INVALID_ARG);
+    bits |= (uintptr_t)W[l];
+  }
+  if (bits & 15u) return fail(MLP2_ERR_ALIGNMENT);
+  const size_t yb = (size_t)p->M * p->dims[p->L] * 2;
+  if (overlaps(Y, yb, X, (size_t)p->M * p->dims[0] * 2)) return fail(MLP2_ERR_INVALID_ARG);
+  for (int l = 0; l < p->L; ++l)
+    if (overlaps(Y, yb, W[l], (size_t)p->dims[l] * p->dims[l + 1] * 2)) return fail(MLP2_ERR_INVALID_ARG);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != p->device) return fail(MLP2_ERR_DEVICE);
+
+  mlp2::ChainArgs c;
+  std::memset(&c, 0, sizeof(c));
+  Args& a = c.a;
+  a.ctrl = p->ctrl;
+  a.M = (int)p->M;
+  a.Mb = p->Mb;
+  a.spin_limit = p->spin_limit;
+  a.drop_signal = -1;
+  a.first_static = 0;
+  const int64_t Mpad = (int64_t)p->Mb * mlp2::kChainTile;
+  for (int l = 0; l < p->L; ++l) {
+    mlp2::ChainLayer& L = c.layer[l];
+    L.A = l == 0 ? (const uint16_t*)X : p->Z[l - 1];
+    L.W = (const uint16_t*)W[l];
+    L.out = l == p->L - 1 ? (uint16_t*)Y : p->Z[l];
+    L.ready_in = l == 0 ? nullptr : p->ready[l - 1];
+    L.ready_out = l == p->L - 1 ? nullptr : p->ready[l];
+    L.K = (int)p->dims[l];
+    L.N = (int)p->dims[l + 1];
+    L.alast = l == 0 ? (int)p->M - 1 : (int)Mpad - 1;
+    L.act = l == p->L - 1 ? MLP2_ACT_IDENTITY : p->act;
+    L.guard = l == p->L - 1;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (mode == MLP2_MODE_TILE_PIPELINED) {
+    a.orderp = p->order_pipe;
+    a.items1 = p->total;
+    a.lists = claim_lists(p->grid);
+    c.wait = 1;
+    c.end_of_run = 1;
+    if (mlp2::launch_chain(c, p->grid, s) != hipSuccess) return fail(MLP2_ERR_HIP);
+    return MLP2_OK;
+  }
+  for (int l = 0; l < p->L; ++l) {  // one launch per layer, in order: the stream orders the layers
+    const int grid = std::min(p->grid, p->items[l]);
+    a.orderp = p->order_seq + p->seq_off[l];
+    a.items1 = p->items[l];
+    a.lists = claim_lists(grid);
+    c.wait = 0;
+    c.end_of_run = l == p->L - 1;
+    if (mlp2::launch_chain(c, grid, s) != hipSuccess) return fail(MLP2_ERR_HIP);
+  }
+  return MLP2_OK;
+}
+
+int mlp2_chain_check(mlp2_chain_t p) {
+  if (!p) return fail(MLP2_ERR_INVALID_ARG);
+  uint32_t ctrl[mlp2::CTRL_WORDS];
+  if (hipMemcpy(ctrl, p->ctrl, sizeof(ctrl), hipMemcpyDeviceToHost) != hipSuccess) return fail(MLP2_ERR_HIP);
+  if (ctrl[mlp2::CTRL_ERROR] == 0) return MLP2_OK;
+  if (hipMemset((char*)p->ws + p->counters_off, 0, p->counters_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+    return fail(MLP2_ERR_HIP);
+  return fail(MLP2_ERR_TIMEOUT);
+}
+
+int mlp2_chain_set_spin_limit(mlp2_chain_t p, int64_t polls) {
+  if (!p || polls < 1 || polls > 0xFFFFFFFFLL) return fail(MLP2_ERR_INVALID_ARG);
+  p->spin_limit = (uint32_t)polls;
+  return MLP2_OK;
+}
+
+void mlp2_chain_destroy(mlp2_chain_t p) {
+  if (!p) return;
+  int cur = -1;
+  (void)hipGetDevice(&cur);
+  if (cur != p->device) (void)hipSetDevice(p->device);
+  (void)hipDeviceSynchronize();
+  (void)hipFree(p->ws);
+  if (cur != p->device && cur >= 0) (void)hipSetDevice(cur);
+  delete p;
 }
 
 }  // extern "C"

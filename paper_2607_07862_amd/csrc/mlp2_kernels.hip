@@ -442,6 +442,97 @@ static const Entry* find_entry(const KernelConfig& c) {
   return nullptr;
 }
 
+// ------------------------------------------------------------------ GEMM chain
+//
+// An L-layer chain Z_l = act(Z_{l-1} W_l), Y = Z_{L-1} W_L: the producer /
+// consumer relation of the two-layer kernel at every layer boundary (Sec.
+// III-A).  An item is a 128 x 128 output tile of one layer over its whole K.
+// A middle layer's item consumes like a GEMM2 item (it waits per K-slice on
+// the ready counters of the layer below, row block mb) and produces like a
+// GEMM1 item (activation, its Z rows stored, then its own ready counter
+// released).  The one-launch rank table places every item after all the
+// items it reads (plus a lag of about one grid), so the deadlock argument of
+// the two-layer kernels holds unchanged: an item waits only for lower ranks,
+// and a work-group takes its next ticket only after its current item's last
+// wait.  The sequential mode launches each layer's items on their own, in
+// layer order, without waits; both modes run this item function.
+using ChainT = TileFor<kChainTile, kChainTile, 2>::type;
+
+__device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int tile, uint32_t epoch, char* lds,
+                                           int* s_slot, Claim& next, int* s_next, TraceAcc& tr) {
+  using T = ChainT;
+  const Args& a = c.a;
+  const ChainLayer& L = c.layer[layer];
+  const int mb = tile % a.Mb, nb = tile / a.Mb;
+  const int m0 = mb * T::BM, n0 = nb * T::BN;
+  const int K = L.K;
+  f32x4 acc[1][T::TN][T::TM];
+  const uint16_t* Bp[1] = {L.W};
+  if (c.wait && L.ready_in) {
+    ReadyWait w{L.ready_in, a.ctrl + CTRL_ERROR, mb, a.Mb, T::BN, (K - 1) / T::BN, epoch + 1u, a.spin_limit, s_slot,
+                0, &tr};
+    ClaimAtLastStage<ReadyWait> hook{w, &next, K - kBK};
+    mainloop<T, 1>(L.A, K, m0, L.alast, Bp, L.N, n0, 0, K, acc, lds, hook, tr);
+  } else {
+    NoWait nowait;
+    ClaimAtLastStage<NoWait> hook{nowait, &next, K - kBK};
+    mainloop<T, 1>(L.A, K, m0, L.alast, Bp, L.N, n0, 0, K, acc, lds, hook, tr);
+  }
+  next.park(s_next);
+  FragPos<T> fp(m0, n0);
+#pragma unroll
+  for (int tm = 0; tm < T::TM; ++tm)
+#pragma unroll
+    for (int tp = 0; tp < T::TN / 2; ++tp) {
+      float v[8];
+      pair_values<T>(acc[0], tp, tm, v);
+      if (L.act == ACT_GELU_TANH) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = gelu_tanh(v[i]);
+      }
+      const int row = fp.row0 + 16 * tm, col = fp.col0 + 32 * tp;
+      if (!L.guard || row < a.M) *reinterpret_cast<u32x4*>(L.out + (long)row * L.N + col) = pack_bf16x8(v);
+    }
+  // Producer signal (one per tile and run): this tile's output rows are released.
+  if (L.ready_out) signal_ready(L.ready_out + (long)tile * kLine);
+}
+
+__global__ __launch_bounds__(kThreads, 2) void k_mlp2_chain(ChainArgs c) {
+  __shared__ __attribute__((aligned(1024))) char lds[ChainT::template lds_bytes<1>()];
+  __shared__ int s_item, s_slot;
+  const Args& a = c.a;
+  const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
+  const int total = a.items1;
+  int p;
+  {
+    Claim first = make_claim(a);
+    first.issue();
+    first.park(&s_item);
+    __syncthreads();
+    p = uniform(s_item);
+  }
+  for (;;) {
+    if (p >= total) break;
+    __syncthreads();  // every wave has read s_item before the item's claim rewrites it
+    TraceAcc tr;
+    Claim next = make_claim(a);
+    const uint32_t e = uniform(a.orderp[p]);
+    chain_item(c, (int)(e >> 24), (int)(e & 0xffffffu), epoch, lds, &s_slot, next, &s_item, tr);
+    __syncthreads();
+    p = uniform(s_item);
+  }
+  finish_kernel(a, epoch, c.end_of_run != 0);
+}
+
+hipError_t chain_occupancy(int* blocks_per_cu) {
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, (const void*)&k_mlp2_chain, kThreads, 0);
+}
+
+hipError_t launch_chain(const ChainArgs& c, int grid, hipStream_t stream) {
+  void* args[] = {const_cast<ChainArgs*>(&c)};
+  return hipLaunchKernel((const void*)&k_mlp2_chain, dim3(grid), dim3(kThreads), args, 0, stream);
+}
+
 bool config_supported(const KernelConfig& c) { return find_entry(c) != nullptr; }
 
 hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu) {

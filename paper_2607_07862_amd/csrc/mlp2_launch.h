@@ -22,4 +22,34 @@ hipError_t launch_sequential(const KernelConfig& c, const Args& a1, const Args& 
 hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
 hipError_t launch_workqueue(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
 
+// ---- GEMM chain: Z_l = act(Z_{l-1} W_l), Y = Z_{L-1} W_L, 128 x 128 tiles, no split-K.
+constexpr int kChainMaxLayers = 8;
+constexpr int kChainTile = 128;
+
+// One layer of a chain launch (passed by value with every launch).
+struct ChainLayer {
+  const uint16_t* A;         // input rows, row stride K: X or the previous layer's Z
+  const uint16_t* W;         // [K, N]
+  uint16_t* out;             // this layer's Z [Mpad, N], or Y [M, N] for the last layer
+  const uint32_t* ready_in;  // the producing layer's ready counters (null: first layer)
+  uint32_t* ready_out;       // this layer's ready counters (null: last layer)
+  int K, N;
+  int alast;                 // last input row a load may touch (rows past it are clamped to it)
+  int act;                   // activation on the output (MLP2_ACT_IDENTITY or MLP2_ACT_GELU_TANH)
+  int guard;                 // store rows < M only (the last layer writes Y)
+};
+
+// Arguments of a chain launch.  `a` carries the control words, claim lists,
+// spin limit, M, Mb and the rank table (orderp, a.items1 ranks; entry =
+// layer << 24 | tile with tile = nb * Mb + mb).
+struct ChainArgs {
+  Args a;
+  ChainLayer layer[kChainMaxLayers];
+  int wait;        // items wait on their producing layer's ready counters (one launch for all layers)
+  int end_of_run;  // the run's last launch: it advances the epoch
+};
+
+hipError_t chain_occupancy(int* blocks_per_cu);
+hipError_t launch_chain(const ChainArgs& c, int grid, hipStream_t stream);
+
 }  // namespace mlp2

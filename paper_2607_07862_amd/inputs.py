@@ -106,6 +106,16 @@ def make_inputs(M: int, H: int, F: int, act: int, seed: int) -> dict:
     return {"X": X, "W1": W1, "W2": W2}
 
 
+def chain_inputs(M: int, dims, seed: int) -> dict:
+    """CPU bf16 tensors of a GEMM chain: ``X [M, D_0]`` ~ N(0, 1) and ``Ws``, one
+    ``[D_{l-1}, D_l]`` per layer ~ N(0, 1/D_{l-1}) (the fan-in scaling of the workloads)."""
+    gen = torch.Generator(device="cpu")
+    gen.manual_seed(int(seed))
+    X = _randn_bf16(gen, (M, dims[0]), 1.0)
+    Ws = [_randn_bf16(gen, (dims[l], dims[l + 1]), float(1.0 / np.sqrt(dims[l]))) for l in range(len(dims) - 1)]
+    return {"X": X, "Ws": Ws}
+
+
 def workload_inputs(w: Workload) -> dict:
     return make_inputs(w.M, w.H, w.F, w.act, w.seed)
 
