@@ -101,6 +101,71 @@ def device_random_inputs(w):
     return {"X": X, "W1": W1, "W2": W2}
 
 
+CHAIN_LAYERS, CHAIN_WIDTH, CHAIN_ROWS = 4, 8192, (1024, 4096, 16384)
+
+
+def chain_row(B, M: int, steps: int, iters: int) -> dict:
+    """The GEMM chain of CHAIN_LAYERS layers of CHAIN_WIDTH x CHAIN_WIDTH weights
+    (GELU between layers) on M rows: both modes (blocks of `steps` runs, and
+    `iters` runs per mode timed one by one in alternating order) and eager
+    PyTorch (hipBLASLt GEMMs and a GELU kernel per layer) on the same inputs."""
+    import torch
+    import torch.nn.functional as Fn
+
+    dims = [CHAIN_WIDTH] * (CHAIN_LAYERS + 1)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2000 + M)
+    X = torch.randn(M, dims[0], device="cuda", generator=gen).to(torch.bfloat16)
+    Ws = [(torch.randn(dims[l], dims[l + 1], device="cuda", generator=gen) * dims[l] ** -0.5).to(torch.bfloat16)
+          for l in range(CHAIN_LAYERS)]
+    Y = torch.empty(M, dims[-1], dtype=torch.bfloat16, device="cuda")
+    plan = B.ChainPlan(M, dims, B.ACT_GELU_TANH)
+    modes = (B.MODE_TILE_PIPELINED, B.MODE_SEQUENTIAL)
+    for _ in range(5):
+        for m in modes:
+            plan.run(X, Ws, Y, m)
+    torch.cuda.synchronize()
+
+    def timed(fn, n):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(n):
+            fn()
+        e.record()
+        e.synchronize()
+        return s.elapsed_time(e) * 1000 / n
+
+    blocks = {m: timed(lambda m=m: plan.run(X, Ws, Y, m), steps) for m in modes}
+    one = {m: [] for m in modes}
+    for _ in range(iters):
+        for m in modes:
+            one[m].append(timed(lambda m=m: plan.run(X, Ws, Y, m), 1))
+    assert plan.check() == B.OK
+    plan.close()
+
+    def eager():
+        Z = X
+        for l, W in enumerate(Ws):
+            Z = Z @ W
+            if l < CHAIN_LAYERS - 1:
+                Z = Fn.gelu(Z, approximate="tanh")
+        return Z
+
+    eager()
+    te = timed(eager, steps)
+    flops = 2.0 * M * sum(dims[l] * dims[l + 1] for l in range(CHAIN_LAYERS))
+    p_us, s_us = blocks[modes[0]], blocks[modes[1]]
+    mp, ms = statistics.median(one[modes[0]]), statistics.median(one[modes[1]])
+    return {
+        "M": M, "layers": CHAIN_LAYERS, "width": CHAIN_WIDTH,
+        "pipelined_us": round(p_us, 2), "sequential_us": round(s_us, 2), "gain_pct": round((s_us - p_us) / s_us * 100, 1),
+        "interleaved_median_us": {"pipelined": round(mp, 2), "sequential": round(ms, 2),
+                                  "gain_pct": round((ms - mp) / ms * 100, 1)},
+        "torch_eager_us": round(te, 2),
+        "mfma_frac": round(flops / (p_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
+    }
+
+
 def torch_eager_us(w, g, steps):
     """Mean µs per step of the same MLP in eager PyTorch on the platform
     libraries (hipBLASLt GEMMs plus an elementwise activation kernel), bf16
@@ -310,6 +375,10 @@ def main():
     ap.add_argument("--interleave-iters", type=int, default=100,
                     help="warm runs per mode timed one by one in alternating order (0 skips; a third of it per table row)")
     ap.add_argument("--no-attainable", action="store_true", help="skip the stream and library-GEMM references")
+    ap.add_argument("--chain", action="store_true",
+                    help="also time the GEMM chain: 4 layers of 8192 x 8192 weights, GELU between")
+    ap.add_argument("--chain-rows", default=",".join(str(m) for m in CHAIN_ROWS),
+                    help="row counts of the chain leg (comma-separated)")
     ap.add_argument("--paper-shapes", action="store_true",
                     help="also time the paper's own workload: 8192x8192 weights, no activation, M = 1024 ... 32768")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
@@ -464,6 +533,14 @@ def main():
             table[key] = row
             log(f"TABLE {key:12s} {row}")
 
+    chain = {}
+    if args.chain:
+        for Mc in [int(x) for x in args.chain_rows.split(",")]:
+            row = chain_row(B, Mc, max(5, args.steps // 5), 10)
+            chain[f"chain{CHAIN_LAYERS}x{CHAIN_WIDTH}_m{Mc}"] = row
+            log(f"CHAIN m{Mc:<6d} {row}")
+            torch.cuda.empty_cache()
+
     paper = {}
     if args.paper_shapes:
         for key in I.PAPER_ORDER:
@@ -548,6 +625,7 @@ def main():
         "cpu_baseline": cpu,
         "workloads": table,
         **({"paper_shapes": paper} if paper else {}),
+        **({"chain": chain} if chain else {}),
     }
     print(json.dumps(out), flush=True)
 
