@@ -84,6 +84,11 @@ struct mlp2_chain_s {
   uint32_t* order_pipe = nullptr; // every item of every layer, after its producers
   int seq_off[mlp2::kChainMaxLayers] = {};
   size_t counters_off = 0, counters_bytes = 0;
+  // Row groups (chain_group_rows): launches over whole groups of group_rows
+  // rows (`group`) and over the remaining rows (`tail`), in row order.
+  int64_t group_rows = 0;
+  mlp2_chain_s* group = nullptr;
+  mlp2_chain_s* tail = nullptr;
 };
 
 namespace {
@@ -878,22 +883,25 @@ std::vector<uint32_t> chain_rank_table(const mlp2_chain_s* p, int lag) {
 
 extern "C" {
 
-mlp2_chain_t mlp2_chain_plan(int64_t M, int layers, const int64_t* dims, int act, int dtype) {
-  g_last_error = MLP2_OK;
-  if (M < 1 || layers < 1 || !dims || (act != MLP2_ACT_IDENTITY && act != MLP2_ACT_GELU_TANH) || dtype != MLP2_DTYPE_BF16) {
-    fail(MLP2_ERR_INVALID_ARG);
-    return nullptr;
-  }
-  if (layers > mlp2::kChainMaxLayers || M > (1 << 20)) { fail(MLP2_ERR_UNSUPPORTED); return nullptr; }
-  for (int l = 0; l <= layers; ++l)
-    if (dims[l] < mlp2::kChainTile || dims[l] % mlp2::kChainTile || dims[l] > (1 << 16)) {
-      fail(dims[l] < 1 ? MLP2_ERR_INVALID_ARG : MLP2_ERR_UNSUPPORTED);
-      return nullptr;
-    }
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || !is_gfx950(dev)) { fail(MLP2_ERR_DEVICE); return nullptr; }
-  hipDeviceProp_t prop;
-  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) { fail(MLP2_ERR_HIP); return nullptr; }
+}  // extern "C"
+
+namespace {
+
+// Rows per launch group of a chain: 0 runs each mode's launches over all
+// rows.  A launch of more than about 4.4 TFLOP lost its lead (and its
+// clock) in both the two-layer and the chain measurements; the chain runs
+// best in groups of about 1.1 TFLOP per launch (4 layers of 8192 x 8192 at
+// 16384 rows: one launch 10.5 ms pipelined and 9.5 sequential, groups of
+// 4096 rows 8.6 and 8.9, groups of 8192 rows 8.7 and 8.9), so it groups once
+// the rows exceed two such groups.
+int64_t chain_group_rows(int64_t M, int layers, const int64_t* dims) {
+  double macs = 0;
+  for (int l = 0; l < layers; ++l) macs += (double)dims[l] * (double)dims[l + 1];
+  const int64_t rows = (int64_t)(0.55e12 / macs) / 256 * 256;
+  return rows >= 256 && M > 2 * rows ? rows : 0;
+}
+
+mlp2_chain_s* make_chain(int64_t M, int layers, const int64_t* dims, int act, int dev, const hipDeviceProp_t& prop) {
   int occ = 0;
   if (mlp2::chain_occupancy(&occ) != hipSuccess || occ < 1) { fail(MLP2_ERR_HIP); return nullptr; }
 
@@ -957,6 +965,44 @@ mlp2_chain_t mlp2_chain_plan(int64_t M, int layers, const int64_t* dims, int act
   return p;
 }
 
+int launch_chain_plan(const mlp2_chain_s* p, const void* X, const void* const* W, void* Y, hipStream_t s, int mode);
+
+}  // namespace
+
+extern "C" {
+
+mlp2_chain_t mlp2_chain_plan(int64_t M, int layers, const int64_t* dims, int act, int dtype) {
+  g_last_error = MLP2_OK;
+  if (M < 1 || layers < 1 || !dims || (act != MLP2_ACT_IDENTITY && act != MLP2_ACT_GELU_TANH) || dtype != MLP2_DTYPE_BF16) {
+    fail(MLP2_ERR_INVALID_ARG);
+    return nullptr;
+  }
+  if (layers > mlp2::kChainMaxLayers || M > (1 << 20)) { fail(MLP2_ERR_UNSUPPORTED); return nullptr; }
+  for (int l = 0; l <= layers; ++l)
+    if (dims[l] < mlp2::kChainTile || dims[l] % mlp2::kChainTile || dims[l] > (1 << 16)) {
+      fail(dims[l] < 1 ? MLP2_ERR_INVALID_ARG : MLP2_ERR_UNSUPPORTED);
+      return nullptr;
+    }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || !is_gfx950(dev)) { fail(MLP2_ERR_DEVICE); return nullptr; }
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) { fail(MLP2_ERR_HIP); return nullptr; }
+  const int64_t rows = chain_group_rows(M, layers, dims);
+  if (!rows) return make_chain(M, layers, dims, act, dev, prop);
+  auto* p = new mlp2_chain_s();
+  p->M = M; p->L = layers; p->act = act; p->device = dev; p->num_cus = prop.multiProcessorCount;
+  for (int l = 0; l <= layers; ++l) p->dims[l] = dims[l];
+  p->group_rows = rows;
+  if (!(p->group = make_chain(rows, layers, dims, act, dev, prop)) ||
+      (M % rows && !(p->tail = make_chain(M % rows, layers, dims, act, dev, prop)))) {
+    const int code = g_last_error != MLP2_OK ? g_last_error : MLP2_ERR_HIP;
+    mlp2_chain_destroy(p);
+    fail(code);
+    return nullptr;
+  }
+  return p;
+}
+
 int mlp2_chain_run(mlp2_chain_t p, const void* X, const void* const* W, void* Y, void* stream, int mode) {
   if (!p || !X || !W || !Y) return fail(MLP2_ERR_INVALID_ARG);
   if (mode != MLP2_MODE_SEQUENTIAL && mode != MLP2_MODE_TILE_PIPELINED) return fail(MLP2_ERR_INVALID_ARG);
@@ -972,7 +1018,25 @@ int mlp2_chain_run(mlp2_chain_t p, const void* X, const void* const* W, void* Y,
     if (overlaps(Y, yb, W[l], (size_t)p->dims[l] * p->dims[l + 1] * 2)) return fail(MLP2_ERR_INVALID_ARG);
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev != p->device) return fail(MLP2_ERR_DEVICE);
+  hipStream_t s = (hipStream_t)stream;
+  if (!p->group) return launch_chain_plan(p, X, W, Y, s, mode);
+  // Row groups, in order on the stream: each group's launches read its rows of X and write its rows of Y.
+  const int64_t R = p->group_rows, d0 = p->dims[0], dl = p->dims[p->L];
+  int64_t r0 = 0;
+  for (; r0 + R <= p->M; r0 += R) {
+    const int rc = launch_chain_plan(p->group, (const uint16_t*)X + r0 * d0, W, (uint16_t*)Y + r0 * dl, s, mode);
+    if (rc != MLP2_OK) return rc;
+  }
+  if (p->tail) return launch_chain_plan(p->tail, (const uint16_t*)X + r0 * d0, W, (uint16_t*)Y + r0 * dl, s, mode);
+  return MLP2_OK;
+}
 
+}  // extern "C"
+
+namespace {
+
+// One evaluation of a chain plan without row groups.
+int launch_chain_plan(const mlp2_chain_s* p, const void* X, const void* const* W, void* Y, hipStream_t s, int mode) {
   mlp2::ChainArgs c;
   std::memset(&c, 0, sizeof(c));
   Args& a = c.a;
@@ -996,7 +1060,6 @@ int mlp2_chain_run(mlp2_chain_t p, const void* X, const void* const* W, void* Y,
     L.act = l == p->L - 1 ? MLP2_ACT_IDENTITY : p->act;
     L.guard = l == p->L - 1;
   }
-  hipStream_t s = (hipStream_t)stream;
   if (mode == MLP2_MODE_TILE_PIPELINED) {
     a.orderp = p->order_pipe;
     a.items1 = p->total;
@@ -1018,8 +1081,17 @@ int mlp2_chain_run(mlp2_chain_t p, const void* X, const void* const* W, void* Y,
   return MLP2_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
 int mlp2_chain_check(mlp2_chain_t p) {
   if (!p) return fail(MLP2_ERR_INVALID_ARG);
+  if (p->group) {
+    const int a = mlp2_chain_check(p->group);
+    const int b = p->tail ? mlp2_chain_check(p->tail) : MLP2_OK;
+    return a != MLP2_OK ? fail(a) : b != MLP2_OK ? fail(b) : MLP2_OK;
+  }
   uint32_t ctrl[mlp2::CTRL_WORDS];
   if (hipMemcpy(ctrl, p->ctrl, sizeof(ctrl), hipMemcpyDeviceToHost) != hipSuccess) return fail(MLP2_ERR_HIP);
   if (ctrl[mlp2::CTRL_ERROR] == 0) return MLP2_OK;
@@ -1031,11 +1103,15 @@ int mlp2_chain_check(mlp2_chain_t p) {
 int mlp2_chain_set_spin_limit(mlp2_chain_t p, int64_t polls) {
   if (!p || polls < 1 || polls > 0xFFFFFFFFLL) return fail(MLP2_ERR_INVALID_ARG);
   p->spin_limit = (uint32_t)polls;
+  if (p->group) (void)mlp2_chain_set_spin_limit(p->group, polls);
+  if (p->tail) (void)mlp2_chain_set_spin_limit(p->tail, polls);
   return MLP2_OK;
 }
 
 void mlp2_chain_destroy(mlp2_chain_t p) {
   if (!p) return;
+  mlp2_chain_destroy(p->group);
+  mlp2_chain_destroy(p->tail);
   int cur = -1;
   (void)hipGetDevice(&cur);
   if (cur != p->device) (void)hipSetDevice(p->device);

@@ -8,8 +8,9 @@
 * with the flag waits cut to one poll a pipelined run may give up; the plan
   reports it, recovers, and its next runs are exact;
 * a run captured into a graph replays with the eager bits, in both modes;
-* at the paper's shape (four 8192 x 8192 layers, 4096 rows) sampled rows
-  match the oracle and the modes agree bit for bit.
+* at the paper's shape (four 8192 x 8192 layers, 4096 rows in one launch,
+  16684 rows in row groups with a shorter last one) sampled rows match the
+  oracle and the modes agree bit for bit.
 """
 import numpy as np
 import pytest
@@ -150,8 +151,12 @@ def test_argument_errors(lib):
     plan.close()
 
 
-def test_paper_shape_four_layers_sampled_rows(lib):
-    M, dims, act = 4096, [8192] * 5, 1
+@pytest.mark.parametrize("M", [4096, 16684])
+def test_paper_shape_four_layers_sampled_rows(lib, M):
+    """4096 rows run as one launch per mode; 16684 rows in row groups of 4096
+    and a last group of 300 (the sampled rows include both sides of a group
+    boundary and the last row)."""
+    dims, act = [8192] * 5, 1
     print(f"\n[chain] {M} rows, dims {dims}", flush=True)
     d = I.chain_inputs(M, dims, seed=45)
     X, Ws = _device(d)
@@ -161,7 +166,7 @@ def test_paper_shape_four_layers_sampled_rows(lib):
     torch.cuda.synchronize()
     assert plan.check() == B.OK
     assert_bit_equal(Ys, Yp, "chain Y sequential vs pipelined")
-    rows = I.sample_rows(M, 12, 45)
+    rows = np.unique(np.concatenate([I.sample_rows(M, 12, 45), [min(4095, M - 1), min(4096, M - 1), M - 1]]))
     ref = _oracle(d, M, dims, act, rows=rows)
     assert_matches_oracle(Yp[torch.as_tensor(rows, device="cuda")], ref, "sampled rows")
     plan.close()
