@@ -101,7 +101,7 @@ def device_random_inputs(w):
     return {"X": X, "W1": W1, "W2": W2}
 
 
-CHAIN_LAYERS, CHAIN_WIDTH, CHAIN_ROWS = 4, 8192, (1024, 4096, 16384)
+CHAIN_LAYERS, CHAIN_WIDTH, CHAIN_ROWS = 4, 8192, (128, 1024, 4096, 16384)
 
 
 def chain_row(B, M: int, steps: int, iters: int) -> dict:

@@ -228,7 +228,8 @@ int mlp2_trace_attach(mlp2_plan_t plan, void* buffer, int records_per_group);
  * and produce).  Z_0 = X [M, D_0]; Z_l = act(Z_{l-1} . W_l) for l < L;
  * Y = Z_{L-1} . W_L [M, D_L].  W_l is [D_{l-1}, D_l] row-major bf16; fp32
  * accumulation; the intermediates are stored as bf16 in the plan's
- * workspace.  Items are 128 x 128 output tiles over their whole K. */
+ * workspace.  Items are output tiles over their whole K: 128 x 128, or
+ * 64 x 64 when the narrowest layer would have fewer 128-row tiles than CUs. */
 typedef struct mlp2_chain_s* mlp2_chain_t; /* opaque; created by mlp2_chain_plan, freed by mlp2_chain_destroy */
 
 /* Plan an L-layer chain on the current device.  dims holds L + 1 widths

@@ -70,8 +70,10 @@ struct mlp2_chain_s {
   int act = 0;
   int device = -1;
   int num_cus = 0;
+  int tile = 0;                           // chain tile shape (index into kChainTiles)
+  int bt = 0;                             // its rows and columns
   int Mb = 0;
-  int items[mlp2::kChainMaxLayers] = {};  // tiles per layer: Mb * D_l / 128
+  int items[mlp2::kChainMaxLayers] = {};  // tiles per layer: Mb * D_l / bt
   int total = 0;
   int grid = 0;
   uint32_t spin_limit = 1u << 20;
@@ -902,15 +904,22 @@ int64_t chain_group_rows(int64_t M, int layers, const int64_t* dims) {
 }
 
 mlp2_chain_s* make_chain(int64_t M, int layers, const int64_t* dims, int act, int dev, const hipDeviceProp_t& prop) {
+  // 128 x 128 tiles, unless the narrowest layer would then have fewer tiles
+  // than CUs: 64 x 64 tiles (four times the items) for chains of few rows.
+  int64_t narrowest = dims[1];
+  for (int l = 1; l <= layers; ++l) narrowest = std::min(narrowest, dims[l]);
+  const int tile = (int64_t)ceil_div(M, 128) * (narrowest / 128) < prop.multiProcessorCount ? 1 : 0;
   int occ = 0;
-  if (mlp2::chain_occupancy(&occ) != hipSuccess || occ < 1) { fail(MLP2_ERR_HIP); return nullptr; }
+  if (mlp2::chain_occupancy(tile, &occ) != hipSuccess || occ < 1) { fail(MLP2_ERR_HIP); return nullptr; }
 
   auto* p = new mlp2_chain_s();
   p->M = M; p->L = layers; p->act = act; p->device = dev; p->num_cus = prop.multiProcessorCount;
   for (int l = 0; l <= layers; ++l) p->dims[l] = dims[l];
-  p->Mb = ceil_div(M, mlp2::kChainTile);
+  p->tile = tile;
+  p->bt = mlp2::kChainTiles[tile];
+  p->Mb = ceil_div(M, p->bt);
   for (int l = 0; l < layers; ++l) {
-    p->items[l] = (int)(p->Mb * (dims[l + 1] / mlp2::kChainTile));
+    p->items[l] = (int)(p->Mb * (dims[l + 1] / p->bt));
     p->seq_off[l] = p->total;
     p->total += p->items[l];
   }
@@ -918,7 +927,7 @@ mlp2_chain_s* make_chain(int64_t M, int layers, const int64_t* dims, int act, in
   p->grid = std::min(occ * p->num_cus, p->total);
 
   // workspace: intermediates, then ready counters and control words (zeroed), then rank tables
-  const int64_t Mpad = (int64_t)p->Mb * mlp2::kChainTile;
+  const int64_t Mpad = (int64_t)p->Mb * p->bt;
   const size_t line = mlp2::kLine * 4;
   size_t off = 0, z_off[mlp2::kChainMaxLayers] = {}, r_off[mlp2::kChainMaxLayers] = {};
   for (int l = 0; l + 1 < layers; ++l) {
@@ -979,7 +988,7 @@ mlp2_chain_t mlp2_chain_plan(int64_t M, int layers, const int64_t* dims, int act
   }
   if (layers > mlp2::kChainMaxLayers || M > (1 << 20)) { fail(MLP2_ERR_UNSUPPORTED); return nullptr; }
   for (int l = 0; l <= layers; ++l)
-    if (dims[l] < mlp2::kChainTile || dims[l] % mlp2::kChainTile || dims[l] > (1 << 16)) {
+    if (dims[l] < mlp2::kChainWidthUnit || dims[l] % mlp2::kChainWidthUnit || dims[l] > (1 << 16)) {
       fail(dims[l] < 1 ? MLP2_ERR_INVALID_ARG : MLP2_ERR_UNSUPPORTED);
       return nullptr;
     }
@@ -1046,7 +1055,7 @@ int launch_chain_plan(const mlp2_chain_s* p, const void* X, const void* const* W
   a.spin_limit = p->spin_limit;
   a.drop_signal = -1;
   a.first_static = 0;
-  const int64_t Mpad = (int64_t)p->Mb * mlp2::kChainTile;
+  const int64_t Mpad = (int64_t)p->Mb * p->bt;
   for (int l = 0; l < p->L; ++l) {
     mlp2::ChainLayer& L = c.layer[l];
     L.A = l == 0 ? (const uint16_t*)X : p->Z[l - 1];
@@ -1066,7 +1075,7 @@ int launch_chain_plan(const mlp2_chain_s* p, const void* X, const void* const* W
     a.lists = claim_lists(p->grid);
     c.wait = 1;
     c.end_of_run = 1;
-    if (mlp2::launch_chain(c, p->grid, s) != hipSuccess) return fail(MLP2_ERR_HIP);
+    if (mlp2::launch_chain(p->tile, c, p->grid, s) != hipSuccess) return fail(MLP2_ERR_HIP);
     return MLP2_OK;
   }
   for (int l = 0; l < p->L; ++l) {  // one launch per layer, in order: the stream orders the layers
@@ -1076,7 +1085,7 @@ int launch_chain_plan(const mlp2_chain_s* p, const void* X, const void* const* W
     a.lists = claim_lists(grid);
     c.wait = 0;
     c.end_of_run = l == p->L - 1;
-    if (mlp2::launch_chain(c, grid, s) != hipSuccess) return fail(MLP2_ERR_HIP);
+    if (mlp2::launch_chain(p->tile, c, grid, s) != hipSuccess) return fail(MLP2_ERR_HIP);
   }
   return MLP2_OK;
 }

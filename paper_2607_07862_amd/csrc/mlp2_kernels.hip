@@ -446,7 +446,9 @@ static const Entry* find_entry(const KernelConfig& c) {
 //
 // An L-layer chain Z_l = act(Z_{l-1} W_l), Y = Z_{L-1} W_L: the producer /
 // consumer relation of the two-layer kernel at every layer boundary (Sec.
-// III-A).  An item is a 128 x 128 output tile of one layer over its whole K.
+// III-A).  An item is a T output tile of one layer over its whole K (128 x
+// 128 with a two-stage ring, or 64 x 64 with four stages for chains of few
+// rows, whose 128-row tiles would leave most CUs idle).
 // A middle layer's item consumes like a GEMM2 item (it waits per K-slice on
 // the ready counters of the layer below, row block mb) and produces like a
 // GEMM1 item (activation, its Z rows stored, then its own ready counter
@@ -456,11 +458,12 @@ static const Entry* find_entry(const KernelConfig& c) {
 // and a work-group takes its next ticket only after its current item's last
 // wait.  The sequential mode launches each layer's items on their own, in
 // layer order, without waits; both modes run this item function.
-using ChainT = TileFor<kChainTile, kChainTile, 2>::type;
+using ChainT128 = TileFor<128, 128, 2>::type;
+using ChainT64 = TileFor<64, 64, 4>::type;
 
+template <class T>
 __device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int tile, uint32_t epoch, char* lds,
                                            int* s_slot, Claim& next, int* s_next, TraceAcc& tr) {
-  using T = ChainT;
   const Args& a = c.a;
   const ChainLayer& L = c.layer[layer];
   const int mb = tile % a.Mb, nb = tile / a.Mb;
@@ -497,8 +500,9 @@ __device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int ti
   if (L.ready_out) signal_ready(L.ready_out + (long)tile * kLine);
 }
 
+template <class T>
 __global__ __launch_bounds__(kThreads, 2) void k_mlp2_chain(ChainArgs c) {
-  __shared__ __attribute__((aligned(1024))) char lds[ChainT::template lds_bytes<1>()];
+  __shared__ __attribute__((aligned(1024))) char lds[T::template lds_bytes<1>()];
   __shared__ int s_item, s_slot;
   const Args& a = c.a;
   const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
@@ -517,20 +521,24 @@ __global__ __launch_bounds__(kThreads, 2) void k_mlp2_chain(ChainArgs c) {
     TraceAcc tr;
     Claim next = make_claim(a);
     const uint32_t e = uniform(a.orderp[p]);
-    chain_item(c, (int)(e >> 24), (int)(e & 0xffffffu), epoch, lds, &s_slot, next, &s_item, tr);
+    chain_item<T>(c, (int)(e >> 24), (int)(e & 0xffffffu), epoch, lds, &s_slot, next, &s_item, tr);
     __syncthreads();
     p = uniform(s_item);
   }
   finish_kernel(a, epoch, c.end_of_run != 0);
 }
 
-hipError_t chain_occupancy(int* blocks_per_cu) {
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, (const void*)&k_mlp2_chain, kThreads, 0);
+static const void* chain_kernel(int tile) {
+  return tile == 0 ? (const void*)&k_mlp2_chain<ChainT128> : (const void*)&k_mlp2_chain<ChainT64>;
 }
 
-hipError_t launch_chain(const ChainArgs& c, int grid, hipStream_t stream) {
+hipError_t chain_occupancy(int tile, int* blocks_per_cu) {
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, chain_kernel(tile), kThreads, 0);
+}
+
+hipError_t launch_chain(int tile, const ChainArgs& c, int grid, hipStream_t stream) {
   void* args[] = {const_cast<ChainArgs*>(&c)};
-  return hipLaunchKernel((const void*)&k_mlp2_chain, dim3(grid), dim3(kThreads), args, 0, stream);
+  return hipLaunchKernel(chain_kernel(tile), dim3(grid), dim3(kThreads), args, 0, stream);
 }
 
 bool config_supported(const KernelConfig& c) { return find_entry(c) != nullptr; }

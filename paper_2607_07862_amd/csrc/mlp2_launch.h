@@ -22,9 +22,11 @@ hipError_t launch_sequential(const KernelConfig& c, const Args& a1, const Args& 
 hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
 hipError_t launch_workqueue(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
 
-// ---- GEMM chain: Z_l = act(Z_{l-1} W_l), Y = Z_{L-1} W_L, 128 x 128 tiles, no split-K.
+// ---- GEMM chain: Z_l = act(Z_{l-1} W_l), Y = Z_{L-1} W_L, no split-K.
 constexpr int kChainMaxLayers = 8;
-constexpr int kChainTile = 128;
+constexpr int kChainWidthUnit = 128;  // every width is a multiple of this
+// Tile shapes of the chain kernel: 0 = 128 x 128 (two-stage ring), 1 = 64 x 64 (four stages).
+constexpr int kChainTiles[2] = {128, 64};
 
 // One layer of a chain launch (passed by value with every launch).
 struct ChainLayer {
@@ -49,7 +51,7 @@ struct ChainArgs {
   int end_of_run;  // the run's last launch: it advances the epoch
 };
 
-hipError_t chain_occupancy(int* blocks_per_cu);
-hipError_t launch_chain(const ChainArgs& c, int grid, hipStream_t stream);
+hipError_t chain_occupancy(int tile, int* blocks_per_cu);
+hipError_t launch_chain(int tile, const ChainArgs& c, int grid, hipStream_t stream);
 
 }  // namespace mlp2
