@@ -22,7 +22,11 @@ latency per step.  Beside it the line carries:
   against the published peaks;
 * a table of the modes on every MLP workload, beside eager PyTorch on the
   same inputs (hipBLASLt GEMMs plus an activation kernel) as a reference;
-* the fp64 CPU oracle timed on a bounded sample of the headline workload.
+* the fp64 CPU oracle timed on a bounded sample of the headline workload;
+* with ``--paper-shapes``, the paper's own workload (8192 x 8192 weights,
+  no activation, M = 1024 ... 32768) in every mode, beside eager PyTorch;
+* with ``--chain``, the GEMM chain (4 layers of 8192 x 8192, GELU between,
+  M from ``--chain-rows``) in both modes, beside eager PyTorch.
 
 Only ``--gpus 1`` is supported: the build targets a single GPU.
 """
