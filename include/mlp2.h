@@ -261,6 +261,18 @@ int mlp2_chain_check(mlp2_chain_t plan);
  * path); MLP2_ERR_INVALID_ARG outside 1 .. 2^32 - 1. */
 int mlp2_chain_set_spin_limit(mlp2_chain_t plan, int64_t polls);
 
+/* Persistent work-groups of the chain's one-launch mode (of a whole row
+ * group's launch with row groups); 0 for a NULL plan. */
+int mlp2_chain_grid(mlp2_chain_t plan);
+
+/* Per-item timing records of a chain plan (trace builds only; otherwise
+ * MLP2_ERR_UNSUPPORTED), as mlp2_trace_attach with G = mlp2_chain_grid:
+ * every launch of a run records into section 0 (the sequential mode's
+ * per-layer launches one after another, so its buffer holds the last
+ * layer's); an entry's low 32 bits are layer << 24 | tile; with row groups
+ * the last whole group's launches record. */
+int mlp2_chain_trace_attach(mlp2_chain_t plan, void* buffer, int records_per_group);
+
 /* Free the chain plan and its workspace (synchronises the device first).  NULL-safe. */
 void mlp2_chain_destroy(mlp2_chain_t plan);
 

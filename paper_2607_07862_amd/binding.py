@@ -41,6 +41,8 @@ EXPORTS = (
     "mlp2_chain_check",
     "mlp2_chain_set_spin_limit",
     "mlp2_chain_destroy",
+    "mlp2_chain_grid",
+    "mlp2_chain_trace_attach",
 )
 
 
@@ -144,6 +146,10 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.mlp2_chain_check.argtypes = [P]
     lib.mlp2_chain_set_spin_limit.restype = ctypes.c_int
     lib.mlp2_chain_set_spin_limit.argtypes = [P, ctypes.c_int64]
+    lib.mlp2_chain_grid.restype = ctypes.c_int
+    lib.mlp2_chain_grid.argtypes = [P]
+    lib.mlp2_chain_trace_attach.restype = ctypes.c_int
+    lib.mlp2_chain_trace_attach.argtypes = [P, P, ctypes.c_int]
     lib.mlp2_chain_destroy.restype = None
     lib.mlp2_chain_destroy.argtypes = [P]
     _lib = lib
@@ -321,6 +327,15 @@ class ChainPlan:
 
     def check(self) -> int:
         return self.lib.mlp2_chain_check(self.handle)
+
+    def grid(self) -> int:
+        return int(self.lib.mlp2_chain_grid(self.handle))
+
+    def attach_trace(self, buffer, records_per_group: int) -> None:
+        """Attach a device int64 tensor as the timing-trace buffer (trace builds only)."""
+        rc = self.lib.mlp2_chain_trace_attach(self.handle, _ptr(buffer), int(records_per_group))
+        if rc != OK:
+            raise Mlp2Error(rc, "mlp2_chain_trace_attach")
 
     def set_spin_limit(self, polls: int) -> None:
         rc = self.lib.mlp2_chain_set_spin_limit(self.handle, int(polls))

@@ -86,6 +86,8 @@ struct mlp2_chain_s {
   uint32_t* order_pipe = nullptr; // every item of every layer, after its producers
   int seq_off[mlp2::kChainMaxLayers] = {};
   size_t counters_off = 0, counters_bytes = 0;
+  uint64_t* trace = nullptr;  // caller-owned timing buffer (trace builds)
+  int trace_cap = 0;
   // Row groups (chain_group_rows): launches over whole groups of group_rows
   // rows (`group`) and over the remaining rows (`tail`), in row order.
   int64_t group_rows = 0;
@@ -1055,6 +1057,9 @@ int launch_chain_plan(const mlp2_chain_s* p, const void* X, const void* const* W
   a.spin_limit = p->spin_limit;
   a.drop_signal = -1;
   a.first_static = 0;
+  a.trace = p->trace;
+  a.trace_cap = p->trace_cap;
+  a.trace_groups = p->grid;
   const int64_t Mpad = (int64_t)p->Mb * p->bt;
   for (int l = 0; l < p->L; ++l) {
     mlp2::ChainLayer& L = c.layer[l];
@@ -1108,6 +1113,17 @@ int mlp2_chain_check(mlp2_chain_t p) {
     return fail(MLP2_ERR_HIP);
   return fail(MLP2_ERR_TIMEOUT);
 }
+
+int mlp2_chain_trace_attach(mlp2_chain_t p, void* buffer, int records_per_group) {
+  if (!p || (buffer && records_per_group < 1) || ((uintptr_t)buffer & 7u)) return fail(MLP2_ERR_INVALID_ARG);
+  if (!mlp2::kTrace) return fail(MLP2_ERR_UNSUPPORTED);
+  if (p->group) return mlp2_chain_trace_attach(p->group, buffer, records_per_group);  // the whole groups' launches
+  p->trace = (uint64_t*)buffer;
+  p->trace_cap = buffer ? records_per_group : 0;
+  return MLP2_OK;
+}
+
+int mlp2_chain_grid(mlp2_chain_t p) { return !p ? 0 : p->group ? mlp2_chain_grid(p->group) : p->grid; }
 
 int mlp2_chain_set_spin_limit(mlp2_chain_t p, int64_t polls) {
   if (!p || polls < 1 || polls > 0xFFFFFFFFLL) return fail(MLP2_ERR_INVALID_ARG);

@@ -481,6 +481,7 @@ __device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int ti
     ClaimAtLastStage<NoWait> hook{nowait, &next, K - kBK};
     mainloop<T, 1>(L.A, K, m0, L.alast, Bp, L.N, n0, 0, K, acc, lds, hook, tr);
   }
+  if constexpr (kTrace) tr_mark_mainloop(tr);
   next.park(s_next);
   FragPos<T> fp(m0, n0);
 #pragma unroll
@@ -515,13 +516,18 @@ __global__ __launch_bounds__(kThreads, 2) void k_mlp2_chain(ChainArgs c) {
     __syncthreads();
     p = uniform(s_item);
   }
+  int n_items = 0;
   for (;;) {
     if (p >= total) break;
     __syncthreads();  // every wave has read s_item before the item's claim rewrites it
     TraceAcc tr;
+    if constexpr (kTrace) tr.c_start = trace_clock();
+    const uint64_t t_start = trace_now();
     Claim next = make_claim(a);
     const uint32_t e = uniform(a.orderp[p]);
     chain_item<T>(c, (int)(e >> 24), (int)(e & 0xffffffu), epoch, lds, &s_slot, next, &s_item, tr);
+    // trace entry: layer << 24 | tile; every launch of a run records into section 0
+    if constexpr (kTrace) tr_record(a, 0, n_items++, p, e, t_start, tr);
     __syncthreads();
     p = uniform(s_item);
   }

@@ -137,9 +137,54 @@ def clock_by_eighth(recs, t0):
     return out
 
 
+def chain_summary(B, M: int, layers: int = 4, width: int = 8192):
+    """Per layer of one traced pipelined run of the GEMM chain (GELU between
+    layers, device-drawn inputs): items, mean item, mainloop and flag-wait
+    times, flag share, cycles per item and clock."""
+    import numpy as np
+    import torch
+
+    dims = [width] * (layers + 1)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(3000 + M)
+    X = torch.randn(M, width, device="cuda", generator=gen).to(torch.bfloat16)
+    Ws = [(torch.randn(width, width, device="cuda", generator=gen) * width ** -0.5).to(torch.bfloat16) for _ in range(layers)]
+    Y = torch.empty(M, width, dtype=torch.bfloat16, device="cuda")
+    plan = B.ChainPlan(M, dims, B.ACT_GELU_TANH)
+    G = plan.grid()
+    buf = torch.zeros(2 * G * (1 + 8 * CAP), dtype=torch.int64, device="cuda")
+    for _ in range(5):
+        plan.run(X, Ws, Y, B.MODE_TILE_PIPELINED)
+        plan.run(X, Ws, Y, B.MODE_SEQUENTIAL)
+    torch.cuda.synchronize()
+    plan.attach_trace(buf, CAP)
+    plan.run(X, Ws, Y, B.MODE_TILE_PIPELINED)
+    torch.cuda.synchronize()
+    plan.attach_trace(None, 1)
+    assert plan.check() == B.OK
+    plan.close()
+    recs = _records(buf, G)
+    t0 = min(x[3] for x in recs)
+    span = (max(x[5] for x in recs) - t0) * TICK_US
+    rows = []
+    for layer in range(layers):
+        K = [x for x in recs if (x[1] >> 24) == layer]
+        if not K:
+            continue
+        R = np.array([x[3:] for x in K], dtype=np.float64)  # start, main, end, ring, flag, cycles
+        item = (R[:, 2] - R[:, 0]) * TICK_US
+        rows.append({"layer": layer + 1, "n": len(K), "span": span, "item": item.mean(),
+                     "main": ((R[:, 1] - R[:, 0]) * TICK_US).mean(), "flag": (R[:, 4] * TICK_US).mean(),
+                     "flag_share": (R[:, 4] * TICK_US).sum() / item.sum(), "kcycles": R[:, 5].mean() / 1e3,
+                     "mhz": R[:, 5].sum() / item.sum(),
+                     "start": ((R[:, 0] - t0) * TICK_US).min(), "end": ((R[:, 2] - t0) * TICK_US).max()})
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--workloads", default="tiny,l8b_decode,l8b_prefill,l70b_gated,l70b_shard8")
+    ap.add_argument("--chain-rows", default="", help="also trace the GEMM chain (4 x 8192, GELU) at these row counts")
     ap.add_argument("--out", default=None)
     args = ap.parse_args()
     from paper_2607_07862_amd import binding as B
@@ -170,7 +215,19 @@ def main():
             "two one-launch modes, the latest end among the GEMM1 items writing the Z columns it reads minus its",
             "start (0 when they were done before it started).  Cycles are the item's core clock cycles",
             "(shader-clock counter); the clock is cycles over the item's real time.", ""]
-    text = "\n".join(head + lines + ["", "Clock over the run (items grouped by the eighth of the run they end in):", ""] + clock_lines) + "\n"
+    chain_lines = []
+    if args.chain_rows:
+        chain_lines = ["", "GEMM chain (4 layers of 8192 x 8192, GELU between), one traced pipelined run; per layer:", "",
+                       "| rows | launch µs | layer | items | first start µs | last end µs | item µs | mainloop µs | flag wait µs | flag share | k cycles / item | clock MHz |",
+                       "|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+        for Mc in [int(x) for x in args.chain_rows.split(",")]:
+            for x in chain_summary(B, Mc):
+                chain_lines.append(f"| {Mc} | {x['span']:.1f} | {x['layer']} | {x['n']} | {x['start']:.1f} | {x['end']:.1f} | "
+                                   f"{x['item']:.1f} | {x['main']:.1f} | {x['flag']:.1f} | {100 * x['flag_share']:.1f} % | "
+                                   f"{x['kcycles']:.1f} | {x['mhz']:.0f} |")
+            print(chain_lines[-1], flush=True)
+    text = "\n".join(head + lines + ["", "Clock over the run (items grouped by the eighth of the run they end in):", ""]
+                     + clock_lines + chain_lines) + "\n"
     if args.out:
         with open(args.out, "w") as f:
             f.write(text)
