@@ -145,7 +145,9 @@ typedef struct mlp2_info {
 
 /* Create a plan for Y[M,H] = act(X[M,H] . W1) . W2 on the current HIP device.
  * Requires 1 <= M <= 1<<20, H and F multiples of 64 in [64, 1<<18], act in
- * enum mlp2_act and dtype == MLP2_DTYPE_BF16.  Allocates the workspace (the
+ * enum mlp2_act and dtype == MLP2_DTYPE_BF16, and every operand one launch
+ * reads (X or a row group's X, Z, each weight matrix) below 4 GB: the loads
+ * address an operand with 32-bit byte offsets (MLP2_ERR_UNSUPPORTED otherwise).  Allocates the workspace (the
  * bf16 intermediate Z, split-K partials, counters) on the current device.
  * Returns NULL on failure; mlp2_last_error() gives the code. */
 mlp2_plan_t mlp2_plan(int64_t M, int64_t H, int64_t F, int act, int dtype);
@@ -234,7 +236,8 @@ typedef struct mlp2_chain_s* mlp2_chain_t; /* opaque; created by mlp2_chain_plan
 
 /* Plan an L-layer chain on the current device.  dims holds L + 1 widths
  * D_0 .. D_L (host array, read during the call), each a multiple of 128 in
- * [128, 65536]; 1 <= L <= 8; 1 <= M <= 1<<20; act is MLP2_ACT_IDENTITY or
+ * [128, 65536]; 1 <= L <= 8; 1 <= M <= 1<<20; X, every intermediate and
+ * every weight below 4 GB per launch (32-bit load offsets); act is MLP2_ACT_IDENTITY or
  * MLP2_ACT_GELU_TANH (applied after every layer but the last); dtype
  * MLP2_DTYPE_BF16.  Allocates the intermediates, ready counters and rank
  * tables.  NULL on failure (mlp2_last_error: MLP2_ERR_INVALID_ARG for null or

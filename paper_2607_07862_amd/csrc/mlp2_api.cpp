@@ -506,6 +506,15 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
   }
   const int bm = p->kc.bm, bn1 = p->kc.bn1, bn2 = p->kc.bn2;
   p->Mb = ceil_div(M, bm);
+  // The direct-to-LDS loads address each operand with a 32-bit byte offset
+  // from its base: every operand one launch reads (X, Z, each weight matrix)
+  // stays below 4 GB.
+  const uint64_t lim = (uint64_t)1 << 32;
+  if ((uint64_t)M * H * 2 >= lim || (uint64_t)p->Mb * bm * F * 2 >= lim || (uint64_t)H * F * 2 >= lim) {
+    delete p;
+    fail(MLP2_ERR_UNSUPPORTED);
+    return nullptr;
+  }
   p->Nb1 = (int)(F / bn1);
   p->Nb2 = (int)(H / bn2);
   int occ[4] = {0, 0, 0, 0};
@@ -920,6 +929,19 @@ mlp2_chain_s* make_chain(int64_t M, int layers, const int64_t* dims, int act, in
   p->tile = tile;
   p->bt = mlp2::kChainTiles[tile];
   p->Mb = ceil_div(M, p->bt);
+  // 32-bit byte offsets of the direct-to-LDS loads: X, every intermediate
+  // and every weight matrix stay below 4 GB.
+  const uint64_t lim = (uint64_t)1 << 32;
+  bool too_big = (uint64_t)M * dims[0] * 2 >= lim;
+  for (int l = 0; l < layers; ++l) {
+    too_big |= (uint64_t)dims[l] * dims[l + 1] * 2 >= lim;
+    if (l + 1 < layers) too_big |= (uint64_t)p->Mb * p->bt * dims[l + 1] * 2 >= lim;
+  }
+  if (too_big) {
+    delete p;
+    fail(MLP2_ERR_UNSUPPORTED);
+    return nullptr;
+  }
   for (int l = 0; l < layers; ++l) {
     p->items[l] = (int)(p->Mb * (dims[l + 1] / p->bt));
     p->seq_off[l] = p->total;
