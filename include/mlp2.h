@@ -38,6 +38,10 @@
  * Activations: identity; GELU tanh form 0.5 z (1 + tanh(sqrt(2/pi)(z + 0.044715 z^3)));
  * SwiGLU silu(X.Wg) * (X.Wu) with silu(g) = g / (1 + exp(-g)).
  *
+ * The mlp2_chain_* entry points at the end run the same protocol over a
+ * chain of L GEMMs (Z_l = act(Z_{l-1} . W_l), Y = Z_{L-1} . W_L), where the
+ * middle layers both consume and produce.
+ *
  * Error behaviour: every entry point validates its arguments on the host
  * before it enqueues anything; a failing call has no side effect and returns
  * a negative MLP2_ERR_* code (mlp2_plan returns NULL and records the code for
