@@ -26,7 +26,10 @@ latency per step.  Beside it the line carries:
 * with ``--paper-shapes``, the paper's own workload (8192 x 8192 weights,
   no activation, M = 1024 ... 32768) in every mode, beside eager PyTorch;
 * with ``--chain``, the GEMM chain (4 layers of 8192 x 8192, GELU between,
-  M from ``--chain-rows``) in both modes, beside eager PyTorch.
+  M from ``--chain-rows``) in both modes, beside eager PyTorch;
+* with ``--microbatch``, the sequential mode in micro-batches of rows (the
+  plan's row groups; chunk sizes 1024 ... 8192) beside the pipelined mode,
+  on the paper's shapes at 8192 and 16384 rows.
 
 Only ``--gpus 1`` is supported: the build targets a single GPU.
 """
@@ -168,6 +171,48 @@ def chain_row(B, M: int, steps: int, iters: int) -> dict:
         "torch_eager_us": round(te, 2),
         "mfma_frac": round(flops / (p_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
     }
+
+
+MICROBATCH_ROWS = (1024, 2048, 4096, 8192)
+
+
+def microbatch_row(B, I, key: str, iters: int) -> dict:
+    """The paper's comparison on one GPU: the sequential mode run in
+    micro-batches of rows (the plan's row groups: back-to-back launches over
+    row chunks, each the whole two-kernel sequence) for several chunk sizes,
+    beside the default plan's pipelined and sequential runs; medians of
+    `iters` runs of each, timed one by one in alternating order."""
+    import torch
+
+    w = I.WORKLOADS[key]
+    g = device_random_inputs(w)
+    Y = torch.empty(w.M, w.H, dtype=torch.bfloat16, device="cuda")
+    plans = {"pipelined": (B.Plan(w.M, w.H, w.F, w.act), B.MODE_TILE_PIPELINED),
+             "sequential": (B.Plan(w.M, w.H, w.F, w.act), B.MODE_SEQUENTIAL)}
+    for r in MICROBATCH_ROWS:
+        if r < w.M:
+            plans[f"sequential_microbatch_{r}"] = (B.Plan(w.M, w.H, w.F, w.act, {"row_group": r}), B.MODE_SEQUENTIAL)
+    for plan, mode in plans.values():
+        for _ in range(3):
+            plan.run(g["X"], g["W1"], g["W2"], Y, mode)
+    torch.cuda.synchronize()
+    times = {k: [] for k in plans}
+    for _ in range(iters):
+        for k, (plan, mode) in plans.items():
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record()
+            plan.run(g["X"], g["W1"], g["W2"], Y, mode)
+            e.record()
+            e.synchronize()
+            times[k].append(s.elapsed_time(e) * 1000)
+    for plan, _ in plans.values():
+        assert plan.check() == B.OK
+        plan.close()
+    row = {k: round(statistics.median(v), 2) for k, v in times.items()}
+    micro = min((v, k) for k, v in row.items() if k.startswith("sequential_microbatch"))
+    row["best_microbatch"] = micro[1]
+    row["pipelined_gain_vs_best_microbatch_pct"] = round((micro[0] - row["pipelined"]) / micro[0] * 100, 1)
+    return row
 
 
 def torch_eager_us(w, g, steps):
@@ -379,6 +424,9 @@ def main():
     ap.add_argument("--interleave-iters", type=int, default=100,
                     help="warm runs per mode timed one by one in alternating order (0 skips; a third of it per table row)")
     ap.add_argument("--no-attainable", action="store_true", help="skip the stream and library-GEMM references")
+    ap.add_argument("--microbatch", action="store_true",
+                    help="also time the sequential mode in micro-batches of rows (the paper's comparison, on one GPU) "
+                         "beside the pipelined mode, on the paper's 8192 x 8192 shapes at 8192 and 16384 rows")
     ap.add_argument("--chain", action="store_true",
                     help="also time the GEMM chain: 4 layers of 8192 x 8192 weights, GELU between")
     ap.add_argument("--chain-rows", default=",".join(str(m) for m in CHAIN_ROWS),
@@ -537,6 +585,13 @@ def main():
             table[key] = row
             log(f"TABLE {key:12s} {row}")
 
+    microbatch = {}
+    if args.microbatch:
+        for key in ("paper_m8192", "paper_m16384"):
+            microbatch[key] = microbatch_row(B, I, key, 15)
+            log(f"MICROBATCH {key:14s} {microbatch[key]}")
+            torch.cuda.empty_cache()
+
     chain = {}
     if args.chain:
         for Mc in [int(x) for x in args.chain_rows.split(",")]:
@@ -630,6 +685,7 @@ def main():
         "workloads": table,
         **({"paper_shapes": paper} if paper else {}),
         **({"chain": chain} if chain else {}),
+        **({"microbatch": microbatch} if microbatch else {}),
     }
     print(json.dumps(out), flush=True)
 
