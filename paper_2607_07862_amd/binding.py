@@ -104,14 +104,18 @@ _lib = None
 def load(path: str | None = None) -> ctypes.CDLL:
     """Load the compiled library (raises if it was not built).
 
-    ``MLP2_TRACE=1`` in the environment selects the timing-trace build
-    ``libmlp2_trace.so`` (``python -m paper_2607_07862_amd.build --trace``).
+    The first call loads the product library ``libmlp2.so`` unless ``path``
+    names another build (the timing-trace tool passes ``TRACE_LIB_PATH``);
+    later calls without a path return the loaded one.  A process holds one
+    library: asking for a different path after the first load raises.
     """
     global _lib
     if _lib is not None:
+        if path is not None and os.path.abspath(_lib._name) != os.path.abspath(path):
+            raise RuntimeError(f"{_lib._name} is already loaded; cannot also load {path}")
         return _lib
     if path is None:
-        path = TRACE_LIB_PATH if os.environ.get("MLP2_TRACE") == "1" else LIB_PATH
+        path = LIB_PATH
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with `python -m paper_2607_07862_amd.build`")
     lib = ctypes.CDLL(path)
@@ -154,6 +158,11 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.mlp2_chain_destroy.argtypes = [P]
     _lib = lib
     return lib
+
+
+def loaded_path() -> str | None:
+    """Path of the library this process has loaded, or None."""
+    return None if _lib is None else _lib._name
 
 
 def strerror(code: int) -> str:

@@ -1,14 +1,16 @@
 """Build the HIP library ``libmlp2.so`` in-tree for gfx950 with hipcc.
 
 The library holds the kernels and the C ABI declared in ``include/mlp2.h``.
-``python -m paper_2607_07862_amd.build`` (or ``__graft_entry__.build()``)
-always recompiles.
+``python -m paper_2607_07862_amd.build`` always recompiles (``--trace``: the
+timing-trace build ``libmlp2_trace.so``; ``--all``: both, which is what
+``__graft_entry__.build()`` does).
 """
 from __future__ import annotations
 
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -35,15 +37,25 @@ def build(verbose: bool = False, trace: bool = False) -> str:
     os.makedirs(build_dir, exist_ok=True)
     common = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
               "-I" + os.path.join(ROOT, "include"), "-I" + CSRC] + DEVICE_FLAGS + (["-DMLP2_TRACE"] if trace else [])
+    cmds = []
     for src in SOURCES:
         obj = os.path.join(build_dir, src + ".o")
-        cmd = common + (["-x", "hip"] if src.endswith(".cpp") else []) + ["-c", os.path.join(CSRC, src), "-o", obj]
-        _run(cmd, verbose)
+        cmds.append(common + (["-x", "hip"] if src.endswith(".cpp") else []) + ["-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
+    with ThreadPoolExecutor(len(cmds)) as ex:  # the sources compile independently
+        for f in [ex.submit(_run, c, verbose) for c in cmds]:
+            f.result()
     tmp = lib_path + ".tmp"
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs, verbose)
     os.replace(tmp, lib_path)
     return lib_path
+
+
+def build_all(verbose: bool = False) -> list:
+    """Both libraries from the current sources, side by side: the product and the timing-trace build."""
+    with ThreadPoolExecutor(2) as ex:
+        futs = [ex.submit(build, verbose, False), ex.submit(build, verbose, True)]
+        return [f.result() for f in futs]
 
 
 def _run(cmd, verbose):
@@ -58,4 +70,7 @@ def _run(cmd, verbose):
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv, trace="--trace" in sys.argv))
+    if "--all" in sys.argv:
+        print("\n".join(build_all(verbose="-v" in sys.argv)))
+    else:
+        print(build(verbose="-v" in sys.argv, trace="--trace" in sys.argv))

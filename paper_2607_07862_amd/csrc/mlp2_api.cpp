@@ -807,38 +807,55 @@ int mlp2_plan_info(mlp2_plan_t p, mlp2_info_t* out) {
 
 const void* mlp2_intermediate(mlp2_plan_t p) { return p ? p->Z : nullptr; }
 
+}  // extern "C"
+
+namespace {
+
+// Whether a single-launch plan accepts `value` for option `key`.
+bool option_valid(const mlp2_plan_s* p, int key, int64_t value) {
+  switch (key) {
+    case MLP2_OPT_SPIN_LIMIT: return value >= 1 && value <= 0xFFFFFFFFLL;
+    case MLP2_OPT_DROP_SIGNAL: return value >= -1 && value < (int64_t)p->Mb * p->Nb1;
+    case MLP2_OPT_ORDER: return value >= MLP2_ORDER_AUTO && value <= MLP2_ORDER_BANDED;
+    case MLP2_OPT_GRID: return value >= 0 && value <= p->max_grid;  // 0 = automatic
+    default: return false;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
 int mlp2_set_option(mlp2_plan_t p, int key, int64_t value) {
   if (!p) return fail(MLP2_ERR_INVALID_ARG);
   if (p->group) {  // every group's plan takes the option (a dropped signal: the whole groups')
+    // The value is checked against both sub-plans before either changes, so
+    // a value one of them refuses leaves the grouped plan as it was.
+    const bool to_tail = p->tail && key != MLP2_OPT_DROP_SIGNAL;
+    if (!option_valid(p->group, key, value) || (to_tail && !option_valid(p->tail, key, value)))
+      return fail(MLP2_ERR_INVALID_ARG);
     int rc = mlp2_set_option(p->group, key, value);
-    if (rc == MLP2_OK && p->tail && key != MLP2_OPT_DROP_SIGNAL) rc = mlp2_set_option(p->tail, key, value);
+    if (rc == MLP2_OK && to_tail) rc = mlp2_set_option(p->tail, key, value);
     if (rc == MLP2_OK && key == MLP2_OPT_ORDER) p->order = (int)value;
     return rc;
   }
+  if (!option_valid(p, key, value)) return fail(MLP2_ERR_INVALID_ARG);
   switch (key) {
     case MLP2_OPT_SPIN_LIMIT:
-      if (value < 1 || value > 0xFFFFFFFFLL) return fail(MLP2_ERR_INVALID_ARG);
       p->spin_limit = (uint32_t)value;
       return MLP2_OK;
     case MLP2_OPT_DROP_SIGNAL:
-      if (value < -1 || value >= (int64_t)p->Mb * p->Nb1) return fail(MLP2_ERR_INVALID_ARG);
       p->drop_signal = (int)value;
       return MLP2_OK;
     case MLP2_OPT_ORDER:
-      if (value < MLP2_ORDER_AUTO || value > MLP2_ORDER_BANDED) return fail(MLP2_ERR_INVALID_ARG);
       p->order = (int)value;
       if (hipDeviceSynchronize() != hipSuccess || upload_order(p) != MLP2_OK) return fail(MLP2_ERR_HIP);
       return MLP2_OK;
-    case MLP2_OPT_GRID:
-      // 0 = automatic; otherwise 1 .. the work-groups that fit the device at once
-      if (value < 0 || value > p->max_grid)
-        return fail(MLP2_ERR_INVALID_ARG);
+    default:  // MLP2_OPT_GRID: 0 = automatic, else 1 .. the work-groups that fit the device at once
       p->grid_override = (int)value;
       // the pipelined rank table places GEMM2 items about one grid after their producers
       if (hipDeviceSynchronize() != hipSuccess || upload_order(p) != MLP2_OK) return fail(MLP2_ERR_HIP);
       return MLP2_OK;
-    default:
-      return fail(MLP2_ERR_INVALID_ARG);
   }
 }
 

@@ -211,9 +211,10 @@ __device__ __forceinline__ int swz_b(int k) {
 // inline assembly so that the compiler does not serialise every LDS read
 // behind it (it cannot tell the ring's stages apart); completion is tracked
 // explicitly with s_waitcnt vmcnt.  M0 carries the LDS address; the kernels
-// use M0 for nothing else.
+// use M0 for nothing else, and the asm declares it clobbered so that the
+// compiler never keeps a value of its own there across a load.
 __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base) : "memory");
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base) : "memory", "m0");
 }
 
 // Wait until at most n of this wave's vector-memory operations are outstanding.

@@ -138,3 +138,12 @@ def sample_rows(M: int, count: int, seed: int) -> np.ndarray:
     rng = np.random.default_rng(1000 + seed)
     mid = rng.choice(np.arange(1, M - 1), size=max(count - 2, 0), replace=False)
     return np.unique(np.concatenate([[0, M - 1], mid]))
+
+
+def sample_rows_per_block(M: int, block: int, count: int, seed: int) -> np.ndarray:
+    """``sample_rows(M, count, seed)`` plus one seeded row inside every block of
+    ``block`` consecutive rows (a different offset in each block), sorted."""
+    rng = np.random.default_rng(2000 + seed)
+    starts = np.arange(0, M, block)
+    per = np.array([s + rng.integers(0, min(block, M - s)) for s in starts], dtype=np.int64)
+    return np.unique(np.concatenate([sample_rows(M, count, seed), per]))

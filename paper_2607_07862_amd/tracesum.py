@@ -21,7 +21,6 @@ import argparse
 import os
 import sys
 
-os.environ["MLP2_TRACE"] = "1"
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 sys.path.insert(0, ROOT)
 
@@ -191,7 +190,7 @@ def main():
     from paper_2607_07862_amd import inputs as I
     import bench
 
-    B.load()
+    B.load(B.TRACE_LIB_PATH)  # the timing-trace build, chosen here and nowhere at import time
     lines = ["| workload | mode | launch µs | kind | items | item µs | mainloop µs | ring wait µs | flag wait µs | epilogue µs | flag share | producer-implied wait µs | k cycles / item | clock MHz |",
              "|---|---|---:|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
     clock_lines = ["| workload | mode | launch µs | clock MHz in each eighth of the run |", "|---|---|---:|---|"]

@@ -29,4 +29,7 @@ def lib():
         pytest.skip("no GPU")
     from paper_2607_07862_amd import binding
 
-    return binding.load()
+    lib = binding.load()
+    # the GPU suite checks the product library, never the timing-trace build
+    assert os.path.abspath(binding.loaded_path()) == os.path.abspath(binding.LIB_PATH), binding.loaded_path()
+    return lib

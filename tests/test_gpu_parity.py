@@ -7,7 +7,8 @@
   element by element against the full oracle;
 * the five MLP workloads run at full size in the launch configuration the
   bench times, compared on a seeded sample of rows the oracle computes one
-  by one (max|Y_ref| taken over the sample, which is stricter);
+  by one: one row inside every row block of the plan's tiles and 24 more
+  (max|Y_ref| taken over the sample, which is stricter);
 * structural cases (identity and zero weights) must be bit-exact.
 """
 import numpy as np
@@ -37,6 +38,10 @@ SMALL = [
     (129, 256, 384, 2, {"bm": 128, "splitk1": 2}),
     (200, 320, 640, 2, None),
     (140, 256, 384, 0, {"splitk1": 2, "splitk2": 3}),
+    # 129..256 rows, SwiGLU, H a multiple of 128: the default plan's 256-row
+    # tiles with the 128-column GEMM2 tile run as two 64-column halves
+    (200, 1024, 1024, 2, None),
+    (256, 512, 768, 2, None),
 ]
 
 
@@ -45,6 +50,9 @@ def test_small_shapes_against_full_oracle(lib, M, H, F, act, tuning):
     d = I.make_inputs(M, H, F, act, seed=M * 7 + H + F)
     g = device_inputs(d)
     plan = B.Plan(M, H, F, act, tuning)
+    if act == 2 and 128 < M <= 256 and H % 128 == 0 and tuning is None:
+        info = plan.info()
+        assert (info["bm"], info["bn2"]) == (256, 128), info  # the two-half GEMM2 tile
     Ys, Zs, Yp, Zp = both_modes(plan, g)
     Yq, Zq = workqueue_mode(plan, g)
     ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
@@ -82,7 +90,9 @@ def test_workloads_full_size_sampled_rows(lib, key):
     Yq, Zq = workqueue_mode(plan, g)
     assert_bit_equal(Ys, Yq, "Y sequential vs workqueue")
     assert_bit_equal(Zs, Zq, "Z sequential vs workqueue")
-    rows = I.sample_rows(w.M, 24, w.seed)
+    # one row in every row block of the plan's tiles (a grouped plan's blocks
+    # tile each group, and groups are whole blocks) beside 24 seeded rows
+    rows = I.sample_rows_per_block(w.M, plan.info()["bm"], 24, w.seed)
     ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), w.M, w.H, w.F, w.act, rows=rows)
     r = assert_matches_oracle(Yp[torch.as_tensor(rows, device="cuda")], ref, f"{w.name} sampled rows")
     print(f"[parity] {w.name}: max_abs_err={r['max_abs_err']:.4g} bound={r['bound']:.4g} rel_rms={r['rel_rms']:.3g}")

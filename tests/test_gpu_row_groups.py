@@ -73,6 +73,32 @@ def test_automatic_groups_follow_the_last_level_cache(lib):
     one.close()
 
 
+def test_grouped_option_refused_by_one_sub_plan_changes_neither(lib):
+    """512-row groups take 128 x 128 tiles (two work-groups per CU), the 200-row
+    rest 256-row tiles (one per CU): a grid only the groups accept is refused
+    and leaves both sub-plans as they were; one both accept applies to both."""
+    M, H, F, act = 712, 256, 512, 1
+    d = I.make_inputs(M, H, F, act, seed=91)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, {"row_group": 512})
+    info = plan.info()
+    cus = info["num_cus"]
+    assert info["row_group"] == 512 and info["occupancy"] >= 2, info
+    before = info["grid_pipelined"]
+    with pytest.raises(B.Mlp2Error):
+        plan.set_option(B.OPT_GRID, cus + 8)  # within the groups' limit, beyond the rest's
+    assert plan.info()["grid_pipelined"] == before
+    Ys, _, Yp, _ = both_modes(plan, g)
+    assert_bit_equal(Ys, Yp, "after the refused option")
+    plan.set_option(B.OPT_GRID, cus // 2)
+    assert plan.info()["grid_pipelined"] == cus // 2
+    Ys2, _, Yp2, _ = both_modes(plan, g)
+    assert_bit_equal(Ys, Yp2, "with a smaller grid in every sub-plan")
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
+    assert_matches_oracle(Yp2, ref, "grouped, smaller grid")
+    plan.close()
+
+
 def test_grouped_dropped_signal_times_out_and_recovers(lib):
     M, H, F, act = 600, 128, 256, 1
     d = I.make_inputs(M, H, F, act, seed=90)
