@@ -110,9 +110,9 @@ enum mlp2_order {
 /* Optional tuning for mlp2_plan_ex; a zero field means "choose automatically". */
 typedef struct mlp2_tuning {
   int bm;        /* row-block height shared by both GEMMs: 32, 64, 128 or 256            */
-  int bn1;       /* GEMM1 column-block width (= GEMM2 K-slice granularity): 64 or 128     */
+  int bn1;       /* GEMM1 column-block width (= GEMM2 K-slice granularity): 64, 128 or 256*/
   int splitk1;   /* GEMM1 split-K factor (>= 1)                                           */
-  int bn2;       /* GEMM2 column-block width: 64 or 128                                   */
+  int bn2;       /* GEMM2 column-block width: 64, 128 or 256                              */
   int splitk2;   /* GEMM2 split-K factor (>= 1)                                           */
   int grid;      /* persistent grid of every launch (no more work-groups than fit the
                     device at once)                                                      */
@@ -121,7 +121,15 @@ typedef struct mlp2_tuning {
   int row_group; /* rows per launch group: 0 = automatic (groups once Z of all rows exceeds
                     the 256 MB last-level cache), -1 = one launch over all rows, else a
                     multiple of 256 (groups of that many rows, the last one shorter)      */
-  int reserved[5];
+  int waves;     /* 64-wide waves per work-group: 4 or 8 (as built for the tile shape)     */
+  int lag;       /* pipelined mode, shared roles: ranks between a GEMM2 item and the last
+                    GEMM1 item it reads in the claim order; 0 = automatic (one grid),
+                    -1 = every GEMM2 item after every GEMM1 item                          */
+  int p1;        /* pipelined mode: 0 = shared roles (every work-group takes both kinds of
+                    item from one rank order); else work-groups with index g % 64 < p1
+                    take only GEMM1 items and the others only GEMM2 items (a static
+                    producer / consumer split of the grid, p1 in 1..63 of every 64)       */
+  int reserved[2];
 } mlp2_tuning_t;
 
 /* What a plan chose, for reports and tests. */
@@ -144,7 +152,10 @@ typedef struct mlp2_info {
   int grid_gemm2;        /* persistent work-groups of the GEMM2 launch      */
   int row_group;         /* rows per launch group (0: one launch over all rows);
                             the tile fields above are those of a whole group */
-  int reserved[4];
+  int waves;             /* 64-wide waves per work-group                    */
+  int lag;               /* pipelined rank-table lag in ranks (shared roles) */
+  int p1;                /* static GEMM1 share of every 64 work-groups (0: shared roles) */
+  int reserved[1];
 } mlp2_info_t;
 
 /* Create a plan for Y[M,H] = act(X[M,H] . W1) . W2 on the current HIP device.

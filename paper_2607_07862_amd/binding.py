@@ -57,7 +57,10 @@ class Tuning(ctypes.Structure):
         ("order", ctypes.c_int),
         ("stages", ctypes.c_int),
         ("row_group", ctypes.c_int),
-        ("reserved", ctypes.c_int * 5),
+        ("waves", ctypes.c_int),
+        ("lag", ctypes.c_int),
+        ("p1", ctypes.c_int),
+        ("reserved", ctypes.c_int * 2),
     ]
 
 
@@ -88,7 +91,10 @@ class Info(ctypes.Structure):
         ("grid_gemm1", ctypes.c_int),
         ("grid_gemm2", ctypes.c_int),
         ("row_group", ctypes.c_int),
-        ("reserved", ctypes.c_int * 4),
+        ("waves", ctypes.c_int),
+        ("lag", ctypes.c_int),
+        ("p1", ctypes.c_int),
+        ("reserved", ctypes.c_int * 1),
     ]
 
 

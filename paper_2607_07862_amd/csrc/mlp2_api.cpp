@@ -33,6 +33,8 @@ struct mlp2_plan_s {
   int grid_override = 0;
   int max_grid = 0;  // work-groups of every kernel of the plan that fit the device at once
   int order = MLP2_ORDER_AUTO;
+  int lag = 0;  // pipelined rank-table lag (tuning; 0 = one grid, -1 = after every GEMM1 item)
+  int p1 = 0;   // static GEMM1 share of every 64 work-groups of the pipelined launch (0 = shared roles)
   uint32_t spin_limit = 1u << 20;
   int drop_signal = -1;
   uint64_t* trace = nullptr;  // caller-owned timing buffer (trace builds)
@@ -111,6 +113,17 @@ int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 // Claim lists of a launch: one per XCD (8), or one per work-group for grids
 // below 8, so that every list has a work-group.
 int claim_lists(int grid) { return std::min(8, std::max(1, grid)); }
+
+// Work-groups of the GEMM1 role in a pipelined launch of `grid` work-groups
+// split with share p1 of every 64 (those with index g % 64 < p1).
+int role1_groups(int p1, int grid) { return grid / 64 * p1 + std::min(grid % 64, p1); }
+
+// A role split leaves work-groups in both roles (no split: always true).
+bool roles_ok(int p1, int grid) {
+  if (p1 == 0) return true;
+  const int n1 = role1_groups(p1, grid);
+  return n1 >= 1 && grid - n1 >= 1;
+}
 
 // Split K into S ranges of kc (a multiple of the stage depth): as many parts
 // as keep the tile count times S within `want` items (one round of the
@@ -325,7 +338,10 @@ int upload_order(mlp2_plan_s* p) {
   // then W1 and W2 stream at once and no longer fit the last-level cache
   // together (measured: 30-37 % slower than the sequential mode at 4096 to
   // 32768 rows); the launch then overlaps only the tail of GEMM1.
-  const int lag = uses_bands(p) ? p->items1 : (p->grid_override ? p->grid_override : p->grid);
+  // The lag: a tuning value in ranks, or every GEMM2 item after every GEMM1
+  // item (-1), or by default about one grid (row bands: after every GEMM1 item).
+  const int grid = p->grid_override ? p->grid_override : p->grid;
+  const int lag = p->lag == -1 || uses_bands(p) ? p->items1 : p->lag > 0 ? p->lag : grid;
   build_merged(p, ord, ord2, lag, merged);
   p->lead1 = 0;
   while (p->lead1 < (int64_t)merged.size() && !(merged[p->lead1] & 0x80000000u)) ++p->lead1;
@@ -382,7 +398,8 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   std::memset(&tz, 0, sizeof(tz));
   if (t) tz = *t;
   if (tz.bm < 0 || tz.bn1 < 0 || tz.bn2 < 0 || tz.splitk1 < 0 || tz.splitk2 < 0 || tz.grid < 0 || tz.order < 0 || tz.stages < 0 ||
-      tz.order > MLP2_ORDER_BANDED || tz.row_group < -1 || (tz.row_group > 0 && tz.row_group % 256)) {
+      tz.order > MLP2_ORDER_BANDED || tz.row_group < -1 || (tz.row_group > 0 && tz.row_group % 256) ||
+      (tz.waves != 0 && tz.waves != 4 && tz.waves != 8) || tz.lag < -1 || tz.p1 < 0 || tz.p1 > 63 || tz.p1 % 8) {
     fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
   }
@@ -461,7 +478,7 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
   // weigh more than idle CUs, so both GEMMs keep their K ranges deep; at 64
   // rows small tiles shorten the latency-bound critical path.  Beyond 256 rows (MFMA-bound): 128 x 128 tiles, two work-groups
   // per CU.
-  int pref[4];
+  int pref[5] = {0, 0, 0, 0, 4};  // bm, bn1, bn2, ring depth, waves
   int min_k1 = 256, min_k2 = 256;  // shallowest K range of one split-K part
   if (M <= 32) {
     pref[0] = 32; pref[1] = 64; pref[2] = 128; pref[3] = 4;
@@ -485,14 +502,18 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
     pref[0] = 128; pref[1] = 128; pref[2] = 128; pref[3] = 2;
   }
   // Fallbacks when the preferred tiles do not divide F / H or are not built.
-  const int cand[][4] = {
-      {pref[0], pref[1], pref[2], pref[3]}, {pref[0], pref[1], 64, pref[3]}, {pref[0], 64, 64, pref[3]},
-      {pref[0], pref[1], pref[2], 4},       {pref[0], pref[1], 64, 4},       {pref[0], 64, 64, 4},
-      {128, 64, 64, 4},                     {64, 64, 64, 4},                 {32, 64, 64, 4},
+  const int w = pref[4];
+  const int cand[][5] = {
+      {pref[0], pref[1], pref[2], pref[3], w}, {pref[0], pref[1], 64, pref[3], w}, {pref[0], 64, 64, pref[3], w},
+      {pref[0], pref[1], pref[2], 4, w},       {pref[0], pref[1], 64, 4, w},       {pref[0], 64, 64, 4, w},
+      {pref[0], pref[1], pref[2], pref[3], 4}, {pref[0], pref[1], 64, pref[3], 4}, {pref[0], 64, 64, pref[3], 4},
+      {pref[0], pref[1], pref[2], 4, 4},       {pref[0], pref[1], 64, 4, 4},       {pref[0], 64, 64, 4, 4},
+      {128, 64, 64, 4, 4},                     {64, 64, 64, 4, 4},                 {32, 64, 64, 4, 4},
   };
   bool found = false;
   for (const auto& c : cand) {
-    KernelConfig k{tz.bm ? tz.bm : c[0], tz.bn1 ? tz.bn1 : c[1], tz.bn2 ? tz.bn2 : c[2], nb, tz.stages ? tz.stages : c[3]};
+    KernelConfig k{tz.bm ? tz.bm : c[0], tz.bn1 ? tz.bn1 : c[1], tz.bn2 ? tz.bn2 : c[2], nb, tz.stages ? tz.stages : c[3],
+                   tz.waves ? tz.waves : c[4]};
     if (F % k.bn1 == 0 && H % k.bn2 == 0 && mlp2::config_supported(k)) {
       p->kc = k;
       found = true;
@@ -539,6 +560,8 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
     p->S2 = choose_split(F, tiles2, occ[1] * p->num_cus, min_k2, &p->kc2);
   }
   p->order = tz.order;
+  p->lag = tz.lag;
+  p->p1 = tz.p1;
   p->items1 = tiles1 * p->S1;
   p->items2 = tiles2 * p->S2;
 
@@ -553,6 +576,11 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
   p->grid1 = std::min(occ[0] * p->num_cus, p->items1);
   p->grid2 = std::min(occ[1] * p->num_cus, p->items2);
   p->grid = std::min(std::min(occ[2], occ[3]) * p->num_cus, p->items1 + p->items2);
+  if (!roles_ok(p->p1, tz.grid ? tz.grid : p->grid)) {  // a role split needs work-groups of both roles
+    delete p;
+    fail(MLP2_ERR_UNSUPPORTED);
+    return nullptr;
+  }
   if (p->items2 >= (1 << 24)) {  // workqueue entries hold a unit id in 24 bits
     delete p;
     fail(MLP2_ERR_UNSUPPORTED);
@@ -673,6 +701,8 @@ int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void*
   a.drop_signal = p->drop_signal;
   a.trace = p->trace;
   a.trace_cap = p->trace_cap;
+  a.p1 = 0;
+  a.lists2 = 0;
 
   const int go = p->grid_override;
   const int grids[2] = {go ? go : p->grid1, go ? go : p->grid2};
@@ -695,8 +725,16 @@ int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void*
     a2.first_static = statics(p->items2, grids[1]);  // nor do GEMM2 items of this mode
     err = mlp2::launch_sequential(p->kc, a, a2, grids, s);
   } else if (mode == MLP2_MODE_TILE_PIPELINED) {
-    a.lists = claim_lists(gridp);
-    a.first_static = statics(p->lead1, gridp);
+    if (p->p1) {  // role split: each role's work-groups claim from lists of their own
+      const int n1 = role1_groups(p->p1, gridp);
+      a.p1 = p->p1;
+      a.lists = claim_lists(n1);
+      a.lists2 = claim_lists(gridp - n1);
+      a.first_static = 0;
+    } else {
+      a.lists = claim_lists(gridp);
+      a.first_static = statics(p->lead1, gridp);
+    }
     err = mlp2::launch_pipelined(p->kc, a, gridp, s);
   } else {
     a.lists = claim_lists(gridp);
@@ -802,6 +840,12 @@ int mlp2_plan_info(mlp2_plan_t p, mlp2_info_t* out) {
   out->order = p->order;
   out->workspace_bytes = (int64_t)p->ws_bytes;
   out->spin_limit = p->spin_limit;
+  out->waves = p->kc.waves;
+  {
+    const int grid = p->grid_override ? p->grid_override : p->grid;
+    out->lag = p->lag == -1 || uses_bands(p) ? p->items1 : p->lag > 0 ? p->lag : grid;
+  }
+  out->p1 = p->p1;
   return MLP2_OK;
 }
 
@@ -817,7 +861,8 @@ bool option_valid(const mlp2_plan_s* p, int key, int64_t value) {
     case MLP2_OPT_SPIN_LIMIT: return value >= 1 && value <= 0xFFFFFFFFLL;
     case MLP2_OPT_DROP_SIGNAL: return value >= -1 && value < (int64_t)p->Mb * p->Nb1;
     case MLP2_OPT_ORDER: return value >= MLP2_ORDER_AUTO && value <= MLP2_ORDER_BANDED;
-    case MLP2_OPT_GRID: return value >= 0 && value <= p->max_grid;  // 0 = automatic
+    case MLP2_OPT_GRID:  // 0 = automatic; a role split keeps work-groups in both roles
+      return value >= 0 && value <= p->max_grid && roles_ok(p->p1, value ? (int)value : p->grid);
     default: return false;
   }
 }

@@ -22,7 +22,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
 
-constexpr int kThreads = 256;  // four 64-wide waves per work-group
 constexpr int kBK = 64;        // K depth of one LDS stage
 
 // Words per 128-byte line.  Every counter that work-groups update with device-
@@ -36,12 +35,13 @@ enum {
   CTRL_EPOCH = 0,                  // runs completed; read at kernel start, bumped by the run's last work-group
   CTRL_ERROR = 1 * kLine,          // nonzero once a bounded flag wait gave up
   CTRL_DONE_ALL = 2 * kLine,       // claim lists of the current kernel whose work-groups have all finished
-  CTRL_TICKET = 3 * kLine,         // CTRL_TICKET + l * kLine: next ticket of claim list l (up to 8 lists)
-  CTRL_DONE = 11 * kLine,          // CTRL_DONE + l * kLine: finished work-groups of claim list l
-  CTRL_QHEAD = 19 * kLine,         // workqueue mode: next queue slot a consumer claims
-  CTRL_QTAIL = 20 * kLine,         // workqueue mode: next queue slot a producer fills
-  CTRL_EPOCH_WQ = 21 * kLine,      // workqueue runs completed (the scoreboards advance in those only)
-  CTRL_WORDS = 22 * kLine
+  CTRL_TICKET = 3 * kLine,         // CTRL_TICKET + l * kLine: next ticket of claim list l (up to 16 lists:
+                                   // 8 per role when the pipelined launch splits the grid into roles)
+  CTRL_DONE = 19 * kLine,          // CTRL_DONE + l * kLine: finished work-groups of claim list l
+  CTRL_QHEAD = 35 * kLine,         // workqueue mode: next queue slot a consumer claims
+  CTRL_QTAIL = 36 * kLine,         // workqueue mode: next queue slot a producer fills
+  CTRL_EPOCH_WQ = 37 * kLine,      // workqueue runs completed (the scoreboards advance in those only)
+  CTRL_WORDS = 38 * kLine
 };
 __device__ __forceinline__ int ctrl_ticket(int l) { return CTRL_TICKET + l * kLine; }
 __device__ __forceinline__ int ctrl_done(int l) { return CTRL_DONE + l * kLine; }
@@ -81,6 +81,9 @@ struct Args {
   int lists;               // claim lists of the launch (1 or 8; work-group g claims from list g % lists)
   int first_static;        // work-groups g < first_static take rank g as their first item without a
                            // ticket (ranks below it are items that never wait); the others claim
+  int p1;                  // pipelined launch: 0 = shared roles; else work-groups with g % 64 < p1 take
+                           // GEMM1 items only (from order1) and the others GEMM2 items only (order2)
+  int lists2;              // claim lists of the GEMM2 role (role split only; `lists` is the GEMM1 role's)
 };
 
 // ------------------------------------------------------------------ optional timing trace
@@ -159,8 +162,11 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 
 // A work-group tile of BM rows (the M side: X or Z rows) by BN columns (the N
 // side: W columns), staged through an NS-deep ring of LDS buffers of kBK rows
-// of K each.  Four waves in a WM x WN grid; each wave owns a (BM/WM) x
-// (BN/WN) sub-tile made of 16x16 MFMA blocks.
+// of K each.  Four or eight 64-wide waves in a WM x WN grid; each wave owns a
+// (BM/WM) x (BN/WN) sub-tile made of 16x16 MFMA blocks.  Eight waves let a
+// large tile (256 x 256: a quarter of the operand bytes per flop of 128 x 128)
+// keep two waves per SIMD, so that one wave's LDS reads overlap the other's
+// products.
 //
 // The MFMA is issued with the *weight* fragment as its A operand and the
 // activation fragment as its B operand, so each lane ends up holding output
@@ -179,7 +185,9 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 template <int BM_, int BN_, int WM_, int WN_, int NS_>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NS = NS_;
-  static_assert(WM * WN == 4, "four waves");
+  static constexpr int NWAVES = WM * WN;
+  static constexpr int THREADS = 64 * NWAVES;
+  static_assert(NWAVES == 4 || NWAVES == 8, "four or eight waves");
   static_assert(BN == 64 || BN == 128 || BN == 256, "weight tile width");
   static_assert(NS >= 2, "at least double buffered");
   static constexpr int MW = BM / WM;  // rows per wave
@@ -189,9 +197,10 @@ struct Tile {
   static_assert(TM >= 1 && TN >= 2 && TN % 2 == 0, "wave tile shape");
   static constexpr int A_BYTES = BM * kBK * 2;
   static constexpr int B_BYTES = kBK * BN * 2;
-  static constexpr int A_DMA = A_BYTES / 1024 / 4;  // 1 KB wave loads per wave and stage
-  static constexpr int B_DMA = B_BYTES / 1024 / 4;
-  static_assert(A_DMA >= 1 && B_DMA >= 1, "tile too small for four waves");
+  static constexpr int A_DMA = A_BYTES / 1024 / NWAVES;  // 1 KB wave loads per wave and stage
+  static constexpr int B_DMA = B_BYTES / 1024 / NWAVES;
+  static_assert(A_DMA >= 1 && B_DMA >= 1 && A_BYTES % (1024 * NWAVES) == 0 && B_BYTES % (1024 * NWAVES) == 0,
+                "every wave loads whole 1 KB pieces of both operands");
   template <int NB>
   static constexpr int stage_bytes() { return A_BYTES + NB * B_BYTES; }
   template <int NB>
@@ -210,11 +219,11 @@ __device__ __forceinline__ int swz_b(int k) {
 // base + voff and writes them to LDS at lds_addr + 16 i.  Issued through
 // inline assembly so that the compiler does not serialise every LDS read
 // behind it (it cannot tell the ring's stages apart); completion is tracked
-// explicitly with s_waitcnt vmcnt.  M0 carries the LDS address; the kernels
-// use M0 for nothing else, and the asm declares it clobbered so that the
-// compiler never keeps a value of its own there across a load.
+// explicitly with s_waitcnt vmcnt.  M0 carries the LDS address: it is an
+// operand of the asm ("{m0}" constraint), so the compiler itself writes it and
+// knows the register holds that value, and never has a value of its own there.
 __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_addr), "v"(voff), "s"(base) : "memory", "m0");
+  asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(lds_addr) : "memory");
 }
 
 // Wait until at most n of this wave's vector-memory operations are outstanding.
@@ -282,7 +291,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   uint32_t a_off[T::A_DMA];
 #pragma unroll
   for (int j = 0; j < T::A_DMA; ++j) {
-    const int ch = wave + 4 * j;  // 1 KB chunk = 8 rows of 128 B
+    const int ch = wave + T::NWAVES * j;  // 1 KB chunk = 8 rows of 128 B
     const int row = 8 * ch + (lane >> 3);
     const int lc = (lane & 7) ^ swz_a(row);
     int gr = m0 + row;
@@ -294,7 +303,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   uint32_t b_off[T::B_DMA];
 #pragma unroll
   for (int j = 0; j < T::B_DMA; ++j) {
-    const int ch = wave + 4 * j;
+    const int ch = wave + T::NWAVES * j;
     const int row = RPC * ch + lane / CPR;
     const int lc = (lane % CPR) ^ swz_b<T::BN>(row);
     b_off[j] = (uint32_t)(((long)row * ldb + n0 + 8 * lc) * 2);
@@ -308,11 +317,11 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
 #pragma unroll
       for (int j = 0; j < T::B_DMA; ++j)
         dma16(Bp[b], b_off[j] + (uint32_t)((long)k * ldb * 2),
-              uniform(sbase + (uint32_t)(T::A_BYTES + b * T::B_BYTES + (wave + 4 * j) * 1024)));
+              uniform(sbase + (uint32_t)(T::A_BYTES + b * T::B_BYTES + (wave + T::NWAVES * j) * 1024)));
     wait(k);
 #pragma unroll
     for (int j = 0; j < T::A_DMA; ++j)
-      dma16(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + 4 * j) * 1024)));
+      dma16(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + T::NWAVES * j) * 1024)));
   };
 
   // Fragment addressing (bytes inside a stage).
@@ -448,8 +457,8 @@ __device__ __forceinline__ void pair_values(const f32x4 (&a)[T::TN][T::TM], int 
 template <class T, int NB>
 struct Partial {
   static constexpr int PER_WAVE = NB * T::TN * T::TM;  // f32x4 per lane
-  static constexpr long PER_ITEM = 4L * PER_WAVE * 64;  // f32x4 per (tile, split)
-  static constexpr int UNITS = 4 * T::TM * (T::TN / 2); // (wave, tm, tp) triples per tile
+  static constexpr long PER_ITEM = (long)T::NWAVES * PER_WAVE * 64;  // f32x4 per (tile, split)
+  static constexpr int UNITS = T::NWAVES * T::TM * (T::TN / 2); // (wave, tm, tp) triples per tile
   __device__ static long block_index(long tile, int S, int s, int w, int b, int tn, int tm) {
     return (tile * S + s) * PER_ITEM + ((long)w * PER_WAVE + ((b * T::TN + tn) * T::TM + tm)) * 64;
   }

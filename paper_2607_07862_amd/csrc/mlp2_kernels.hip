@@ -55,10 +55,35 @@ __device__ __forceinline__ void store_y(const Args& a, int row, int col, const f
 // ranks in order.  Work-groups g < first_static take rank g as their first
 // item without a ticket (those ranks are items that never wait); list l then
 // skips the ranks below first_static it would hand out.
-__device__ __forceinline__ Claim make_claim(const Args& a) {
-  const int l = (int)(blockIdx.x % (unsigned)a.lists);
-  const int skip = l < a.first_static ? (a.first_static - 1 - l) / a.lists + 1 : 0;
-  return Claim{a.ctrl + ctrl_ticket(l), l, a.lists, skip, 0u};
+//
+// With a role split (Args::p1) the pipelined launch holds two sets of claim
+// lists: the GEMM1 role's work-groups (g % 64 < p1) deal the GEMM1 order
+// table's ranks over lists 0..7, the GEMM2 role's the GEMM2 order table's over
+// lists 8..15.  A work-group's list is its index among its role's work-groups
+// modulo the role's list count; with p1 a multiple of 8 that index is
+// congruent to g modulo 8, so every XCD still takes every 8th item of each
+// role.
+struct ListPos {
+  int role;   // -1 shared, 0 GEMM1 role, 1 GEMM2 role
+  int i, n;   // this work-group's index among the work-groups of its set, and their number
+  int lists;  // claim lists of the set
+  int list;   // this work-group's list, as an index into the control words' ticket and done lines
+};
+
+__device__ __forceinline__ ListPos list_pos(const Args& a, bool roles) {
+  const int g = (int)blockIdx.x, G = (int)gridDim.x;
+  if (!roles) return ListPos{-1, g, G, a.lists, g % a.lists};
+  const int q = g / 64, j = g % 64, full = G / 64, rem = G % 64;
+  const int n1 = full * a.p1 + min(rem, a.p1);
+  if (j < a.p1) return ListPos{0, q * a.p1 + j, n1, a.lists, (q * a.p1 + j) % a.lists};
+  const int i = q * (64 - a.p1) + (j - a.p1);
+  return ListPos{1, i, G - n1, a.lists2, 8 + i % a.lists2};
+}
+
+__device__ __forceinline__ Claim make_claim(const Args& a, const ListPos& lp) {
+  const int l = lp.i % lp.lists;
+  const int skip = lp.role < 0 && l < a.first_static ? (a.first_static - 1 - l) / lp.lists + 1 : 0;
+  return Claim{a.ctrl + ctrl_ticket(lp.list), l, lp.lists, skip, 0u};
 }
 
 // ------------------------------------------------------------------ trace records (MLP2_TRACE builds)
@@ -101,7 +126,7 @@ __device__ __forceinline__ void reduce_epilogue(const float* part, long tile, in
   constexpr int G = NB == 1 ? 2 : 1;
   static_assert(U % G == 0, "units per group");
   const int lane = threadIdx.x & 63;
-  for (int u0 = uniform((int)(threadIdx.x >> 6)) * G; u0 < U; u0 += 4 * G) {
+  for (int u0 = uniform((int)(threadIdx.x >> 6)) * G; u0 < U; u0 += T::NWAVES * G) {
     Unit<T> ug[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) ug[g] = Unit<T>(u0 + g);
@@ -242,19 +267,20 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
 // stream-ordered before the plan's next kernel.  Spreading the done counts
 // over the lists keeps the exit atomics, one per work-group, off a single
 // line.
-__device__ __forceinline__ void finish_kernel(const Args& a, uint32_t epoch, bool end_of_run, bool wq_run = false,
-                                              uint32_t wq_epoch = 0) {
+__device__ __forceinline__ void finish_kernel(const Args& a, const ListPos& lp, uint32_t epoch, bool end_of_run,
+                                              bool wq_run = false, uint32_t wq_epoch = 0) {
   __syncthreads();
   if (threadIdx.x == 0) {
-    const int l = (int)(blockIdx.x % (unsigned)a.lists);
-    const uint32_t in_list = (gridDim.x - 1u - (unsigned)l) / (unsigned)a.lists + 1u;
-    const uint32_t old = __hip_atomic_fetch_add(a.ctrl + ctrl_done(l), 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    const int l = lp.i % lp.lists;
+    const uint32_t in_list = (uint32_t)((lp.n - 1 - l) / lp.lists + 1);
+    const uint32_t old = __hip_atomic_fetch_add(a.ctrl + ctrl_done(lp.list), 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
     if (old == in_list - 1u) {
-      __hip_atomic_store(a.ctrl + ctrl_ticket(l), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(a.ctrl + ctrl_done(l), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.ctrl + ctrl_ticket(lp.list), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(a.ctrl + ctrl_done(lp.list), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const uint32_t lists_done =
           __hip_atomic_fetch_add(a.ctrl + CTRL_DONE_ALL, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-      if (lists_done == (uint32_t)a.lists - 1u) {
+      const uint32_t all_lists = (uint32_t)(lp.role < 0 ? a.lists : a.lists + a.lists2);
+      if (lists_done == all_lists - 1u) {
         __hip_atomic_store(a.ctrl + CTRL_DONE_ALL, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(a.ctrl + CTRL_QHEAD, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(a.ctrl + CTRL_QTAIL, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -308,28 +334,35 @@ constexpr int kernel_lds() {
                                 : MaxI<T1::template lds_bytes<NB>(), T2::template lds_bytes<HV>()>::value;
 }
 
-// Work-groups per CU the register budget must allow: two whenever two rings fit in LDS.
+// Work-groups per CU the register budget must allow: two four-wave groups
+// whenever two rings fit in LDS; eight-wave groups run one per CU (two
+// waves per SIMD already).
 template <class T1, int NB, class T2, int HV, int PHASE>
 constexpr int min_blocks() {
-  return kernel_lds<T1, NB, T2, HV, PHASE>() <= 80 * 1024 ? 2 : 1;
+  return kernel_lds<T1, NB, T2, HV, PHASE>() <= 80 * 1024 && T1::NWAVES == 4 ? 2 : 1;
 }
 
 // T1, NB: GEMM1 tile and weight operands; T2, HV: GEMM2 tile half and halves.
+// Both item kinds run in the same work-groups, so their tiles have the same waves.
 template <class T1, int NB, class T2, int HV, int PHASE>
-__global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) void k_mlp2(Args a) {
+__global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>())) void k_mlp2(Args a) {
+  static_assert(T1::THREADS == T2::THREADS, "one work-group shape for both item kinds");
   constexpr int kLds = kernel_lds<T1, NB, T2, HV, PHASE>();
   __shared__ __attribute__((aligned(1024))) char lds[kLds];
   __shared__ int s_item, s_slot;
   const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
   const uint32_t wq_epoch = PHASE == PHASE_WORKQUEUE ? uniform(ld_relaxed(a.ctrl + CTRL_EPOCH_WQ)) : 0u;
-  const int g1 = PHASE == PHASE_GEMM2 ? 0 : a.items1;
-  const int g2 = PHASE == PHASE_GEMM2 || PHASE == PHASE_PIPELINED ? a.items2 : 0;
+  // A role split (pipelined launch only): this work-group takes the items of
+  // one kind, in that kind's order table; otherwise both kinds from one order.
+  const ListPos lp = list_pos(a, PHASE == PHASE_PIPELINED && a.p1 > 0);
+  const int g1 = PHASE == PHASE_GEMM2 || lp.role == 1 ? 0 : a.items1;
+  const int g2 = (PHASE == PHASE_GEMM2 || PHASE == PHASE_PIPELINED) && lp.role != 0 ? a.items2 : 0;
   const int total = g1 + g2;
   int p;
-  if ((int)blockIdx.x < a.first_static) {
+  if (lp.role < 0 && (int)blockIdx.x < a.first_static) {
     p = (int)blockIdx.x;
   } else {
-    Claim first = make_claim(a);
+    Claim first = make_claim(a, lp);
     first.issue();
     first.park(&s_item);
     __syncthreads();
@@ -342,10 +375,10 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
     TraceAcc tr;
     if constexpr (kTrace) tr.c_start = trace_clock();
     const uint64_t t_start = trace_now();
-    Claim next = make_claim(a);
+    Claim next = make_claim(a, lp);
     uint32_t e;  // order-table entry: item id, bit 31 set for a GEMM2 item
     if constexpr (PHASE == PHASE_PIPELINED) {
-      e = uniform(a.orderp[p]);
+      e = lp.role < 0 ? uniform(a.orderp[p]) : lp.role == 0 ? uniform(a.order1[p]) : (uniform(a.order2[p]) | 0x80000000u);
       if (e & 0x80000000u)
         gemm2_item<T2, HV, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr);
       else
@@ -378,13 +411,13 @@ __global__ __launch_bounds__(kThreads, (min_blocks<T1, NB, T2, HV, PHASE>())) vo
       c_pop = trace_clock();
     }
   }
-  finish_kernel(a, epoch, PHASE != PHASE_GEMM1, PHASE == PHASE_WORKQUEUE, wq_epoch);
+  finish_kernel(a, lp, epoch, PHASE != PHASE_GEMM1, PHASE == PHASE_WORKQUEUE, wq_epoch);
 }
 
 // ------------------------------------------------------------------ dispatch table
 
-// Tile shapes by (rows, columns, ring depth).
-template <int BM, int BN, int NS>
+// Tile shapes by (rows, columns, ring depth, waves).
+template <int BM, int BN, int NS, int W = 4>
 struct TileFor;
 template <int NS> struct TileFor<32, 64, NS> { using type = Tile<32, 64, 2, 2, NS>; };
 template <int NS> struct TileFor<32, 128, NS> { using type = Tile<32, 128, 1, 4, NS>; };
@@ -397,9 +430,18 @@ template <int NS> struct TileFor<64, 256, NS> { using type = Tile<64, 256, 1, 4,
 template <int NS> struct TileFor<32, 256, NS> { using type = Tile<32, 256, 1, 4, NS>; };
 template <int NS> struct TileFor<256, 64, NS> { using type = Tile<256, 64, 4, 1, NS>; };
 template <int NS> struct TileFor<256, 128, NS> { using type = Tile<256, 128, 4, 1, NS>; };
+// eight waves
+template <int NS> struct TileFor<256, 256, NS, 8> { using type = Tile<256, 256, 2, 4, NS>; };
+template <int NS> struct TileFor<256, 128, NS, 8> { using type = Tile<256, 128, 4, 2, NS>; };
+template <int NS> struct TileFor<256, 64, NS, 8> { using type = Tile<256, 64, 4, 2, NS>; };
+template <int NS> struct TileFor<128, 256, NS, 8> { using type = Tile<128, 256, 2, 4, NS>; };
+template <int NS> struct TileFor<128, 128, NS, 8> { using type = Tile<128, 128, 2, 4, NS>; };
+template <int NS> struct TileFor<128, 64, NS, 8> { using type = Tile<128, 64, 4, 2, NS>; };
+template <int NS> struct TileFor<64, 256, NS, 8> { using type = Tile<64, 256, 2, 4, NS>; };
+template <int NS> struct TileFor<32, 256, NS, 8> { using type = Tile<32, 256, 1, 8, NS>; };
 
 struct Entry {
-  int bm, bn1, bn2, nb, ns;
+  int bm, bn1, bn2, nb, ns, waves;
   const void* seq1;
   const void* seq2;
   const void* pipe;
@@ -408,14 +450,16 @@ struct Entry {
 
 // GEMM2 of BN2 columns as one tile (HV = 1), or as two halves of BN2 / 2 that
 // share the GEMM1 tile shape (HV = 2).
-#define MLP2_K(BM, BN1, BN2, NB, NS, HV, PH)                                                             \
-  (const void*)&k_mlp2<typename TileFor<BM, BN1, NS>::type, NB, typename TileFor<BM, (BN2) / (HV), NS>::type, HV, PH>
-#define MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, HV)                                                       \
-  Entry {                                                                                             \
-    BM, BN1, BN2, NB, NS, MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_GEMM1),                             \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_GEMM2), MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_PIPELINED), \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, PHASE_WORKQUEUE)                                                 \
+#define MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PH)                                                                   \
+  (const void*)&k_mlp2<typename TileFor<BM, BN1, NS, W>::type, NB, typename TileFor<BM, (BN2) / (HV), NS, W>::type, \
+                       HV, PH>
+#define MLP2_ENTRY_W(BM, BN1, BN2, NB, NS, HV, W)                                                                 \
+  Entry {                                                                                                         \
+    BM, BN1, BN2, NB, NS, W, MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_GEMM1),                                   \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_GEMM2), MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_PIPELINED), \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_WORKQUEUE)                                                     \
   }
+#define MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, HV) MLP2_ENTRY_W(BM, BN1, BN2, NB, NS, HV, 4)
 #define MLP2_ENTRY(BM, BN1, BN2, NB, NS) MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, 1)
 
 static const Entry kEntries[] = {
@@ -434,11 +478,17 @@ static const Entry kEntries[] = {
     // gated GEMM2 of 128 columns runs as two 64-column halves (the GEMM1 shape)
     MLP2_ENTRY_HV(256, 64, 128, 2, 3, 2), MLP2_ENTRY(256, 64, 64, 2, 3), MLP2_ENTRY(256, 128, 128, 1, 3),
     MLP2_ENTRY(256, 64, 64, 1, 3),
+    // eight-wave work-groups: large tiles, two waves per SIMD
+    MLP2_ENTRY_W(256, 256, 256, 1, 2, 1, 8), MLP2_ENTRY_W(256, 128, 128, 1, 3, 1, 8),
+    MLP2_ENTRY_W(256, 256, 128, 1, 2, 1, 8), MLP2_ENTRY_W(256, 128, 256, 1, 2, 2, 8),
+    MLP2_ENTRY_W(256, 128, 256, 2, 2, 2, 8), MLP2_ENTRY_W(256, 64, 128, 2, 3, 2, 8),
+    MLP2_ENTRY_W(128, 128, 128, 1, 4, 1, 8), MLP2_ENTRY_W(128, 256, 256, 1, 3, 1, 8),
+    MLP2_ENTRY_W(128, 64, 64, 1, 4, 1, 8),
 };
 
 static const Entry* find_entry(const KernelConfig& c) {
   for (const Entry& e : kEntries)
-    if (e.bm == c.bm && e.bn1 == c.bn1 && e.bn2 == c.bn2 && e.nb == c.nb && e.ns == c.ns) return &e;
+    if (e.bm == c.bm && e.bn1 == c.bn1 && e.bn2 == c.bn2 && e.nb == c.nb && e.ns == c.ns && e.waves == c.waves) return &e;
   return nullptr;
 }
 
@@ -460,6 +510,8 @@ static const Entry* find_entry(const KernelConfig& c) {
 // layer order, without waits; both modes run this item function.
 using ChainT128 = TileFor<128, 128, 2>::type;
 using ChainT64 = TileFor<64, 64, 4>::type;
+constexpr int kChainThreads = 256;
+static_assert(ChainT128::THREADS == kChainThreads && ChainT64::THREADS == kChainThreads, "chain tiles: four waves");
 
 template <class T>
 __device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int tile, uint32_t epoch, char* lds,
@@ -502,15 +554,16 @@ __device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int ti
 }
 
 template <class T>
-__global__ __launch_bounds__(kThreads, 2) void k_mlp2_chain(ChainArgs c) {
+__global__ __launch_bounds__(kChainThreads, 2) void k_mlp2_chain(ChainArgs c) {
   __shared__ __attribute__((aligned(1024))) char lds[T::template lds_bytes<1>()];
   __shared__ int s_item, s_slot;
   const Args& a = c.a;
   const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
   const int total = a.items1;
+  const ListPos lp = list_pos(a, false);
   int p;
   {
-    Claim first = make_claim(a);
+    Claim first = make_claim(a, lp);
     first.issue();
     first.park(&s_item);
     __syncthreads();
@@ -523,7 +576,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_mlp2_chain(ChainArgs c) {
     TraceAcc tr;
     if constexpr (kTrace) tr.c_start = trace_clock();
     const uint64_t t_start = trace_now();
-    Claim next = make_claim(a);
+    Claim next = make_claim(a, lp);
     const uint32_t e = uniform(a.orderp[p]);
     chain_item<T>(c, (int)(e >> 24), (int)(e & 0xffffffu), epoch, lds, &s_slot, next, &s_item, tr);
     // trace entry: layer << 24 | tile; every launch of a run records into section 0
@@ -531,7 +584,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_mlp2_chain(ChainArgs c) {
     __syncthreads();
     p = uniform(s_item);
   }
-  finish_kernel(a, epoch, c.end_of_run != 0);
+  finish_kernel(a, lp, epoch, c.end_of_run != 0);
 }
 
 static const void* chain_kernel(int tile) {
@@ -539,12 +592,12 @@ static const void* chain_kernel(int tile) {
 }
 
 hipError_t chain_occupancy(int tile, int* blocks_per_cu) {
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, chain_kernel(tile), kThreads, 0);
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, chain_kernel(tile), kChainThreads, 0);
 }
 
 hipError_t launch_chain(int tile, const ChainArgs& c, int grid, hipStream_t stream) {
   void* args[] = {const_cast<ChainArgs*>(&c)};
-  return hipLaunchKernel(chain_kernel(tile), dim3(grid), dim3(kThreads), args, 0, stream);
+  return hipLaunchKernel(chain_kernel(tile), dim3(grid), dim3(kChainThreads), args, 0, stream);
 }
 
 bool config_supported(const KernelConfig& c) { return find_entry(c) != nullptr; }
@@ -553,7 +606,7 @@ hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu) {
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
   const void* k = which == 0 ? e->seq1 : which == 1 ? e->seq2 : which == 2 ? e->pipe : e->wq;
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, kThreads, 0);
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, 64 * e->waves, 0);
 }
 
 hipError_t launch_sequential(const KernelConfig& c, const Args& a1, const Args& a2, const int grids[2],
@@ -561,24 +614,24 @@ hipError_t launch_sequential(const KernelConfig& c, const Args& a1, const Args& 
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
   void* args1[] = {const_cast<Args*>(&a1)};
-  hipError_t err = hipLaunchKernel(e->seq1, dim3(grids[0]), dim3(kThreads), args1, 0, stream);
+  hipError_t err = hipLaunchKernel(e->seq1, dim3(grids[0]), dim3(64 * e->waves), args1, 0, stream);
   if (err != hipSuccess) return err;
   void* args2[] = {const_cast<Args*>(&a2)};
-  return hipLaunchKernel(e->seq2, dim3(grids[1]), dim3(kThreads), args2, 0, stream);
+  return hipLaunchKernel(e->seq2, dim3(grids[1]), dim3(64 * e->waves), args2, 0, stream);
 }
 
 hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipStream_t stream) {
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
   void* args[] = {const_cast<Args*>(&a)};
-  return hipLaunchKernel(e->pipe, dim3(grid), dim3(kThreads), args, 0, stream);
+  return hipLaunchKernel(e->pipe, dim3(grid), dim3(64 * e->waves), args, 0, stream);
 }
 
 hipError_t launch_workqueue(const KernelConfig& c, const Args& a, int grid, hipStream_t stream) {
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
   void* args[] = {const_cast<Args*>(&a)};
-  return hipLaunchKernel(e->wq, dim3(grid), dim3(kThreads), args, 0, stream);
+  return hipLaunchKernel(e->wq, dim3(grid), dim3(64 * e->waves), args, 0, stream);
 }
 
 }  // namespace mlp2

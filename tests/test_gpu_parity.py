@@ -42,6 +42,17 @@ SMALL = [
     # tiles with the 128-column GEMM2 tile run as two 64-column halves
     (200, 1024, 1024, 2, None),
     (256, 512, 768, 2, None),
+    # eight-wave work-groups: 256 x 256 tiles (two row blocks, the second ragged),
+    # 256-row tiles of 128 columns, GEMM2 as two halves, the gated shapes
+    (300, 512, 768, 1, {"waves": 8, "bm": 256, "bn1": 256, "bn2": 256, "stages": 2}),
+    (300, 512, 768, 0, {"waves": 8, "bm": 256, "bn1": 256, "bn2": 128, "stages": 2, "splitk2": 2}),
+    (257, 384, 640, 1, {"waves": 8, "bm": 256, "bn1": 128, "bn2": 128, "stages": 3, "splitk2": 2}),
+    (300, 256, 512, 1, {"waves": 8, "bm": 256, "bn1": 128, "bn2": 256, "stages": 2}),
+    (300, 256, 512, 2, {"waves": 8, "bm": 256, "bn1": 128, "bn2": 256, "stages": 2}),
+    (200, 256, 640, 2, {"waves": 8, "bm": 256, "bn1": 64, "bn2": 128, "stages": 3, "splitk1": 2}),
+    (130, 512, 1024, 1, {"waves": 8, "bm": 128, "bn1": 128, "bn2": 128, "stages": 4, "splitk1": 2, "splitk2": 2}),
+    (100, 1024, 768, 0, {"waves": 8, "bm": 128, "bn1": 256, "bn2": 256, "stages": 3, "splitk1": 2}),
+    (90, 256, 384, 1, {"waves": 8, "bm": 128, "bn1": 64, "bn2": 64, "stages": 4}),
 ]
 
 

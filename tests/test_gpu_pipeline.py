@@ -12,6 +12,9 @@
   blocks of a consumer whose first 64 are all ready (the wait reads
   readiness 64 blocks at a time);
 * the workqueue mode (scoreboards and a device queue) gives the same bits;
+* so do the stage splits of the pipelined launch: the rank-table lag at its
+  extremes (one rank; every GEMM2 item after every GEMM1 item) and static
+  producer / consumer role splits of the grid;
 * a run captured into a graph replays with the eager bits, in every mode.
 """
 import pytest
@@ -48,6 +51,56 @@ def test_orders_and_grids_match_sequential_bits(lib, order, grid):
     assert_bit_equal(Ys, Yp, f"order {order} grid {grid}")
     assert_bit_equal(Ys, Yq, f"order {order} grid {grid} workqueue")
     assert_bit_equal(Ys, Ys2, f"order {order} grid {grid} sequential after the order change")
+    plan.close()
+
+
+# The stage split of the pipelined launch: the rank-table lag (shared roles)
+# at its extremes, and static role splits of the grid, on a shape whose GEMM1
+# spans several rounds of the grid (so consumers really wait on producers).
+SPLITS = [
+    {"lag": 1}, {"lag": -1}, {"lag": 100000}, {"lag": 37},
+    {"p1": 8}, {"p1": 32}, {"p1": 56},
+    {"p1": 32, "waves": 8, "bm": 256, "bn1": 256, "bn2": 256, "stages": 2},
+    {"lag": 1, "waves": 8, "bm": 256, "bn1": 128, "bn2": 128, "stages": 3, "splitk2": 2},
+]
+
+
+@pytest.mark.parametrize("tuning", SPLITS, ids=[",".join(f"{k}{v}" for k, v in t.items()) for t in SPLITS])
+@pytest.mark.parametrize("grid", [0, 60])
+def test_stage_splits_match_sequential_bits(lib, tuning, grid):
+    M, H, F, act = 600, 512, 1536, 1
+    d = I.make_inputs(M, H, F, act, seed=77)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, tuning)
+    info = plan.info()
+    assert info["p1"] == tuning.get("p1", 0)
+    if "lag" in tuning and tuning["lag"] > 0:
+        assert info["lag"] == tuning["lag"]
+    if tuning.get("lag") == -1:
+        assert info["lag"] == info["items1"]
+    if grid:
+        plan.set_option(B.OPT_GRID, grid)
+    Ys = run(plan, g, B.MODE_SEQUENTIAL).clone()
+    Yp = run(plan, g, B.MODE_TILE_PIPELINED).clone()
+    Yp2 = run(plan, g, B.MODE_TILE_PIPELINED)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    assert_bit_equal(Ys, Yp, f"{tuning} grid {grid}")
+    assert_bit_equal(Ys, Yp2, f"{tuning} grid {grid}, second run")
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
+    assert_matches_oracle(Yp, ref, f"{tuning}")
+    plan.close()
+
+
+def test_role_split_needs_both_roles(lib):
+    with pytest.raises(B.Mlp2Error):
+        B.Plan(64, 128, 128, 1, {"p1": 12})  # not a multiple of 8
+    plan = B.Plan(600, 512, 1536, 1, {"p1": 32})
+    with pytest.raises(B.Mlp2Error):
+        plan.set_option(B.OPT_GRID, 1)  # one work-group cannot hold both roles
+    with pytest.raises(B.Mlp2Error):
+        plan.set_option(B.OPT_GRID, 32)  # 32 work-groups: all of them in the GEMM1 role
+    plan.set_option(B.OPT_GRID, 40)  # 32 + 8
     plan.close()
 
 

@@ -152,17 +152,26 @@ def violations(body):
 
 
 def m0_misuse(body):
-    """M0 is written only to address a direct-to-LDS load, immediately before it."""
+    """M0 holds only the LDS addresses of the direct-to-LDS loads.
+
+    The loads take it as an asm operand bound to M0, so the compiler writes
+    the register itself (s_mov / s_add into m0) before each load; no other
+    instruction may name M0 as a source (an indexed move or a second use
+    would mean the compiler kept a value of its own there), and every kernel
+    that issues direct-to-LDS loads writes M0."""
     bad = []
     lines = [l.split(";")[0].strip() for l in body.splitlines()]
     lines = [l for l in lines if l and not l.startswith(".") and not l.startswith("#")]
-    for i, s in enumerate(lines):
-        if re.match(r"s_\w+\s+m0\b", s):
-            nxt = lines[i + 1] if i + 1 < len(lines) else ""
-            if not nxt.startswith("global_load_lds"):
-                bad.append(f"m0 written by '{s}' not followed by a direct-to-LDS load")
-        if re.search(r"\bm0\b", s) and not re.match(r"s_mov_b32\s+m0,", s):
+    writes = 0
+    for s in lines:
+        if re.match(r"s_\w+\s+m0,", s):
+            writes += 1
+            if re.search(r",.*\bm0\b", s):
+                bad.append(f"m0 read by '{s}'")
+        elif re.search(r"\bm0\b", s):
             bad.append(f"m0 used by '{s}'")
+    if any(l.startswith("global_load_lds") for l in lines) and writes == 0:
+        bad.append("direct-to-LDS loads without an M0 write")
     return bad
 
 
