@@ -498,8 +498,21 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
     pref[0] = 128; pref[1] = 64; pref[2] = 64; pref[3] = 4;
   } else if (M <= 256) {
     pref[0] = 256; pref[1] = nb == 1 ? 128 : 64; pref[2] = 128; pref[3] = 3;
+    // Gated: 128 columns of each of Wg and Wu per tile over eight waves, GEMM2
+    // as two 128-column halves (two-stage ring): half the activation bytes per
+    // weight byte of the four-wave 64-column tile (70B gated MLP, 256 rows:
+    // 600 -> 410 us pipelined).
+    if (nb == 2 && F % 128 == 0 && H % 256 == 0) {
+      pref[1] = 128; pref[2] = 256; pref[3] = 2; pref[4] = 8;
+    }
   } else {
     pref[0] = 128; pref[1] = 128; pref[2] = 128; pref[3] = 2;
+    // 256 x 256 tiles over eight waves (a quarter of the operand bytes per flop
+    // of 128 x 128) once they fill every CU: Llama-8B prefill 2048 rows
+    // 523 -> 450 us pipelined, 8192 x 8192 weights at 8192 rows 2074 -> 1726 us.
+    if (nb == 1 && F % 256 == 0 && H % 256 == 0 && (int64_t)ceil_div(M, 256) * (F / 256) >= p->num_cus) {
+      pref[0] = 256; pref[1] = 256; pref[2] = 256; pref[3] = 2; pref[4] = 8;
+    }
   }
   // Fallbacks when the preferred tiles do not divide F / H or are not built.
   const int w = pref[4];

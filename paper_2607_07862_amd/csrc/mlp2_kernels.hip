@@ -80,7 +80,8 @@ __device__ __forceinline__ ListPos list_pos(const Args& a, bool roles) {
   return ListPos{1, i, G - n1, a.lists2, 8 + i % a.lists2};
 }
 
-__device__ __forceinline__ Claim make_claim(const Args& a, const ListPos& lp) {
+__device__ __forceinline__ Claim make_claim(const Args& a, bool roles) {
+  const ListPos lp = list_pos(a, roles);
   const int l = lp.i % lp.lists;
   const int skip = lp.role < 0 && l < a.first_static ? (a.first_static - 1 - l) / lp.lists + 1 : 0;
   return Claim{a.ctrl + ctrl_ticket(lp.list), l, lp.lists, skip, 0u};
@@ -267,10 +268,11 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
 // stream-ordered before the plan's next kernel.  Spreading the done counts
 // over the lists keeps the exit atomics, one per work-group, off a single
 // line.
-__device__ __forceinline__ void finish_kernel(const Args& a, const ListPos& lp, uint32_t epoch, bool end_of_run,
+__device__ __forceinline__ void finish_kernel(const Args& a, bool roles, uint32_t epoch, bool end_of_run,
                                               bool wq_run = false, uint32_t wq_epoch = 0) {
   __syncthreads();
   if (threadIdx.x == 0) {
+    const ListPos lp = list_pos(a, roles);
     const int l = lp.i % lp.lists;
     const uint32_t in_list = (uint32_t)((lp.n - 1 - l) / lp.lists + 1);
     const uint32_t old = __hip_atomic_fetch_add(a.ctrl + ctrl_done(lp.list), 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
@@ -362,7 +364,7 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
   if (lp.role < 0 && (int)blockIdx.x < a.first_static) {
     p = (int)blockIdx.x;
   } else {
-    Claim first = make_claim(a, lp);
+    Claim first = make_claim(a, lp.role >= 0);
     first.issue();
     first.park(&s_item);
     __syncthreads();
@@ -375,7 +377,7 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
     TraceAcc tr;
     if constexpr (kTrace) tr.c_start = trace_clock();
     const uint64_t t_start = trace_now();
-    Claim next = make_claim(a, lp);
+    Claim next = make_claim(a, lp.role >= 0);
     uint32_t e;  // order-table entry: item id, bit 31 set for a GEMM2 item
     if constexpr (PHASE == PHASE_PIPELINED) {
       e = lp.role < 0 ? uniform(a.orderp[p]) : lp.role == 0 ? uniform(a.order1[p]) : (uniform(a.order2[p]) | 0x80000000u);
@@ -411,7 +413,7 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
       c_pop = trace_clock();
     }
   }
-  finish_kernel(a, lp, epoch, PHASE != PHASE_GEMM1, PHASE == PHASE_WORKQUEUE, wq_epoch);
+  finish_kernel(a, lp.role >= 0, epoch, PHASE != PHASE_GEMM1, PHASE == PHASE_WORKQUEUE, wq_epoch);
 }
 
 // ------------------------------------------------------------------ dispatch table
@@ -560,10 +562,9 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_mlp2_chain(ChainArgs c) {
   const Args& a = c.a;
   const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
   const int total = a.items1;
-  const ListPos lp = list_pos(a, false);
   int p;
   {
-    Claim first = make_claim(a, lp);
+    Claim first = make_claim(a, false);
     first.issue();
     first.park(&s_item);
     __syncthreads();
@@ -576,7 +577,7 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_mlp2_chain(ChainArgs c) {
     TraceAcc tr;
     if constexpr (kTrace) tr.c_start = trace_clock();
     const uint64_t t_start = trace_now();
-    Claim next = make_claim(a, lp);
+    Claim next = make_claim(a, false);
     const uint32_t e = uniform(a.orderp[p]);
     chain_item<T>(c, (int)(e >> 24), (int)(e & 0xffffffu), epoch, lds, &s_slot, next, &s_item, tr);
     // trace entry: layer << 24 | tile; every launch of a run records into section 0
@@ -584,7 +585,7 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_mlp2_chain(ChainArgs c) {
     __syncthreads();
     p = uniform(s_item);
   }
-  finish_kernel(a, lp, epoch, c.end_of_run != 0);
+  finish_kernel(a, false, epoch, c.end_of_run != 0);
 }
 
 static const void* chain_kernel(int tile) {

@@ -39,9 +39,10 @@ SMALL = [
     (200, 320, 640, 2, None),
     (140, 256, 384, 0, {"splitk1": 2, "splitk2": 3}),
     # 129..256 rows, SwiGLU, H a multiple of 128: the default plan's 256-row
-    # tiles with the 128-column GEMM2 tile run as two 64-column halves
+    # tiles with the GEMM2 tile run as two halves of the GEMM1 tile's width
     (200, 1024, 1024, 2, None),
     (256, 512, 768, 2, None),
+    (200, 384, 640, 2, None),
     # eight-wave work-groups: 256 x 256 tiles (two row blocks, the second ragged),
     # 256-row tiles of 128 columns, GEMM2 as two halves, the gated shapes
     (300, 512, 768, 1, {"waves": 8, "bm": 256, "bn1": 256, "bn2": 256, "stages": 2}),
@@ -63,7 +64,11 @@ def test_small_shapes_against_full_oracle(lib, M, H, F, act, tuning):
     plan = B.Plan(M, H, F, act, tuning)
     if act == 2 and 128 < M <= 256 and H % 128 == 0 and tuning is None:
         info = plan.info()
-        assert (info["bm"], info["bn2"]) == (256, 128), info  # the two-half GEMM2 tile
+        # the GEMM2 tile runs as two halves of the GEMM1 tile's width: eight waves
+        # of 128 + 128 columns where H allows, else four waves of 64 + 64
+        want = (256, 256, 8) if H % 256 == 0 and F % 128 == 0 else (256, 128, 4)
+        assert (info["bm"], info["bn2"], info["waves"]) == want, info
+        assert info["bn2"] == 2 * info["bn1"], info
     Ys, Zs, Yp, Zp = both_modes(plan, g)
     Yq, Zq = workqueue_mode(plan, g)
     ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
