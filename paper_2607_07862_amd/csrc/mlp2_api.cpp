@@ -17,53 +17,10 @@
 
 #include "../../include/mlp2.h"
 #include "mlp2_launch.h"
+#include "mlp2_plan_impl.h"
 
 using mlp2::Args;
 using mlp2::KernelConfig;
-
-struct mlp2_plan_s {
-  int64_t M = 0, H = 0, F = 0;
-  int act = 0;
-  int device = -1;
-  KernelConfig kc{};
-  int Mb = 0, Nb1 = 0, Nb2 = 0;
-  int S1 = 1, S2 = 1, kc1 = 0, kc2 = 0;
-  int items1 = 0, items2 = 0;
-  int grid = 0, grid1 = 0, grid2 = 0, occupancy = 0, num_cus = 0;
-  int grid_override = 0;
-  int max_grid = 0;  // work-groups of every kernel of the plan that fit the device at once
-  int order = MLP2_ORDER_AUTO;
-  int lag = 0;  // pipelined rank-table lag (tuning; 0 = one grid, -1 = after every GEMM1 item)
-  int p1 = 0;   // static GEMM1 share of every 64 work-groups of the pipelined launch (0 = shared roles)
-  uint32_t spin_limit = 1u << 20;
-  int drop_signal = -1;
-  uint64_t* trace = nullptr;  // caller-owned timing buffer (trace builds)
-  int trace_cap = 0;
-  // workspace
-  void* ws = nullptr;
-  size_t ws_bytes = 0;
-  uint16_t* Z = nullptr;
-  float* part1 = nullptr;
-  float* part2 = nullptr;
-  uint32_t* cnt1 = nullptr;
-  uint32_t* cnt2 = nullptr;
-  uint32_t* ready = nullptr;
-  uint32_t* board = nullptr;
-  uint32_t* queue = nullptr;
-  uint32_t* ctrl = nullptr;
-  uint32_t* order1 = nullptr;
-  uint32_t* order2 = nullptr;
-  uint32_t* orderp = nullptr;
-  int64_t lead1 = 0;  // leading ranks of the pipelined table that are GEMM1 items (they never wait)
-  size_t counters_off = 0, counters_bytes = 0;
-  // Row groups (group_rows_for): a grouped plan runs as back-to-back launches
-  // of `group` over whole groups of group_rows rows and of `tail` over the
-  // remaining rows; every launch writes its rows of this plan's Z.
-  int64_t group_rows = 0;
-  mlp2_plan_s* group = nullptr;
-  mlp2_plan_s* tail = nullptr;
-  bool z_external = false;  // a group's plan: Z belongs to the grouped plan
-};
 
 struct mlp2_chain_s {
   int64_t M = 0;
@@ -105,6 +62,14 @@ int fail(int code) {
   g_last_error = code;
   return code;
 }
+
+}  // namespace
+
+namespace mlp2 {
+int record_error(int code) { return fail(code); }
+}  // namespace mlp2
+
+namespace {
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -329,6 +294,24 @@ bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
   return x < y + nb && y < x + na;
 }
 
+// Ranks between a GEMM2 item and the last GEMM1 item it reads in the
+// pipelined rank table (the stage split of a launch whose work-groups take
+// both kinds of item).  A tuning value, or every GEMM2 item after every
+// GEMM1 item (tuning -1, row bands, or a GEMM1 list shorter than two grids:
+// its second round is a partial tail that GEMM2 items should fill rather
+// than delay), else one grid.  Measured over lags of 1, grid/4, grid/2,
+// grid, 2 grids and all GEMM1 first on the five workloads and 8192^2 weights
+// at 4096 rows: a lag below one grid claims GEMM2 items before the GEMM1
+// items they wait for are running (up to 50 % slower); at or beyond one grid
+// all are within a few percent, all-first ahead for the 1.75-round prefill
+// GEMM1 (456 against 465 us) and one grid ahead for two and more rounds.
+int merged_lag(const mlp2_plan_s* p) {
+  const int grid = p->grid_override ? p->grid_override : p->grid;
+  if (p->lag > 0) return p->lag;
+  if (p->lag == -1 || uses_bands(p) || p->items1 < 2 * grid) return p->items1;
+  return grid;
+}
+
 int upload_order(mlp2_plan_s* p) {
   std::vector<uint32_t> ord, ord2, merged;
   build_order(p, ord);
@@ -338,10 +321,7 @@ int upload_order(mlp2_plan_s* p) {
   // then W1 and W2 stream at once and no longer fit the last-level cache
   // together (measured: 30-37 % slower than the sequential mode at 4096 to
   // 32768 rows); the launch then overlaps only the tail of GEMM1.
-  // The lag: a tuning value in ranks, or every GEMM2 item after every GEMM1
-  // item (-1), or by default about one grid (row bands: after every GEMM1 item).
-  const int grid = p->grid_override ? p->grid_override : p->grid;
-  const int lag = p->lag == -1 || uses_bands(p) ? p->items1 : p->lag > 0 ? p->lag : grid;
+  const int lag = merged_lag(p);
   build_merged(p, ord, ord2, lag, merged);
   p->lead1 = 0;
   while (p->lead1 < (int64_t)merged.size() && !(merged[p->lead1] & 0x80000000u)) ++p->lead1;
@@ -464,12 +444,17 @@ mlp2_plan_s* make_grouped(int64_t M, int64_t H, int64_t F, int act, const mlp2_t
   return p;
 }
 
-mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuning_t& tz, int dev,
-                       const hipDeviceProp_t& prop, uint16_t* z_ext) {
+}  // namespace
+
+namespace mlp2 {
+
+// Everything a single-launch plan fixes before it has memory: tiles, split-K
+// factors, grids, the stage split.  No allocation (occupancy queries only).
+int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, const mlp2_tuning_t& tz, int dev,
+                   int num_cus) {
   const int nb = act == MLP2_ACT_SWIGLU ? 2 : 1;
-  auto* p = new mlp2_plan_s();
   p->M = M; p->H = H; p->F = F; p->act = act; p->device = dev;
-  p->num_cus = prop.multiProcessorCount;
+  p->num_cus = num_cus;
 
   // ---- tile choice by regime (each row chosen by measurement on MI355X).
   // Up to 256 rows the plan streams weights: one row block holds every row,
@@ -533,31 +518,20 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
       break;
     }
   }
-  if (!found) {
-    delete p;
-    fail(MLP2_ERR_UNSUPPORTED);
-    return nullptr;
-  }
+  if (!found) return MLP2_ERR_UNSUPPORTED;
   const int bm = p->kc.bm, bn1 = p->kc.bn1, bn2 = p->kc.bn2;
   p->Mb = ceil_div(M, bm);
   // The direct-to-LDS loads address each operand with a 32-bit byte offset
   // from its base: every operand one launch reads (X, Z, each weight matrix)
   // stays below 4 GB.
   const uint64_t lim = (uint64_t)1 << 32;
-  if ((uint64_t)M * H * 2 >= lim || (uint64_t)p->Mb * bm * F * 2 >= lim || (uint64_t)H * F * 2 >= lim) {
-    delete p;
-    fail(MLP2_ERR_UNSUPPORTED);
-    return nullptr;
-  }
+  if ((uint64_t)M * H * 2 >= lim || (uint64_t)p->Mb * bm * F * 2 >= lim || (uint64_t)H * F * 2 >= lim)
+    return MLP2_ERR_UNSUPPORTED;
   p->Nb1 = (int)(F / bn1);
   p->Nb2 = (int)(H / bn2);
   int occ[4] = {0, 0, 0, 0};
   for (int w = 0; w < 4; ++w) {
-    if (mlp2::occupancy(p->kc, w, &occ[w]) != hipSuccess || occ[w] < 1) {
-      delete p;
-      fail(MLP2_ERR_HIP);
-      return nullptr;
-    }
+    if (mlp2::occupancy(p->kc, w, &occ[w]) != hipSuccess || occ[w] < 1) return MLP2_ERR_HIP;
   }
   const int tiles1 = p->Mb * p->Nb1, tiles2 = p->Mb * p->Nb2;
   if (tz.splitk1) {
@@ -580,28 +554,25 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
 
   p->occupancy = occ[2];
   p->max_grid = std::min(std::min(occ[0], occ[1]), std::min(occ[2], occ[3])) * p->num_cus;
-  if (tz.grid > p->max_grid) {
-    delete p;
-    fail(MLP2_ERR_UNSUPPORTED);
-    return nullptr;
-  }
+  if (tz.grid > p->max_grid) return MLP2_ERR_UNSUPPORTED;
   p->grid_override = tz.grid;
   p->grid1 = std::min(occ[0] * p->num_cus, p->items1);
   p->grid2 = std::min(occ[1] * p->num_cus, p->items2);
   p->grid = std::min(std::min(occ[2], occ[3]) * p->num_cus, p->items1 + p->items2);
-  if (!roles_ok(p->p1, tz.grid ? tz.grid : p->grid)) {  // a role split needs work-groups of both roles
-    delete p;
-    fail(MLP2_ERR_UNSUPPORTED);
-    return nullptr;
-  }
-  if (p->items2 >= (1 << 24)) {  // workqueue entries hold a unit id in 24 bits
-    delete p;
-    fail(MLP2_ERR_UNSUPPORTED);
-    return nullptr;
-  }
+  if (!roles_ok(p->p1, tz.grid ? tz.grid : p->grid)) return MLP2_ERR_UNSUPPORTED;  // both roles need work-groups
+  if (p->items2 >= (1 << 24)) return MLP2_ERR_UNSUPPORTED;  // workqueue entries hold a unit id in 24 bits
+  return MLP2_OK;
+}
 
-  // ---- workspace: Z, partials, counters, order table
+// Byte offsets of the workspace parts of a configured plan (Z only when the
+// plan owns it); returns the total size.
+size_t plan_layout(const mlp2_plan_s* p, bool own_z, PlanLayout* L) {
+  const int nb = p->act == MLP2_ACT_SWIGLU ? 2 : 1;
+  const int bm = p->kc.bm, bn1 = p->kc.bn1, bn2 = p->kc.bn2;
+  const int tiles1 = p->Mb * p->Nb1, tiles2 = p->Mb * p->Nb2;
   const int64_t Mpad = (int64_t)p->Mb * bm;
+  const int64_t F = p->F;
+  const bool z_ext = !own_z;
   size_t off = 0;
   const size_t z_off = off;
   if (!z_ext) off = align_up(off + (size_t)Mpad * F * 2, 256);
@@ -630,29 +601,55 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
   off = align_up(off + (size_t)p->items2 * 4, 256);
   const size_t ordp_off = off;
   off = align_up(off + ((size_t)p->items1 + p->items2) * 4, 256);
-  p->ws_bytes = off;
+  *L = PlanLayout{z_off, p1_off, p2_off, c1_off, c2_off, r_off, b_off, q_off, ctrl_off, cnt_off, cnt_end,
+                  ord_off, ord2_off, ordp_off, off};
+  return off;
+}
+
+// Points a configured plan's workspace fields into memory at `b` laid out by L
+// (Z at z_ext when the plan does not own it).
+void bind_plan(mlp2_plan_s* p, char* b, const PlanLayout& L, uint16_t* z_ext) {
+  p->Z = z_ext ? z_ext : (uint16_t*)(b + L.z_off);
+  p->z_external = z_ext != nullptr;
+  p->part1 = p->S1 > 1 ? (float*)(b + L.p1_off) : nullptr;
+  p->part2 = p->S2 > 1 ? (float*)(b + L.p2_off) : nullptr;
+  p->cnt1 = (uint32_t*)(b + L.c1_off);
+  p->cnt2 = (uint32_t*)(b + L.c2_off);
+  p->ready = (uint32_t*)(b + L.r_off);
+  p->board = (uint32_t*)(b + L.b_off);
+  p->queue = (uint32_t*)(b + L.q_off);
+  p->ctrl = (uint32_t*)(b + L.ctrl_off);
+  p->order1 = (uint32_t*)(b + L.ord_off);
+  p->order2 = (uint32_t*)(b + L.ord2_off);
+  p->orderp = (uint32_t*)(b + L.ordp_off);
+  p->counters_off = L.cnt_off;
+  p->counters_bytes = L.cnt_end - L.cnt_off;
+}
+
+}  // namespace mlp2
+
+namespace {
+
+mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuning_t& tz, int dev,
+                       const hipDeviceProp_t& prop, uint16_t* z_ext) {
+  auto* p = new mlp2_plan_s();
+  const int rc = mlp2::configure_plan(p, M, H, F, act, tz, dev, prop.multiProcessorCount);
+  if (rc != MLP2_OK) {
+    delete p;
+    fail(rc);
+    return nullptr;
+  }
+  mlp2::PlanLayout L;
+  p->ws_bytes = mlp2::plan_layout(p, z_ext == nullptr, &L);
   if (hipMalloc(&p->ws, p->ws_bytes) != hipSuccess) {
     delete p;
     fail(MLP2_ERR_HIP);
     return nullptr;
   }
   char* b = (char*)p->ws;
-  p->Z = z_ext ? z_ext : (uint16_t*)(b + z_off);
-  p->z_external = z_ext != nullptr;
-  p->part1 = p->S1 > 1 ? (float*)(b + p1_off) : nullptr;
-  p->part2 = p->S2 > 1 ? (float*)(b + p2_off) : nullptr;
-  p->cnt1 = (uint32_t*)(b + c1_off);
-  p->cnt2 = (uint32_t*)(b + c2_off);
-  p->ready = (uint32_t*)(b + r_off);
-  p->board = (uint32_t*)(b + b_off);
-  p->queue = (uint32_t*)(b + q_off);
-  p->ctrl = (uint32_t*)(b + ctrl_off);
-  p->order1 = (uint32_t*)(b + ord_off);
-  p->order2 = (uint32_t*)(b + ord2_off);
-  p->orderp = (uint32_t*)(b + ordp_off);
-  p->counters_off = cnt_off;
-  p->counters_bytes = cnt_end - cnt_off;
-  if (hipMemset(b + cnt_off, 0, cnt_end - cnt_off) != hipSuccess ||
+  mlp2::bind_plan(p, b, L, z_ext);
+  const int64_t Mpad = (int64_t)p->Mb * p->kc.bm;
+  if (hipMemset(b + L.cnt_off, 0, L.cnt_end - L.cnt_off) != hipSuccess ||
       (!z_ext && hipMemset(p->Z, 0, (size_t)Mpad * F * 2) != hipSuccess) ||
       upload_order(p) != MLP2_OK || hipDeviceSynchronize() != hipSuccess) {
     (void)hipFree(p->ws);
@@ -673,7 +670,7 @@ mlp2_plan_t mlp2_plan(int64_t M, int64_t H, int64_t F, int act, int dtype) {
 
 }  // extern "C"
 
-namespace {
+namespace mlp2 {
 
 // One evaluation of a single-launch plan (each kernel launched once) with
 // its Z rows at Z.
@@ -758,7 +755,7 @@ int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void*
   return MLP2_OK;
 }
 
-}  // namespace
+}  // namespace mlp2
 
 extern "C" {
 
@@ -774,16 +771,16 @@ int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void*
   if (hipGetDevice(&dev) != hipSuccess || dev != p->device) return fail(MLP2_ERR_DEVICE);
 
   hipStream_t s = (hipStream_t)stream;
-  if (!p->group) return launch_plan(p, X, W1, W2, Y, p->Z, s, mode);
+  if (!p->group) return mlp2::launch_plan(p, X, W1, W2, Y, p->Z, s, mode);
   // Row groups, in order on the stream: each group's launches read its rows
   // of X and write its rows of Z and Y.
   const int64_t R = p->group_rows;
   int64_t r0 = 0;
   for (; r0 + R <= p->M; r0 += R) {
-    const int rc = launch_plan(p->group, (const uint16_t*)X + r0 * p->H, W1, W2, (uint16_t*)Y + r0 * p->H, p->Z + r0 * p->F, s, mode);
+    const int rc = mlp2::launch_plan(p->group, (const uint16_t*)X + r0 * p->H, W1, W2, (uint16_t*)Y + r0 * p->H, p->Z + r0 * p->F, s, mode);
     if (rc != MLP2_OK) return rc;
   }
-  if (p->tail) return launch_plan(p->tail, (const uint16_t*)X + r0 * p->H, W1, W2, (uint16_t*)Y + r0 * p->H, p->Z + r0 * p->F, s, mode);
+  if (p->tail) return mlp2::launch_plan(p->tail, (const uint16_t*)X + r0 * p->H, W1, W2, (uint16_t*)Y + r0 * p->H, p->Z + r0 * p->F, s, mode);
   return MLP2_OK;
 }
 
@@ -854,10 +851,7 @@ int mlp2_plan_info(mlp2_plan_t p, mlp2_info_t* out) {
   out->workspace_bytes = (int64_t)p->ws_bytes;
   out->spin_limit = p->spin_limit;
   out->waves = p->kc.waves;
-  {
-    const int grid = p->grid_override ? p->grid_override : p->grid;
-    out->lag = p->lag == -1 || uses_bands(p) ? p->items1 : p->lag > 0 ? p->lag : grid;
-  }
+  out->lag = merged_lag(p);
   out->p1 = p->p1;
   return MLP2_OK;
 }
