@@ -240,6 +240,28 @@ int mlp2_set_option(mlp2_plan_t plan, int key, int64_t value);
  * or MLP2_ERR_UNSUPPORTED. */
 int mlp2_trace_attach(mlp2_plan_t plan, void* buffer, int records_per_group);
 
+/* ---- Allocation-free run (for callers that cannot allocate device memory:
+ * code under graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Plans and enqueues one evaluation of Y = act(X . W1) . W2 in
+ * `mode` on `stream`, exactly as mlp2_plan + mlp2_run would with the
+ * column-first tile order and every GEMM2 item after every GEMM1 item in the
+ * pipelined rank table, and calls no allocating routine: every piece of
+ * workspace (Z, split-K partials, counters, rank tables) lives in a static
+ * device array of 64 MiB that the library holds on each GPU it runs on until
+ * the process ends.  Arguments and layouts as mlp2_plan / mlp2_run (device
+ * pointers, row-major bf16, 16-byte aligned; the caller owns X, W1, W2, Y).
+ * Returns MLP2_OK once enqueued; MLP2_ERR_UNSUPPORTED when the plan's
+ * workspace exceeds the 64 MiB (e.g. the 70B gated MLP at 256 rows or a
+ * prefill batch: use mlp2_plan for those), and the codes of mlp2_plan and
+ * mlp2_run otherwise; mlp2_last_error() records the code.  Every call on a
+ * device shares that device's array and starts by clearing its counters (a
+ * small fill kernel on `stream`, no memset node), so calls that overlap on one
+ * device (two streams or two host threads) race and give undefined results.
+ * A flag wait that times out is not reported here (there is no plan to check):
+ * the kernels still exit, and mlp2_run + mlp2_check diagnose such a case. */
+int mlp2_run_noalloc(int64_t M, int64_t H, int64_t F, int act, int dtype, const void* X, const void* W1,
+                     const void* W2, void* Y, void* stream, int mode);
+
 /* ---- GEMM chain: the producer / consumer relation at every layer boundary
  * (Sec. III-A applied to a chain of GEMMs whose middle kernels both consume
  * and produce).  Z_0 = X [M, D_0]; Z_l = act(Z_{l-1} . W_l) for l < L;

@@ -43,6 +43,7 @@ EXPORTS = (
     "mlp2_chain_destroy",
     "mlp2_chain_grid",
     "mlp2_chain_trace_attach",
+    "mlp2_run_noalloc",
 )
 
 
@@ -162,6 +163,9 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.mlp2_chain_trace_attach.argtypes = [P, P, ctypes.c_int]
     lib.mlp2_chain_destroy.restype = None
     lib.mlp2_chain_destroy.argtypes = [P]
+    lib.mlp2_run_noalloc.restype = ctypes.c_int
+    lib.mlp2_run_noalloc.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                     P, P, P, P, P, ctypes.c_int]
     _lib = lib
     return lib
 
@@ -292,6 +296,29 @@ def _hip_memcpy_d2d(dst: int, src: int, nbytes: int) -> None:
     rc = _hip.hipMemcpy(dst, src, nbytes, 3)  # hipMemcpyDeviceToDevice
     if rc != 0:
         raise RuntimeError(f"hipMemcpy failed ({rc})")
+
+
+def run_noalloc(X, W1, W2, Y, act: int, mode, stream=None) -> None:
+    """``mlp2_run_noalloc``: one evaluation with the library's static device
+    workspace (no allocation; shapes from X [M,H] and W1 [H,F] / [2,H,F])."""
+    import torch
+
+    lib = load()
+    M, H = int(X.shape[0]), int(X.shape[1])
+    F = int(W1.shape[-1])
+    n1 = 2 if act == ACT_SWIGLU else 1
+    dev = X.device
+    _check_tensor(X, "X", M * H, dev)
+    _check_tensor(W1, "W1", n1 * H * F, dev)
+    _check_tensor(W2, "W2", F * H, dev)
+    _check_tensor(Y, "Y", M * H, dev)
+    mode = MODES.get(mode, mode)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    rc = lib.mlp2_run_noalloc(M, H, F, int(act), DTYPE_BF16, _ptr(X), _ptr(W1), _ptr(W2), _ptr(Y), sp, int(mode))
+    if rc != OK:
+        raise Mlp2Error(rc, "mlp2_run_noalloc")
 
 
 class ChainPlan:

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB_NAME = "libmlp2.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
-SOURCES = ["mlp2_kernels.hip", "mlp2_api.cpp"]
+SOURCES = ["mlp2_kernels.hip", "mlp2_api.cpp", "mlp2_noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed fp32 VALU ops are turned off for all device code.  The atomic
