@@ -2,34 +2,40 @@
 """Latency of the two-layer MLP Y = act(X W1) W2 on one MI355X, in each mode.
 
 A step is one ``mlp2_run`` (the whole hot path: GEMM1 + activation + ready
-signals + GEMM2) over one batch of synthetic inputs already resident in HBM.
-W warm-up steps, then exactly K back-to-back steps of the tile-pipelined mode
-timed between a synchronise on each side; ``value`` is that block's mean
-latency per step.  Beside it the line carries:
+signals + GEMM2) over one batch of synthetic input already resident in HBM.
+The headline workload is the largest single-GPU configuration, the 70B gated
+MLP (256 x 8192 x 28672, SwiGLU, seed 3).  W warm-up steps, then exactly K
+back-to-back steps of the tile-pipelined mode timed between a synchronise on
+each side; ``value`` is that block's mean latency per step, which is the
+average duration of the pipelined kernel (one launch per step, HIP events on
+the stream it is launched on).  Beside it the line carries:
 
 * the sequential mode's latency: the mean of equal blocks timed just before
-  and just after the pipelined one;
-* the workqueue mode's (the paper's scoreboard-and-queue scheduling of GEMM2
-  units), same block timing;
-* cold latencies of the pipelined and sequential modes (a 1 GiB read evicts
-  the L2s and the 256 MB MALL before each timed run, modes interleaved);
-* both modes timed run by run in alternating order (medians, p10/p90);
-* the roofline fraction of the dominant kernel (the pipelined launch, timed
-  with HIP events on the stream it is launched on), HBM traffic from
-  committed rocprofv3 counter summaries when they match the current kernel
-  sources, and what the GPU attains outside the library (a 4 GiB read-only
-  stream, an 8192^3 hipBLASLt GEMM) as context for the fractions, which stay
-  against the published peaks;
-* a table of the modes on every MLP workload, beside eager PyTorch on the
-  same inputs (hipBLASLt GEMMs plus an activation kernel) as a reference;
-* the fp64 CPU oracle timed on a bounded sample of the headline workload;
+  and just after the pipelined one; the workqueue mode's; a repeat of the
+  pipelined block and the drift between the two;
+* cold latencies of both modes (a 1 GiB read evicts the L2s and the 256 MB
+  MALL before each timed run, modes interleaved) and the cold roofline
+  fraction; both modes timed run by run in alternating order (medians);
+* the roofline of the pipelined launch (algorithmic bytes or flops over its
+  duration, against the published peak) with the HBM traffic per launch from
+  the committed rocprofv3 counter summary of that workload while it matches
+  the current kernel sources, and what the GPU attains outside the library
+  (a 4 GiB read-only stream, an 8192^3 hipBLASLt GEMM) as context;
+* every MLP workload on its own seeded inputs (the seeds of its
+  configuration): both modes blocked, interleaved and cold, eager PyTorch on
+  the same inputs (hipBLASLt GEMMs plus an activation kernel), and the same
+  roofline object with traffic;
+* the paper's micro-batching comparison on one GPU: 8192 x 8192 weights at
+  8192 and 16384 rows, chunks of rows in a two-stream stage pipeline captured
+  in a HIP graph, chunk sizes swept, beside the one-launch pipelined and
+  sequential modes (graph-captured too);
+* the fp64 CPU oracle timed on this host (one full evaluation of the
+  headline workload when it fits the budget), with the host's CPU count and
+  the BLAS thread count;
 * with ``--paper-shapes``, the paper's own workload (8192 x 8192 weights,
   no activation, M = 1024 ... 32768) in every mode, beside eager PyTorch;
 * with ``--chain``, the GEMM chain (4 layers of 8192 x 8192, GELU between,
-  M from ``--chain-rows``) in both modes, beside eager PyTorch;
-* with ``--microbatch``, the sequential mode in micro-batches of rows (the
-  plan's row groups; chunk sizes 1024 ... 8192) beside the pipelined mode,
-  on the paper's shapes at 8192 and 16384 rows.
+  M from ``--chain-rows``) in both modes, beside eager PyTorch.
 
 Only ``--gpus 1`` is supported: the build targets a single GPU.
 """
@@ -84,7 +90,11 @@ def bound_of(w) -> str:
     return "mfma" if w.alg_flops() / w.alg_bytes() > BF16_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3 else "hbm"
 
 
-def roofline(w, us: float) -> dict:
+def roofline(w, us: float, key: str = None) -> dict:
+    """The roofline object of one workload's pipelined launch taking `us` µs:
+    algorithmic bytes (or flops) per launch over the launch time, against the
+    published peak; HBM traffic per launch from the committed counter summary
+    of that workload when it matches the current kernel sources (else null)."""
     if bound_of(w) == "hbm":
         achieved = w.alg_bytes() / (us * 1e-6) / 1e9
         r = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
@@ -92,6 +102,7 @@ def roofline(w, us: float) -> dict:
         achieved = w.alg_flops() / (us * 1e-6) / 1e12
         r = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
     r["frac"] = round(achieved / r["peak"], 4)
+    r["traffic"] = measured_traffic(key) if key else None
     return r
 
 
@@ -173,45 +184,113 @@ def chain_row(B, M: int, steps: int, iters: int) -> dict:
     }
 
 
-MICROBATCH_ROWS = (1024, 2048, 4096, 8192)
+# Micro-batching legs: rows of the paper's 8192 x 8192 shapes and the chunk sizes swept at each.
+MICROBATCH = {"paper_m8192": (1024, 2048, 4096), "paper_m16384": (2048, 4096, 8192)}
 
 
-def microbatch_row(B, I, key: str, iters: int) -> dict:
-    """The paper's comparison on one GPU: the sequential mode run in
-    micro-batches of rows (the plan's row groups: back-to-back launches over
-    row chunks, each the whole two-kernel sequence) for several chunk sizes,
-    beside the default plan's pipelined and sequential runs; medians of
-    `iters` runs of each, timed one by one in alternating order."""
+def _graph_of(fn):
+    """A HIP graph holding whatever `fn(stream)` enqueues, captured on a side stream."""
+    import torch
+
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(graph, stream=cap):
+        fn(cap)
+    torch.cuda.synchronize()
+    return graph
+
+
+def _replay_us(graphs: dict, replays: int) -> dict:
+    """Median µs per replay of each graph, graphs replayed in alternating order."""
+    import torch
+
+    for gr in graphs.values():
+        for _ in range(3):
+            gr.replay()
+    torch.cuda.synchronize()
+    times = {k: [] for k in graphs}
+    for _ in range(replays):
+        for k, gr in graphs.items():
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            gr.replay()
+            b.record()
+            b.synchronize()
+            times[k].append(a.elapsed_time(b) * 1e3)
+    return {k: statistics.median(v) for k, v in times.items()}
+
+
+def microbatch_row(B, I, key: str, chunks, replays: int) -> dict:
+    """The paper's headline comparison (Sec. IV-A: micro-batched execution,
+    the chunk size swept and the best kept, the baseline captured in a graph)
+    on one GPU.  The rows are cut into chunks of c rows, one plan per chunk;
+    chunk i's GEMM1 (the STAGE1 launch) runs on one stream while chunk i-1's
+    GEMM2 (STAGE2) runs on a second stream of the same priority, each GEMM2
+    ordered after its chunk's GEMM1 by an event, and the whole sequence is
+    captured in a HIP graph.  Beside it, one launch over all rows in the
+    pipelined and in the sequential mode, each also graph-captured; every
+    graph is replayed in alternating order, medians of `replays` replays.
+    Inputs are drawn on the device (timing does not depend on the values);
+    the micro-batched Y is checked against the one-launch sequential Y."""
     import torch
 
     w = I.WORKLOADS[key]
     g = device_random_inputs(w)
-    Y = torch.empty(w.M, w.H, dtype=torch.bfloat16, device="cuda")
-    plans = {"pipelined": (B.Plan(w.M, w.H, w.F, w.act), B.MODE_TILE_PIPELINED),
-             "sequential": (B.Plan(w.M, w.H, w.F, w.act), B.MODE_SEQUENTIAL)}
-    for r in MICROBATCH_ROWS:
-        if r < w.M:
-            plans[f"sequential_microbatch_{r}"] = (B.Plan(w.M, w.H, w.F, w.act, {"row_group": r}), B.MODE_SEQUENTIAL)
-    for plan, mode in plans.values():
-        for _ in range(3):
-            plan.run(g["X"], g["W1"], g["W2"], Y, mode)
-    torch.cuda.synchronize()
-    times = {k: [] for k in plans}
-    for _ in range(iters):
-        for k, (plan, mode) in plans.items():
-            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            s.record()
-            plan.run(g["X"], g["W1"], g["W2"], Y, mode)
-            e.record()
-            e.synchronize()
-            times[k].append(s.elapsed_time(e) * 1000)
-    for plan, _ in plans.values():
+    X, W1, W2 = g["X"], g["W1"], g["W2"]
+    plans, graphs, outs = [], {}, {}
+
+    def whole(mode):
+        plan = B.Plan(w.M, w.H, w.F, w.act)
+        plans.append(plan)
+        Y = torch.empty(w.M, w.H, dtype=torch.bfloat16, device="cuda")
+        outs[mode] = Y
+        return _graph_of(lambda s: plan.run(X, W1, W2, Y, mode, stream=s))
+
+    graphs["pipelined"] = whole(B.MODE_TILE_PIPELINED)
+    graphs["sequential"] = whole(B.MODE_SEQUENTIAL)
+    for c in chunks:
+        if w.M % c or c >= w.M:
+            continue
+        cp = [B.Plan(c, w.H, w.F, w.act) for _ in range(w.M // c)]
+        plans.extend(cp)
+        Y = torch.empty(w.M, w.H, dtype=torch.bfloat16, device="cuda")
+        outs[c] = Y
+
+        def chunked(s, cp=cp, Y=Y, c=c):
+            s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+            s1.wait_stream(s)
+            s2.wait_stream(s)
+            for i, plan in enumerate(cp):
+                r = slice(i * c, (i + 1) * c)
+                plan.run(X[r], W1, W2, Y[r], B.MODE_STAGE1, stream=s1)
+                ev = torch.cuda.Event()
+                ev.record(s1)
+                s2.wait_event(ev)
+                plan.run(X[r], W1, W2, Y[r], B.MODE_STAGE2, stream=s2)
+            s.wait_stream(s1)
+            s.wait_stream(s2)
+
+        graphs[f"microbatch_{c}"] = _graph_of(chunked)
+    t = _replay_us(graphs, replays)
+    for plan in plans:
         assert plan.check() == B.OK
         plan.close()
-    row = {k: round(statistics.median(v), 2) for k, v in times.items()}
-    micro = min((v, k) for k, v in row.items() if k.startswith("sequential_microbatch"))
+    ref = outs[B.MODE_SEQUENTIAL].float()
+    scale = ref.abs().max().item()
+    row = {"M": w.M, "how": "graph replays, alternating order, medians; micro-batches: STAGE1 and STAGE2 of chunk "
+                            "plans on two streams ordered by events"}
+    row.update({k: round(v, 2) for k, v in t.items()})
+    errs = {}
+    for c in chunks:
+        if c in outs:
+            errs[str(c)] = round((outs[c].float() - ref).abs().max().item() / scale, 6)
+    row["microbatch_max_rel_diff_vs_sequential"] = errs
+    micro = min((v, k) for k, v in t.items() if k.startswith("microbatch_"))
     row["best_microbatch"] = micro[1]
-    row["pipelined_gain_vs_best_microbatch_pct"] = round((micro[0] - row["pipelined"]) / micro[0] * 100, 1)
+    row["pipelined_gain_vs_best_microbatch_pct"] = round((micro[0] - t["pipelined"]) / micro[0] * 100, 1)
+    row["pipelined_gain_vs_sequential_pct"] = round((t["sequential"] - t["pipelined"]) / t["sequential"] * 100, 1)
+    del g, X, W1, W2, outs
     return row
 
 
@@ -225,7 +304,8 @@ def torch_eager_us(w, g, steps):
 
     X, W2 = g["X"], g["W2"]
     if w.gated:
-        W1 = torch.cat([g["W1"][: w.H], g["W1"][w.H :]], dim=1)  # [H, 2F]: gate columns, then up columns
+        W1v = g["W1"].reshape(2, w.H, w.F)
+        W1 = torch.cat([W1v[0], W1v[1]], dim=1)  # [H, 2F]: gate columns, then up columns
 
         def step():
             gu = X @ W1
@@ -375,7 +455,10 @@ def attainable():
 
 
 def cpu_baseline(w, d, budget_s: float):
-    """The oracle as it stands, timed on this host on a bounded sample of the workload."""
+    """The oracle as it stands, timed on this host: one full evaluation of the
+    workload (every output row, the weights decoded once inside the call) when
+    a first 32-row call predicts it fits the budget, else as many 32-row calls
+    as fit (each decodes the weights again) scaled to all rows."""
     import numpy as np
 
     from oracle import mlp2_oracle as O
@@ -384,49 +467,105 @@ def cpu_baseline(w, d, budget_s: float):
     try:
         from threadpoolctl import threadpool_info
 
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+        blas = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] + [1])
     except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
+        blas = None
     X, W1, W2 = I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"])
-    # Sample: row blocks of the workload, as many as fit the time budget
-    # (each evaluation decodes the weights and runs both fp64 GEMMs).
     rows_per = min(w.M, 32)
-    times, rows_done = [], 0
+    t0 = time.perf_counter()
+    O.mlp2(X, W1, W2, w.M, w.H, w.F, w.act, rows=np.arange(rows_per))
+    t_first = time.perf_counter() - t0
+    host = {"cpu_count": os.cpu_count(), "blas_threads": blas}
+    if t_first * max(1.0, w.M / rows_per) <= budget_s or w.M <= rows_per:
+        t0 = time.perf_counter()
+        O.mlp2(X, W1, W2, w.M, w.H, w.F, w.act)
+        t_full = time.perf_counter() - t0
+        return {"value": round(t_full * 1e6, 1), "unit": "us", "cores": int(blas or os.cpu_count() or 1),
+                "kind": "oracle", **host,
+                "sample": f"one full evaluation of {w.name} ({w.M} rows; fp64 numpy, weights decoded once in the call)"}
+    times, rows_done = [t_first], rows_per
     t_all = time.perf_counter()
-    while True:
-        rows = np.arange(rows_done % w.M, rows_done % w.M + rows_per) % w.M
+    while time.perf_counter() - t_all < budget_s and rows_done < w.M:
+        rows = np.arange(rows_done, min(w.M, rows_done + rows_per))
         t0 = time.perf_counter()
         O.mlp2(X, W1, W2, w.M, w.H, w.F, w.act, rows=rows)
         times.append(time.perf_counter() - t0)
-        rows_done += rows_per
-        if time.perf_counter() - t_all > budget_s or rows_done >= 4 * w.M:
-            break
-    per_row = sum(times) / rows_done
-    return {
-        "value": round(per_row * w.M * 1e6, 1),
-        "unit": "us",
-        "cores": int(cores),
-        "kind": "oracle",
-        "sample": f"{rows_done} output rows of {w.name} in {len(times)} calls of {rows_per} rows (fp64 numpy, "
-        f"weights decoded per call); value = measured time per row x M={w.M}",
+        rows_done += len(rows)
+    return {"value": round(sum(times) / rows_done * w.M * 1e6, 1), "unit": "us",
+            "cores": int(blas or os.cpu_count() or 1), "kind": "oracle", **host,
+            "sample": f"{rows_done} output rows of {w.name} in {len(times)} calls of up to {rows_per} rows (fp64 "
+                      f"numpy, weights decoded per call), scaled to M={w.M}"}
+
+
+def table_row(B, I, key: str, stream, steps: int, iters: int, cold_iters: int, flush, tuning=None) -> dict:
+    """One workload on its seeded inputs: both modes and the workqueue mode
+    (blocks of `steps` runs), both modes run by run in alternating order
+    (`iters` each, medians), cold medians (`cold_iters` each, a 1 GiB read
+    before every run), eager PyTorch on the same inputs, and the roofline of
+    the pipelined launch with its counter-measured HBM traffic."""
+    import torch
+
+    wk = I.WORKLOADS[key]
+    gk = {k: v.to("cuda") for k, v in I.workload_inputs(wk).items()}
+    rr = Runner(B, wk, gk, tuning, stream)
+    for _ in range(20):
+        rr.run(B.MODE_TILE_PIPELINED)
+        rr.run(B.MODE_SEQUENTIAL)
+        rr.run(B.MODE_WORKQUEUE)
+    s_before = rr.block(B.MODE_SEQUENTIAL, steps)
+    p_us = rr.block(B.MODE_TILE_PIPELINED, steps)
+    s_us = (s_before + rr.block(B.MODE_SEQUENTIAL, steps)) / 2
+    q_us = rr.block(B.MODE_WORKQUEUE, steps)
+    ivk = rr.interleaved(iters)
+    mp, ms = statistics.median(ivk[B.MODE_TILE_PIPELINED]), statistics.median(ivk[B.MODE_SEQUENTIAL])
+    cold = rr.cold([B.MODE_TILE_PIPELINED, B.MODE_SEQUENTIAL], cold_iters, flush) if cold_iters else None
+    rr.check()
+    inf = rr.info
+    rr.close()
+    te = torch_eager_us(wk, gk, steps)
+    del gk
+    torch.cuda.empty_cache()
+    rf = roofline(wk, p_us, key)
+    row = {
+        "pipelined_us": round(p_us, 2),
+        "sequential_us": round(s_us, 2),
+        "gain_pct": round((s_us - p_us) / s_us * 100, 1),
+        "workqueue_us": round(q_us, 2),
+        "interleaved_median_us": {"pipelined": round(mp, 2), "sequential": round(ms, 2),
+                                  "gain_pct": round((ms - mp) / ms * 100, 1)},
+        "torch_eager_us": round(te, 2),
+        "roofline": rf,
+        "hbm_frac": round(wk.alg_bytes() / (p_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+        "mfma_frac": round(wk.alg_flops() / (p_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
+        "tiles": {k: inf[k] for k in ("bm", "bn1", "splitk1", "bn2", "splitk2", "stages", "waves", "grid_pipelined",
+                                      "lag")},
+        "seed": wk.seed,
     }
+    if cold:
+        cp, cs = statistics.median(cold[B.MODE_TILE_PIPELINED]), statistics.median(cold[B.MODE_SEQUENTIAL])
+        row["cold_median_us"] = {"pipelined": round(cp, 2), "sequential": round(cs, 2),
+                                 "gain_pct": round((cs - cp) / cs * 100, 1)}
+        row["cold_roofline_frac"] = roofline(wk, cp)["frac"]
+    return row
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=100, help="untimed warm-up steps (each mode once per step); clocks settle before the timed block")
-    ap.add_argument("--workload", default="l8b_decode")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5, help="untimed warm-up steps of the headline (each mode once per step)")
+    ap.add_argument("--workload", default="l70b_gated",
+                    help="headline workload (default: the largest single-GPU configuration, the 70B gated MLP)")
     ap.add_argument("--tuning", default="", help="JSON dict of mlp2_tuning_t fields")
-    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--cpu-budget", type=float, default=60.0,
+                    help="longest the CPU oracle may take; beyond it a row sample is timed and scaled")
     ap.add_argument("--cold-iters", type=int, default=20)
-    ap.add_argument("--interleave-iters", type=int, default=100,
-                    help="warm runs per mode timed one by one in alternating order (0 skips; a third of it per table row)")
+    ap.add_argument("--interleave-iters", type=int, default=60,
+                    help="warm runs per mode timed one by one in alternating order (0 skips; half of it per table row)")
     ap.add_argument("--no-attainable", action="store_true", help="skip the stream and library-GEMM references")
-    ap.add_argument("--microbatch", action="store_true",
-                    help="also time the sequential mode in micro-batches of rows (the paper's comparison, on one GPU) "
-                         "beside the pipelined mode, on the paper's 8192 x 8192 shapes at 8192 and 16384 rows")
+    ap.add_argument("--no-microbatch", action="store_true",
+                    help="skip the micro-batching comparison (8192 x 8192 weights at 8192 and 16384 rows)")
+    ap.add_argument("--microbatch-replays", type=int, default=10)
     ap.add_argument("--chain", action="store_true",
                     help="also time the GEMM chain: 4 layers of 8192 x 8192 weights, GELU between")
     ap.add_argument("--chain-rows", default=",".join(str(m) for m in CHAIN_ROWS),
@@ -486,6 +625,7 @@ def main():
     log(f"timing {args.steps} pipelined steps")
     value = r.block(B.MODE_TILE_PIPELINED, args.steps)
     extra = {}
+    flush = None
     if not args.only_pipelined:
         # sequential blocks on both sides of the pipelined one: a drift of the
         # clocks over the blocks reaches the two modes alike
@@ -499,18 +639,19 @@ def main():
             "sequential_before_after_us": [round(seq_before, 3), round(seq_after, 3)],
             "workqueue_us": round(wq_us, 3),
             "pipelined_repeat_us": round(pipe2, 3),
+            "drift_pct": round((pipe2 - value) / value * 100, 2),
             "gain_vs_sequential_pct": round((seq_us - value) / seq_us * 100, 2),
         }
+        flush = torch.ones(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
         if args.cold_iters > 0:
-            flush = torch.ones(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
             cold = r.cold([B.MODE_TILE_PIPELINED, B.MODE_SEQUENTIAL], args.cold_iters, flush)
-            del flush
             cp, cs = cold[B.MODE_TILE_PIPELINED], cold[B.MODE_SEQUENTIAL]
             extra["cold"] = {
                 "pipelined_median_us": round(statistics.median(cp), 2),
                 "pipelined_p10_p90_us": [round(pct(cp, 0.1), 2), round(pct(cp, 0.9), 2)],
                 "sequential_median_us": round(statistics.median(cs), 2),
                 "sequential_p10_p90_us": [round(pct(cs, 0.1), 2), round(pct(cs, 0.9), 2)],
+                "roofline_frac": roofline(w, statistics.median(cp))["frac"],
                 "iters": args.cold_iters,
                 "flush": "1 GiB device read before each timed run (evicts L2 and the last-level cache), modes interleaved",
             }
@@ -531,64 +672,25 @@ def main():
             log(f"interleaved: pipelined {mp:.2f} us, sequential {ms:.2f} us")
     r.check()
     info = r.info
-    roof = roofline(w, value)
-    roof["traffic"] = measured_traffic(args.workload)
+    roof = roofline(w, value, args.workload)
     roof["kernel"] = "k_mlp2 pipelined launch (one per step)"
     r.close()
+    del g
+    torch.cuda.empty_cache()
 
-    # ---- every workload: both modes (device-drawn inputs of the same shapes)
+    # ---- every workload on its seeded inputs
     table = {}
     if not args.no_table and not args.only_pipelined:
         for key in I.WORKLOAD_ORDER:
-            wk = I.WORKLOADS[key]
-            steps = max(10, args.steps // 2)
-            iters = max(10, args.interleave_iters // 3)
-            if key == args.workload:
-                rr_p, rr_s, rr_q, inf = value, extra["sequential_us"], extra["workqueue_us"], info
-                te = torch_eager_us(wk, g, steps)
-                iv = extra.get("interleaved")
-                med = (iv["pipelined_median_us"], iv["sequential_median_us"]) if iv else None
-            else:
-                gk = device_random_inputs(wk)
-                rr = Runner(B, wk, gk, None, stream)
-                for _ in range(30):
-                    rr.run(B.MODE_TILE_PIPELINED)
-                    rr.run(B.MODE_SEQUENTIAL)
-                    rr.run(B.MODE_WORKQUEUE)
-                rr_p = rr.block(B.MODE_TILE_PIPELINED, steps)
-                rr_s = rr.block(B.MODE_SEQUENTIAL, steps)
-                rr_q = rr.block(B.MODE_WORKQUEUE, steps)
-                ivk = rr.interleaved(iters)
-                med = (statistics.median(ivk[B.MODE_TILE_PIPELINED]), statistics.median(ivk[B.MODE_SEQUENTIAL]))
-                rr.check()
-                inf = rr.info
-                rr.close()
-                te = torch_eager_us(wk, gk, steps)
-                del gk
-                torch.cuda.empty_cache()
-            rf = roofline(wk, rr_p)
-            row = {
-                "pipelined_us": round(rr_p, 2),
-                "sequential_us": round(rr_s, 2),
-                "gain_pct": round((rr_s - rr_p) / rr_s * 100, 1),
-                "workqueue_us": round(rr_q, 2),
-                "torch_eager_us": round(te, 2),
-                "bound": rf["bound"],
-                "frac": rf["frac"],
-                "hbm_frac": round(wk.alg_bytes() / (rr_p * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
-                "mfma_frac": round(wk.alg_flops() / (rr_p * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
-                "tiles": [inf["bm"], inf["bn1"], inf["splitk1"], inf["bn2"], inf["splitk2"], inf["stages"]],
-            }
-            if med:
-                row["interleaved_median_us"] = {"pipelined": round(med[0], 2), "sequential": round(med[1], 2),
-                                                "gain_pct": round((med[1] - med[0]) / med[1] * 100, 1)}
+            row = table_row(B, I, key, stream, max(10, args.steps), max(10, args.interleave_iters // 2),
+                            max(0, args.cold_iters // 2), flush)
             table[key] = row
             log(f"TABLE {key:12s} {row}")
 
     microbatch = {}
-    if args.microbatch:
-        for key in ("paper_m8192", "paper_m16384"):
-            microbatch[key] = microbatch_row(B, I, key, 15)
+    if not args.no_microbatch and not args.only_pipelined:
+        for key, chunks in MICROBATCH.items():
+            microbatch[key] = microbatch_row(B, I, key, chunks, args.microbatch_replays)
             log(f"MICROBATCH {key:14s} {microbatch[key]}")
             torch.cuda.empty_cache()
 
@@ -630,10 +732,13 @@ def main():
                                           "gain_pct": round((ms - mp) / ms * 100, 1)},
                 "torch_eager_us": round(te, 2),
                 "mfma_frac": round(wk.alg_flops() / (p_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS, 4),
-                "tiles": [inf["bm"], inf["bn1"], inf["splitk1"], inf["bn2"], inf["splitk2"], inf["stages"]],
+                "tiles": [inf["bm"], inf["bn1"], inf["splitk1"], inf["bn2"], inf["splitk2"], inf["stages"],
+                          inf["waves"]],
             }
             paper[key] = row
             log(f"PAPER {key:14s} {row}")
+    del flush
+    torch.cuda.empty_cache()
 
     att = None
     if not args.no_attainable:
@@ -642,16 +747,15 @@ def main():
         roof["frac_of_attainable"] = round(
             roof["achieved"] / (att["hbm_read_GBs"] if roof["bound"] == "hbm" else att["bf16_gemm_TFLOPs"]), 4)
         for key, row in table.items():
-            wk = I.WORKLOADS[key]
-            t = row["pipelined_us"] * 1e-6
-            row["frac_of_attainable"] = round(
-                wk.alg_bytes() / t / 1e9 / att["hbm_read_GBs"] if row["bound"] == "hbm"
-                else wk.alg_flops() / t / 1e12 / att["bf16_gemm_TFLOPs"], 4)
+            rf = row["roofline"]
+            rf["frac_of_attainable"] = round(
+                rf["achieved"] / (att["hbm_read_GBs"] if rf["bound"] == "hbm" else att["bf16_gemm_TFLOPs"]), 4)
 
     cpu = None
     if not args.no_cpu:
         log(f"timing the CPU oracle (budget {args.cpu_budget}s)")
         cpu = cpu_baseline(w, d, args.cpu_budget)
+        log(f"cpu baseline: {cpu}")
 
     out = {
         "metric": METRIC,
@@ -672,9 +776,10 @@ def main():
             "H": w.H,
             "F": w.F,
             "act": ["identity", "gelu_tanh", "swiglu"][w.act],
+            "seed": w.seed,
             "mode": "tile_pipelined",
-            "tiles": {k: info[k] for k in ("bm", "bn1", "splitk1", "bn2", "splitk2", "stages", "items1", "items2",
-                                           "grid_pipelined", "occupancy")},
+            "tiles": {k: info[k] for k in ("bm", "bn1", "splitk1", "bn2", "splitk2", "stages", "waves", "items1",
+                                           "items2", "grid_pipelined", "occupancy", "lag")},
         },
         **extra,
         "alg_bytes": w.alg_bytes(),
@@ -683,9 +788,9 @@ def main():
         "attainable": att,
         "cpu_baseline": cpu,
         "workloads": table,
+        **({"microbatch": microbatch} if microbatch else {}),
         **({"paper_shapes": paper} if paper else {}),
         **({"chain": chain} if chain else {}),
-        **({"microbatch": microbatch} if microbatch else {}),
     }
     print(json.dumps(out), flush=True)
 

@@ -66,7 +66,20 @@ typedef struct mlp2_plan_s* mlp2_plan_t; /* opaque; created by mlp2_plan, freed 
 
 enum mlp2_act { MLP2_ACT_IDENTITY = 0, MLP2_ACT_GELU_TANH = 1, MLP2_ACT_SWIGLU = 2 };
 enum mlp2_dtype { MLP2_DTYPE_BF16 = 0 };
-enum mlp2_mode { MLP2_MODE_SEQUENTIAL = 0, MLP2_MODE_TILE_PIPELINED = 1, MLP2_MODE_WORKQUEUE = 2 };
+/* MLP2_MODE_STAGE1 / MLP2_MODE_STAGE2 enqueue the first or the second kernel
+ * of the sequential mode alone, for callers that schedule the two stages
+ * themselves (e.g. a micro-batch pipeline over chunks of rows on two streams,
+ * one plan per chunk).  The caller orders a plan's STAGE2 after its STAGE1
+ * (same stream, or an event), and the pair after the plan's previous run;
+ * together they compute what MLP2_MODE_SEQUENTIAL computes, bit for bit.
+ * Not for plans run in row groups (MLP2_ERR_UNSUPPORTED). */
+enum mlp2_mode {
+  MLP2_MODE_SEQUENTIAL = 0,
+  MLP2_MODE_TILE_PIPELINED = 1,
+  MLP2_MODE_WORKQUEUE = 2,
+  MLP2_MODE_STAGE1 = 3,
+  MLP2_MODE_STAGE2 = 4
+};
 
 enum mlp2_status {
   MLP2_OK = 0,

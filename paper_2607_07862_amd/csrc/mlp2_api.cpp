@@ -727,13 +727,14 @@ int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void*
   auto statics = [&](int64_t never_wait_lead, int grid) -> int {
     return grid <= p->num_cus ? (int)std::min<int64_t>(grid, never_wait_lead) : 0;
   };
-  if (mode == MLP2_MODE_SEQUENTIAL) {
+  if (mode == MLP2_MODE_SEQUENTIAL || mode == MLP2_MODE_STAGE1 || mode == MLP2_MODE_STAGE2) {
     a.lists = claim_lists(grids[0]);
     a.first_static = statics(p->items1, grids[0]);  // GEMM1 items never wait
     Args a2 = a;
     a2.lists = claim_lists(grids[1]);
     a2.first_static = statics(p->items2, grids[1]);  // nor do GEMM2 items of this mode
-    err = mlp2::launch_sequential(p->kc, a, a2, grids, s);
+    const int stages = mode == MLP2_MODE_STAGE1 ? 1 : mode == MLP2_MODE_STAGE2 ? 2 : 3;
+    err = mlp2::launch_sequential(p->kc, a, a2, grids, s, stages);
   } else if (mode == MLP2_MODE_TILE_PIPELINED) {
     if (p->p1) {  // role split: each role's work-groups claim from lists of their own
       const int n1 = role1_groups(p->p1, gridp);
@@ -761,8 +762,10 @@ extern "C" {
 
 int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void* Y, void* stream, int mode) {
   if (!p || !X || !W1 || !W2 || !Y) return fail(MLP2_ERR_INVALID_ARG);
-  if (mode != MLP2_MODE_SEQUENTIAL && mode != MLP2_MODE_TILE_PIPELINED && mode != MLP2_MODE_WORKQUEUE)
-    return fail(MLP2_ERR_INVALID_ARG);
+  if (mode < MLP2_MODE_SEQUENTIAL || mode > MLP2_MODE_STAGE2) return fail(MLP2_ERR_INVALID_ARG);
+  // The two stages of a grouped plan cannot be enqueued apart: its whole
+  // groups share one plan, whose split-K arrivals count one GEMM1 pass per run.
+  if (p->group && (mode == MLP2_MODE_STAGE1 || mode == MLP2_MODE_STAGE2)) return fail(MLP2_ERR_UNSUPPORTED);
   if (((uintptr_t)X | (uintptr_t)W1 | (uintptr_t)W2 | (uintptr_t)Y) & 15u) return fail(MLP2_ERR_ALIGNMENT);
   const int nb = p->act == MLP2_ACT_SWIGLU ? 2 : 1;
   const size_t xb = (size_t)p->M * p->H * 2, w1b = (size_t)nb * p->H * p->F * 2, w2b = (size_t)p->F * p->H * 2;

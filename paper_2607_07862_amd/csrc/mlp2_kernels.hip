@@ -611,14 +611,19 @@ hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu) {
 }
 
 hipError_t launch_sequential(const KernelConfig& c, const Args& a1, const Args& a2, const int grids[2],
-                             hipStream_t stream) {
+                             hipStream_t stream, int stages) {
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
-  void* args1[] = {const_cast<Args*>(&a1)};
-  hipError_t err = hipLaunchKernel(e->seq1, dim3(grids[0]), dim3(64 * e->waves), args1, 0, stream);
-  if (err != hipSuccess) return err;
-  void* args2[] = {const_cast<Args*>(&a2)};
-  return hipLaunchKernel(e->seq2, dim3(grids[1]), dim3(64 * e->waves), args2, 0, stream);
+  if (stages & 1) {
+    void* args1[] = {const_cast<Args*>(&a1)};
+    const hipError_t err = hipLaunchKernel(e->seq1, dim3(grids[0]), dim3(64 * e->waves), args1, 0, stream);
+    if (err != hipSuccess) return err;
+  }
+  if (stages & 2) {
+    void* args2[] = {const_cast<Args*>(&a2)};
+    return hipLaunchKernel(e->seq2, dim3(grids[1]), dim3(64 * e->waves), args2, 0, stream);
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipStream_t stream) {

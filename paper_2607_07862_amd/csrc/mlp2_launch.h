@@ -18,8 +18,10 @@ bool config_supported(const KernelConfig& c);
 // Resident work-groups per CU of a kernel: which = 0 (GEMM1 phase), 1 (GEMM2 phase), 2 (pipelined),
 // 3 (workqueue).
 hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu);
-// a1 / a2: arguments of the GEMM1 / GEMM2 launch (they differ only in `lists`).
-hipError_t launch_sequential(const KernelConfig& c, const Args& a1, const Args& a2, const int grids[2], hipStream_t stream);
+// a1 / a2: arguments of the GEMM1 / GEMM2 launch (they differ only in `lists`); stages: 1 = the
+// GEMM1 kernel, 2 = the GEMM2 kernel, 3 = both in that order.
+hipError_t launch_sequential(const KernelConfig& c, const Args& a1, const Args& a2, const int grids[2], hipStream_t stream,
+                             int stages);
 hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
 hipError_t launch_workqueue(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
 

@@ -33,11 +33,13 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def short_name(n: str) -> str:
-    m = re.search(r"k_mlp2<mlp2::Tile<(\d+), (\d+), \d+, \d+, (\d+)>, (\d), mlp2::Tile<(\d+), (\d+), \d+, \d+, \d+>, (\d), (\d)>", n)
+    m = re.search(r"k_mlp2<mlp2::Tile<(\d+), (\d+), (\d+), (\d+), (\d+)>, (\d), mlp2::Tile<(\d+), (\d+), \d+, \d+, \d+>, (\d), (\d)>", n)
     if m:
-        phase = ["gemm1", "gemm2", "pipelined", "workqueue"][int(m.group(8))]
-        bn2 = int(m.group(6)) * int(m.group(7))
-        return f"k_mlp2 {phase} (bm {m.group(1)}, bn1 {m.group(2)}, bn2 {bn2}, nb {m.group(4)}, stages {m.group(3)})"
+        phase = ["gemm1", "gemm2", "pipelined", "workqueue"][int(m.group(10))]
+        bn2 = int(m.group(8)) * int(m.group(9))
+        waves = int(m.group(3)) * int(m.group(4))
+        return (f"k_mlp2 {phase} (bm {m.group(1)}, bn1 {m.group(2)}, bn2 {bn2}, nb {m.group(6)}, stages {m.group(5)}, "
+                f"waves {waves})")
     return n if len(n) < 90 else n[:87] + "..."
 
 

@@ -104,6 +104,45 @@ def test_role_split_needs_both_roles(lib):
     plan.close()
 
 
+def test_stage_modes_compose_the_sequential_mode(lib):
+    """STAGE1 then STAGE2 (same stream, or two streams ordered by an event, as a
+    micro-batch pipeline schedules them) give the sequential mode's bits, also
+    interleaved with runs of the other modes; grouped plans refuse them."""
+    M, H, F, act = 300, 512, 1024, 1
+    d = I.make_inputs(M, H, F, act, seed=31)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act)
+    Ys = run(plan, g, B.MODE_SEQUENTIAL).clone()
+    Y1 = torch.empty_like(Ys)
+    run(plan, g, B.MODE_STAGE1, Y=Y1)
+    run(plan, g, B.MODE_STAGE2, Y=Y1)
+    Yp = run(plan, g, B.MODE_TILE_PIPELINED).clone()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1.wait_stream(torch.cuda.current_stream())
+    s2.wait_stream(torch.cuda.current_stream())
+    Y2 = torch.empty_like(Ys)
+    done1 = torch.cuda.Event()
+    with torch.cuda.stream(s1):
+        run(plan, g, B.MODE_STAGE1, Y=Y2, stream=s1)
+        done1.record(s1)
+    s2.wait_event(done1)
+    with torch.cuda.stream(s2):
+        run(plan, g, B.MODE_STAGE2, Y=Y2, stream=s2)
+    s2.synchronize()
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    assert_bit_equal(Ys, Y1, "stages on one stream")
+    assert_bit_equal(Ys, Y2, "stages on two streams")
+    assert_bit_equal(Ys, Yp, "pipelined after the stages")
+    plan.close()
+    grouped = B.Plan(600, 128, 256, 1, {"row_group": 256})
+    gg = device_inputs(I.make_inputs(600, 128, 256, 1, seed=32))
+    with pytest.raises(B.Mlp2Error) as e:
+        run(grouped, gg, B.MODE_STAGE1)
+    assert e.value.code == B.ERR_UNSUPPORTED
+    grouped.close()
+
+
 @pytest.mark.parametrize("act", [0, 1, 2])
 def test_alternating_inputs_and_modes(lib, act):
     M, H, F = 96, 256, 512
@@ -313,7 +352,7 @@ def test_run_argument_errors(lib):
     Y = torch.empty(M, H, dtype=torch.bfloat16, device="cuda")
     s = torch.cuda.current_stream().cuda_stream
     X, W1, W2, y = (t.data_ptr() for t in (g["X"], g["W1"], g["W2"], Y))
-    assert plan.run_raw(X, W1, W2, y, s, 3) == B.ERR_INVALID_ARG
+    assert plan.run_raw(X, W1, W2, y, s, 5) == B.ERR_INVALID_ARG
     assert plan.run_raw(X, W1, W2, y, s, -1) == B.ERR_INVALID_ARG
     assert plan.run_raw(X + 2, W1, W2, y, s, 0) == B.ERR_ALIGNMENT
     assert plan.run_raw(X, W1, W2, X, s, 0) == B.ERR_INVALID_ARG  # Y aliases X

@@ -24,8 +24,10 @@ COPY = "__amd_rocclr_copyBuffer"
 
 
 def test_short_names():
-    assert P.short_name(PIPE) == "k_mlp2 pipelined (bm 128, bn1 64, bn2 64, nb 1, stages 4)"
-    assert P.short_name(GATED2) == "k_mlp2 gemm2 (bm 256, bn1 64, bn2 128, nb 2, stages 3)"
+    assert P.short_name(PIPE) == "k_mlp2 pipelined (bm 128, bn1 64, bn2 64, nb 1, stages 4, waves 4)"
+    assert P.short_name(GATED2) == "k_mlp2 gemm2 (bm 256, bn1 64, bn2 128, nb 2, stages 3, waves 4)"
+    wide = "void mlp2::k_mlp2<mlp2::Tile<256, 256, 2, 4, 2>, 1, mlp2::Tile<256, 256, 2, 4, 2>, 1, 2>(mlp2::Args)"
+    assert P.short_name(wide) == "k_mlp2 pipelined (bm 256, bn1 256, bn2 256, nb 1, stages 2, waves 8)"
     assert P.short_name("x" * 200).endswith("...")
 
 
@@ -69,5 +71,5 @@ def test_stats_table(tmp_path):
     out = str(tmp_path / "stats.md")
     P.stats(argparse.Namespace(dir=str(tmp_path / "kt"), out=out, cmd="the cmd", title="t"))
     text = open(out).read()
-    assert "| k_mlp2 pipelined (bm 128, bn1 64, bn2 64, nb 1, stages 4) | 10 | 75.00 | 70.00 | 90.00 | 61.5 % |" in text
+    assert "| k_mlp2 pipelined (bm 128, bn1 64, bn2 64, nb 1, stages 4, waves 4) | 10 | 75.00 | 70.00 | 90.00 | 61.5 % |" in text
     assert "the cmd" in text
