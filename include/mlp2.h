@@ -66,7 +66,18 @@ typedef struct mlp2_plan_s* mlp2_plan_t; /* opaque; created by mlp2_plan, freed 
 
 enum mlp2_act { MLP2_ACT_IDENTITY = 0, MLP2_ACT_GELU_TANH = 1, MLP2_ACT_SWIGLU = 2 };
 enum mlp2_dtype { MLP2_DTYPE_BF16 = 0 };
-/* MLP2_MODE_STAGE1 / MLP2_MODE_STAGE2 enqueue the first or the second kernel
+/* MLP2_MODE_SENTINEL is the pipelined launch with the Lamport-style
+ * synchronisation the paper discusses as an alternative (Sec. V-A): GEMM1
+ * tiles store the intermediate at device scope with no fence and no ready
+ * counter, and GEMM2 work-groups re-read each K-slice of it while any element
+ * still holds a sentinel (the bf16 pattern 0xFFFF, which the epilogue never
+ * writes: it turns that NaN into 0x7FC0 in every mode).  The plan keeps two
+ * intermediates for it that alternate run by run, each run refilling the other
+ * with sentinels tile by tile, so no run pre-fills a whole buffer.  Same
+ * results as the other modes, bit for bit.  Not for plans run in row groups
+ * (MLP2_ERR_UNSUPPORTED).
+ *
+ * MLP2_MODE_STAGE1 / MLP2_MODE_STAGE2 enqueue the first or the second kernel
  * of the sequential mode alone, for callers that schedule the two stages
  * themselves (e.g. a micro-batch pipeline over chunks of rows on two streams,
  * one plan per chunk).  The caller orders a plan's STAGE2 after its STAGE1
@@ -78,7 +89,8 @@ enum mlp2_mode {
   MLP2_MODE_TILE_PIPELINED = 1,
   MLP2_MODE_WORKQUEUE = 2,
   MLP2_MODE_STAGE1 = 3,
-  MLP2_MODE_STAGE2 = 4
+  MLP2_MODE_STAGE2 = 4,
+  MLP2_MODE_SENTINEL = 5
 };
 
 enum mlp2_status {
@@ -220,7 +232,8 @@ const void* mlp2_intermediate(mlp2_plan_t plan);
 
 /* Debug and failure-injection knobs (tests only).  Keys:
  *   MLP2_OPT_SPIN_LIMIT   polls before a flag wait gives up (default ~1 s of polling)
- *   MLP2_OPT_DROP_SIGNAL  GEMM1 tile index whose ready signal is skipped (-1 = none)
+ *   MLP2_OPT_DROP_SIGNAL  GEMM1 tile index whose ready signal is skipped (-1 = none); in the
+ *                         sentinel mode the tile's intermediate stores are skipped instead
  *   MLP2_OPT_ORDER        enum mlp2_order (rebuilds the order table)
  *   MLP2_OPT_GRID         persistent grid of every launch (0 = automatic; else
  *                         at most the work-groups that fit the device at once)
@@ -258,7 +271,8 @@ int mlp2_trace_attach(mlp2_plan_t plan, void* buffer, int records_per_group);
  * hipMalloc).  Plans and enqueues one evaluation of Y = act(X . W1) . W2 in
  * `mode` on `stream`, exactly as mlp2_plan + mlp2_run would with the
  * column-first tile order and every GEMM2 item after every GEMM1 item in the
- * pipelined rank table, and calls no allocating routine: every piece of
+ * pipelined rank table (mode: sequential, tile_pipelined or workqueue), and
+ * calls no allocating routine: every piece of
  * workspace (Z, split-K partials, counters, rank tables) lives in a static
  * device array of 64 MiB that the library holds on each GPU it runs on until
  * the process ends.  Arguments and layouts as mlp2_plan / mlp2_run (device

@@ -15,9 +15,9 @@ TRACE_LIB_PATH = os.path.join(PKG, "libmlp2_trace.so")
 
 ACT_IDENTITY, ACT_GELU_TANH, ACT_SWIGLU = 0, 1, 2
 DTYPE_BF16 = 0
-MODE_SEQUENTIAL, MODE_TILE_PIPELINED, MODE_WORKQUEUE, MODE_STAGE1, MODE_STAGE2 = 0, 1, 2, 3, 4
+MODE_SEQUENTIAL, MODE_TILE_PIPELINED, MODE_WORKQUEUE, MODE_STAGE1, MODE_STAGE2, MODE_SENTINEL = 0, 1, 2, 3, 4, 5
 MODES = {"sequential": MODE_SEQUENTIAL, "tile_pipelined": MODE_TILE_PIPELINED, "workqueue": MODE_WORKQUEUE,
-         "stage1": MODE_STAGE1, "stage2": MODE_STAGE2}
+         "stage1": MODE_STAGE1, "stage2": MODE_STAGE2, "sentinel": MODE_SENTINEL}
 ORDER_AUTO, ORDER_COLUMN_FIRST, ORDER_ROW_FIRST, ORDER_REVERSED, ORDER_SHUFFLED, ORDER_BANDED = 0, 1, 2, 3, 4, 5
 OPT_SPIN_LIMIT, OPT_DROP_SIGNAL, OPT_ORDER, OPT_GRID = 1, 2, 3, 4
 

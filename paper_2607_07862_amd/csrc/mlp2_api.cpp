@@ -529,8 +529,8 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
     return MLP2_ERR_UNSUPPORTED;
   p->Nb1 = (int)(F / bn1);
   p->Nb2 = (int)(H / bn2);
-  int occ[4] = {0, 0, 0, 0};
-  for (int w = 0; w < 4; ++w) {
+  int occ[5] = {0, 0, 0, 0, 0};
+  for (int w = 0; w < 5; ++w) {
     if (mlp2::occupancy(p->kc, w, &occ[w]) != hipSuccess || occ[w] < 1) return MLP2_ERR_HIP;
   }
   const int tiles1 = p->Mb * p->Nb1, tiles2 = p->Mb * p->Nb2;
@@ -553,12 +553,12 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
   p->items2 = tiles2 * p->S2;
 
   p->occupancy = occ[2];
-  p->max_grid = std::min(std::min(occ[0], occ[1]), std::min(occ[2], occ[3])) * p->num_cus;
+  p->max_grid = std::min(std::min(std::min(occ[0], occ[1]), std::min(occ[2], occ[3])), occ[4]) * p->num_cus;
   if (tz.grid > p->max_grid) return MLP2_ERR_UNSUPPORTED;
   p->grid_override = tz.grid;
   p->grid1 = std::min(occ[0] * p->num_cus, p->items1);
   p->grid2 = std::min(occ[1] * p->num_cus, p->items2);
-  p->grid = std::min(std::min(occ[2], occ[3]) * p->num_cus, p->items1 + p->items2);
+  p->grid = std::min(std::min(std::min(occ[2], occ[3]), occ[4]) * p->num_cus, p->items1 + p->items2);
   if (!roles_ok(p->p1, tz.grid ? tz.grid : p->grid)) return MLP2_ERR_UNSUPPORTED;  // both roles need work-groups
   if (p->items2 >= (1 << 24)) return MLP2_ERR_UNSUPPORTED;  // workqueue entries hold a unit id in 24 bits
   return MLP2_OK;
@@ -566,7 +566,7 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
 
 // Byte offsets of the workspace parts of a configured plan (Z only when the
 // plan owns it); returns the total size.
-size_t plan_layout(const mlp2_plan_s* p, bool own_z, PlanLayout* L) {
+size_t plan_layout(const mlp2_plan_s* p, bool own_z, PlanLayout* L, bool with_zs) {
   const int nb = p->act == MLP2_ACT_SWIGLU ? 2 : 1;
   const int bm = p->kc.bm, bn1 = p->kc.bn1, bn2 = p->kc.bn2;
   const int tiles1 = p->Mb * p->Nb1, tiles2 = p->Mb * p->Nb2;
@@ -601,8 +601,11 @@ size_t plan_layout(const mlp2_plan_s* p, bool own_z, PlanLayout* L) {
   off = align_up(off + (size_t)p->items2 * 4, 256);
   const size_t ordp_off = off;
   off = align_up(off + ((size_t)p->items1 + p->items2) * 4, 256);
+  const size_t zs_off = off;
+  const size_t zs_bytes = with_zs ? align_up((size_t)2 * Mpad * F * 2, 256) : 0;
+  off += zs_bytes;
   *L = PlanLayout{z_off, p1_off, p2_off, c1_off, c2_off, r_off, b_off, q_off, ctrl_off, cnt_off, cnt_end,
-                  ord_off, ord2_off, ordp_off, off};
+                  ord_off, ord2_off, ordp_off, zs_off, zs_bytes, off};
   return off;
 }
 
@@ -622,6 +625,7 @@ void bind_plan(mlp2_plan_s* p, char* b, const PlanLayout& L, uint16_t* z_ext) {
   p->order1 = (uint32_t*)(b + L.ord_off);
   p->order2 = (uint32_t*)(b + L.ord2_off);
   p->orderp = (uint32_t*)(b + L.ordp_off);
+  p->Zs = L.zs_bytes ? (uint16_t*)(b + L.zs_off) : nullptr;
   p->counters_off = L.cnt_off;
   p->counters_bytes = L.cnt_end - L.cnt_off;
 }
@@ -650,6 +654,7 @@ mlp2_plan_s* make_plan(int64_t M, int64_t H, int64_t F, int act, const mlp2_tuni
   mlp2::bind_plan(p, b, L, z_ext);
   const int64_t Mpad = (int64_t)p->Mb * p->kc.bm;
   if (hipMemset(b + L.cnt_off, 0, L.cnt_end - L.cnt_off) != hipSuccess ||
+      (L.zs_bytes && hipMemset(b + L.zs_off, 0xFF, L.zs_bytes) != hipSuccess) ||  // sentinels everywhere
       (!z_ext && hipMemset(p->Z, 0, (size_t)Mpad * F * 2) != hipSuccess) ||
       upload_order(p) != MLP2_OK || hipDeviceSynchronize() != hipSuccess) {
     (void)hipFree(p->ws);
@@ -713,6 +718,9 @@ int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void*
   a.trace_cap = p->trace_cap;
   a.p1 = 0;
   a.lists2 = 0;
+  a.Zs = p->Zs;
+  a.zs_elems = (long)p->Mb * p->kc.bm * p->F;
+  a.Zr = nullptr;
 
   const int go = p->grid_override;
   const int grids[2] = {go ? go : p->grid1, go ? go : p->grid2};
@@ -747,6 +755,11 @@ int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void*
       a.first_static = statics(p->lead1, gridp);
     }
     err = mlp2::launch_pipelined(p->kc, a, gridp, s);
+  } else if (mode == MLP2_MODE_SENTINEL) {
+    if (!p->Zs) return fail(MLP2_ERR_UNSUPPORTED);
+    a.lists = claim_lists(gridp);
+    a.first_static = statics(p->lead1, gridp);
+    err = mlp2::launch_sentinel(p->kc, a, gridp, s);
   } else {
     a.lists = claim_lists(gridp);
     a.first_static = statics(p->items1, gridp);  // every ranked item is a GEMM1 item
@@ -762,10 +775,12 @@ extern "C" {
 
 int mlp2_run(mlp2_plan_t p, const void* X, const void* W1, const void* W2, void* Y, void* stream, int mode) {
   if (!p || !X || !W1 || !W2 || !Y) return fail(MLP2_ERR_INVALID_ARG);
-  if (mode < MLP2_MODE_SEQUENTIAL || mode > MLP2_MODE_STAGE2) return fail(MLP2_ERR_INVALID_ARG);
-  // The two stages of a grouped plan cannot be enqueued apart: its whole
-  // groups share one plan, whose split-K arrivals count one GEMM1 pass per run.
-  if (p->group && (mode == MLP2_MODE_STAGE1 || mode == MLP2_MODE_STAGE2)) return fail(MLP2_ERR_UNSUPPORTED);
+  if (mode < MLP2_MODE_SEQUENTIAL || mode > MLP2_MODE_SENTINEL) return fail(MLP2_ERR_INVALID_ARG);
+  // The two stages of a grouped plan cannot be enqueued apart (its whole
+  // groups share one plan, whose split-K arrivals count one GEMM1 pass per
+  // run), and its groups share no sentinel intermediates.
+  if (p->group && (mode == MLP2_MODE_STAGE1 || mode == MLP2_MODE_STAGE2 || mode == MLP2_MODE_SENTINEL))
+    return fail(MLP2_ERR_UNSUPPORTED);
   if (((uintptr_t)X | (uintptr_t)W1 | (uintptr_t)W2 | (uintptr_t)Y) & 15u) return fail(MLP2_ERR_ALIGNMENT);
   const int nb = p->act == MLP2_ACT_SWIGLU ? 2 : 1;
   const size_t xb = (size_t)p->M * p->H * 2, w1b = (size_t)nb * p->H * p->F * 2, w2b = (size_t)p->F * p->H * 2;
@@ -810,8 +825,11 @@ int mlp2_check(mlp2_plan_t p) {
   uint32_t ctrl[mlp2::CTRL_WORDS];
   if (hipMemcpy(ctrl, p->ctrl, sizeof(ctrl), hipMemcpyDeviceToHost) != hipSuccess) return fail(MLP2_ERR_HIP);
   if (ctrl[mlp2::CTRL_ERROR] == 0) return MLP2_OK;
-  // Recover: counters and epoch back to zero (the stream is idle by contract).
-  if (hipMemset((char*)p->ws + p->counters_off, 0, p->counters_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+  // Recover: counters and epoch back to zero, both sentinel intermediates
+  // back to sentinels (the stream is idle by contract).
+  const size_t zs_bytes = p->Zs ? (size_t)2 * p->Mb * p->kc.bm * p->F * 2 : 0;
+  if (hipMemset((char*)p->ws + p->counters_off, 0, p->counters_bytes) != hipSuccess ||
+      (zs_bytes && hipMemset(p->Zs, 0xFF, zs_bytes) != hipSuccess) || hipDeviceSynchronize() != hipSuccess)
     return fail(MLP2_ERR_HIP);
   return fail(MLP2_ERR_TIMEOUT);
 }

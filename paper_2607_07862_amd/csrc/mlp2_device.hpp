@@ -16,6 +16,15 @@
 
 namespace mlp2 {
 
+template <class A, class B>
+struct is_same_type {
+  static constexpr bool value = false;
+};
+template <class A>
+struct is_same_type<A, A> {
+  static constexpr bool value = true;
+};
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -41,7 +50,8 @@ enum {
   CTRL_QHEAD = 35 * kLine,         // workqueue mode: next queue slot a consumer claims
   CTRL_QTAIL = 36 * kLine,         // workqueue mode: next queue slot a producer fills
   CTRL_EPOCH_WQ = 37 * kLine,      // workqueue runs completed (the scoreboards advance in those only)
-  CTRL_WORDS = 38 * kLine
+  CTRL_EPOCH_SN = 38 * kLine,      // sentinel runs completed (their parity picks the intermediate buffer)
+  CTRL_WORDS = 39 * kLine
 };
 __device__ __forceinline__ int ctrl_ticket(int l) { return CTRL_TICKET + l * kLine; }
 __device__ __forceinline__ int ctrl_done(int l) { return CTRL_DONE + l * kLine; }
@@ -54,6 +64,11 @@ struct Args {
   const uint16_t* W2;  // [F, H]
   uint16_t* Y;         // [M, H]
   uint16_t* Z;         // [Mpad, F]
+  uint16_t* Zs;        // sentinel mode: two intermediates of [Mpad, F] each, zs_elems apart; sentinel runs
+                       // alternate between them (the other one is refilled with sentinels meanwhile)
+  long zs_elems;
+  uint16_t* Zr;        // inside a sentinel run: the intermediate the next sentinel run uses (refilled with
+                       // sentinels tile by tile); null otherwise
   float* part1;        // GEMM1 split-K partials (fragment-native), or null
   float* part2;        // GEMM2 split-K partials, or null
   uint32_t* cnt1;      // split-K arrival counters of GEMM1: tile t at word t * kLine
@@ -226,6 +241,50 @@ __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t 
   asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base), "{m0}"(lds_addr) : "memory");
 }
 
+// The same load at device scope (sc1, the scope bit of the compiler's own
+// agent-scope atomic loads): it reads the device's point of coherence rather
+// than a line the consumer's XCD L2 may hold.  The sentinel mode's consumers
+// read the intermediate this way, since no release and acquire order it.
+__device__ __forceinline__ void dma16_coherent(const void* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("global_load_lds_dwordx4 %0, %1 sc1" ::"v"(voff), "s"(base), "{m0}"(lds_addr) : "memory");
+}
+
+// ------------------------------------------------------------------ sentinel synchronisation
+//
+// Sec. V-A of the paper: instead of a fence and a flag per tile, the
+// intermediate buffer holds a sentinel value before its producer writes it,
+// and the consumer re-reads until no sentinel is left.  The sentinel is the
+// bf16 pattern 0xFFFF (a NaN with every payload bit set).  The GEMM1 epilogue
+// never writes it (canonicalize_z turns it into the canonical NaN 0x7FC0, in
+// every mode, so the modes stay bit-identical), so an element still holding
+// 0xFFFF has not been written yet; the check is per element, so a load that
+// sees part of a 16-byte piece before the rest was written is caught too.
+constexpr uint16_t kSentinel = 0xFFFF;
+
+__device__ __forceinline__ bool has_sentinel(u32x4 v) {
+  bool any = false;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) any |= (v[i] & 0xFFFFu) == 0xFFFFu || (v[i] >> 16) == 0xFFFFu;
+  return any;
+}
+
+__device__ __forceinline__ u32x4 canonicalize_z(u32x4 v) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if ((v[i] & 0xFFFFu) == 0xFFFFu) v[i] = (v[i] & 0xFFFF0000u) | 0x7FC0u;
+    if ((v[i] >> 16) == 0xFFFFu) v[i] = (v[i] & 0xFFFFu) | 0x7FC00000u;
+  }
+  return v;
+}
+
+// A 16-byte piece of the intermediate stored at device scope without any
+// fence: two 8-byte agent-scope relaxed atomic stores (each single-copy atomic).
+__device__ __forceinline__ void store_coherent16(uint16_t* p, u32x4 v) {
+  uint64_t* q = reinterpret_cast<uint64_t*>(p);
+  __hip_atomic_store(q, (uint64_t)v[0] | ((uint64_t)v[1] << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(q + 1, (uint64_t)v[2] | ((uint64_t)v[3] << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Wait until at most n of this wave's vector-memory operations are outstanding.
 template <int N>
 __device__ __forceinline__ void wait_vm() {
@@ -257,10 +316,18 @@ __device__ __forceinline__ void wait_stages_behind(int after) {
 // every wave's loads of stage it visible and retires every wave's reads of
 // stage it - 1, then the loads of stage it + NS - 1 go into that freed buffer
 // and stage it is multiplied.
-template <class T, int NB, class Wait>
+// A stage check that does nothing (every mode but the sentinel mode).
+struct NoCheck {
+  static constexpr bool kCoherentA = false;
+  template <class... X>
+  __device__ __forceinline__ void operator()(X...) {}
+};
+
+template <class T, int NB, class Wait, class Check = NoCheck>
 __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long lda, int m0, int mlast,
                                          const uint16_t* const (&Bp)[NB], long ldb, int n0, int kbeg, int kend,
-                                         f32x4 (&acc)[NB][T::TN][T::TM], char* lds, Wait& wait, TraceAcc& tr) {
+                                         f32x4 (&acc)[NB][T::TN][T::TM], char* lds, Wait& wait, TraceAcc& tr,
+                                         Check check = Check()) {
   // The thread index passes through an empty asm, so the compiler derives
   // this call's per-lane offsets here instead of hoisting them out of the
   // persistent item loop: in the pipelined kernel, whose items take one of
@@ -320,8 +387,12 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
               uniform(sbase + (uint32_t)(T::A_BYTES + b * T::B_BYTES + (wave + T::NWAVES * j) * 1024)));
     wait(k);
 #pragma unroll
-    for (int j = 0; j < T::A_DMA; ++j)
-      dma16(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + T::NWAVES * j) * 1024)));
+    for (int j = 0; j < T::A_DMA; ++j) {
+      if constexpr (Check::kCoherentA)
+        dma16_coherent(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + T::NWAVES * j) * 1024)));
+      else
+        dma16(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + T::NWAVES * j) * 1024)));
+    }
   };
 
   // Fragment addressing (bytes inside a stage).
@@ -408,6 +479,14 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     const uint64_t t0 = trace_now();
     // Own loads of stage `it` complete: the stages issued after it may stay in flight.
     wait_stages_behind<PER_STAGE, T::NS - 2>(min(T::NS - 2, nk - 1 - it));
+    if constexpr (!is_same_type<Check, NoCheck>::value) {
+      // The stage's activation pieces this wave loaded are in LDS: check them
+      // (and reload any piece that still holds a sentinel) before the barrier
+      // hands the stage to the other waves.
+      const int k = kbeg + it * kBK;
+      const uint32_t sbase = lds_base + (uint32_t)((it % T::NS) * SB);
+      check.template operator()<T>(A, a_off, k, sbase, lds + (it % T::NS) * SB, wave, lane);
+    }
     __syncthreads();
     if constexpr (kTrace) tr.ring += trace_now() - t0;
     if (it + T::NS - 1 < nk) issue(it + T::NS - 1);
@@ -415,6 +494,37 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   }
   __syncthreads();  // every wave is done reading the ring before it is reused
 }
+
+// The sentinel mode's stage check (the consumer side of Sec. V-A): each wave
+// reads back the activation pieces it loaded for the stage (16 bytes per lane
+// per 1 KB piece), and reloads a piece, at device scope, while any lane still
+// sees a sentinel element in it, sleeping between tries.  After spin_limit
+// tries, or once another wait gave up, it latches CTRL_ERROR (bit 2) and
+// stops; the kernel still exits and mlp2_check reports the timeout.
+struct SentinelCheck {
+  static constexpr bool kCoherentA = true;
+  uint32_t* err;  // CTRL_ERROR word
+  uint32_t spin_limit;
+  template <class T>
+  __device__ __forceinline__ void operator()(const uint16_t* A, const uint32_t (&a_off)[T::A_DMA], int k,
+                                             uint32_t sbase, const char* stage, int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < T::A_DMA; ++j) {
+      const int piece = (wave + T::NWAVES * j) * 1024;
+      for (uint32_t tries = 0;; ++tries) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(stage + piece + 16 * lane);
+        if (__builtin_amdgcn_ballot_w64(has_sentinel(v)) == 0) break;  // the same in every lane
+        if (tries >= spin_limit || ((tries & 63u) == 63u && uniform(ld_relaxed(err)) != 0u)) {
+          if (lane == 0) __hip_atomic_fetch_or(err, 4u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+        dma16_coherent(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)piece));
+        wait_vm<0>();
+      }
+    }
+  }
+};
 
 // ------------------------------------------------------------------ fragment <-> tile coordinates
 

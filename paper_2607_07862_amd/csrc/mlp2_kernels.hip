@@ -27,8 +27,8 @@ namespace mlp2 {
 
 // GEMM1 epilogue for one lane: activation in fp32 on the 8 consecutive values
 // of row `row` from column `col`, round to bf16, one 16-byte store into Z.
-template <int NB>
-__device__ __forceinline__ void store_z(const Args& a, long row, int col, const float (&v)[NB][8]) {
+template <int NB, bool SN = false>
+__device__ __forceinline__ void store_z(const Args& a, long row, int col, const float (&v)[NB][8], bool keep = true) {
   float z[8];
   if constexpr (NB == 2) {
 #pragma unroll
@@ -41,7 +41,17 @@ __device__ __forceinline__ void store_z(const Args& a, long row, int col, const 
       for (int i = 0; i < 8; ++i) z[i] = gelu_tanh(z[i]);
     }
   }
-  *reinterpret_cast<u32x4*>(a.Z + row * a.F + col) = pack_bf16x8(z);
+  const u32x4 packed = canonicalize_z(pack_bf16x8(z));  // never the sentinel pattern
+  if constexpr (SN) {
+    // Sentinel mode: the piece goes straight to the device's point of
+    // coherence, with no fence or flag after it; the same piece of the next
+    // sentinel run's intermediate is refilled with sentinels.
+    if (keep) store_coherent16(a.Z + row * a.F + col, packed);  // !keep: a dropped tile (failure injection)
+    const u32x4 sent = {0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+    *reinterpret_cast<u32x4*>(a.Zr + row * a.F + col) = sent;
+  } else {
+    *reinterpret_cast<u32x4*>(a.Z + row * a.F + col) = packed;
+  }
 }
 
 __device__ __forceinline__ void store_y(const Args& a, int row, int col, const float (&v)[8]) {
@@ -148,7 +158,7 @@ __device__ __forceinline__ void reduce_epilogue(const float* part, long tile, in
 
 // GEMM1 item id = tile * S1 + s, tile = nb * Mb + mb.  WQ: the completed
 // tile also feeds the workqueue's scoreboards (wq_epoch: workqueue runs so far).
-template <class T, int NB, bool WQ = false>
+template <class T, int NB, bool WQ = false, bool SN = false>
 __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t epoch, char* lds, int* s_slot,
                                            Claim& next, int* s_next, TraceAcc& tr, uint32_t wq_epoch = 0) {
   const int id = uniform(id_in);
@@ -177,7 +187,7 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
         float v[NB][8];
 #pragma unroll
         for (int b = 0; b < NB; ++b) pair_values<T>(acc[b], tp, tm, v[b]);
-        store_z<NB>(a, fp.row0 + 16 * tm, fp.col0 + 32 * tp, v);
+        store_z<NB, SN>(a, fp.row0 + 16 * tm, fp.col0 + 32 * tp, v, tile != a.drop_signal);
       }
   } else {
     const bool last = arrive_split<T, NB>(a.part1, a.cnt1 + (long)tile * kLine, tile, a.S1, s,
@@ -185,9 +195,10 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
     next.park(s_next);
     if (!last) return;
     reduce_epilogue<T, NB>(a.part1, tile, a.S1, [&](const Unit<T>& u, int lane, const float (&v)[NB][8]) {
-      store_z<NB>(a, u.row(m0, lane), u.col(n0, lane), v);
+      store_z<NB, SN>(a, u.row(m0, lane), u.col(n0, lane), v, tile != a.drop_signal);
     });
   }
+  if constexpr (SN) return;  // no fence and no flag: consumers check the data itself
   // Producer signal (one per tile and run): the tile's Z rows are released, ready[tile] += 1.
   if constexpr (kTrace) {
     wait_all_mem();
@@ -209,9 +220,9 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
 // kernel that holds both item kinds carries one mainloop shape and one
 // register budget.  Each output element still accumulates over K in the
 // same order.
-template <class T, int HV, bool WAIT, class C = Claim>
+template <class T, int HV, bool WAIT, class C = Claim, bool SN = false>
 __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epoch, char* lds, int* s_slot,
-                                           C& next, int* s_next, TraceAcc& tr) {
+                                           C& next, int* s_next, TraceAcc& tr, uint32_t ready_runs = 0) {
   const int p = uniform(p_in);
   const int tile = p / a.S2, s = p - (p / a.S2) * a.S2;
   const int mb = tile % a.Mb, nb = tile / a.Mb;
@@ -224,9 +235,17 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
 #pragma unroll
   for (int h = 0; h < HV; ++h) Bp[h] = a.W2 + h * T::BN;
   const int zlast = a.Mb * T::BM - 1;
-  if constexpr (WAIT) {
-    ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1, epoch + 1u, a.spin_limit, s_slot,
-                0, &tr};
+  if constexpr (SN) {
+    // Sentinel mode: no ready counters; each stage's Z pieces are loaded at
+    // device scope and checked for sentinels before the stage is used.
+    NoWait nowait;
+    ClaimAtLastStage<NoWait, C> hook{nowait, &next, kend - kBK};
+    SentinelCheck check{a.ctrl + CTRL_ERROR, a.spin_limit};
+    mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr, check);
+  } else if constexpr (WAIT) {
+    // ready counters advance once per run of every mode but the sentinel mode
+    ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1, ready_runs + 1u, a.spin_limit,
+                s_slot, 0, &tr};
     ClaimAtLastStage<ReadyWait, C> hook{w, &next, kend - kBK};
     mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   } else {
@@ -269,7 +288,8 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
 // over the lists keeps the exit atomics, one per work-group, off a single
 // line.
 __device__ __forceinline__ void finish_kernel(const Args& a, bool roles, uint32_t epoch, bool end_of_run,
-                                              bool wq_run = false, uint32_t wq_epoch = 0) {
+                                              bool wq_run = false, uint32_t wq_epoch = 0, bool sn_run = false,
+                                              uint32_t sn_epoch = 0) {
   __syncthreads();
   if (threadIdx.x == 0) {
     const ListPos lp = list_pos(a, roles);
@@ -287,6 +307,7 @@ __device__ __forceinline__ void finish_kernel(const Args& a, bool roles, uint32_
         __hip_atomic_store(a.ctrl + CTRL_QHEAD, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(a.ctrl + CTRL_QTAIL, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (wq_run) __hip_atomic_store(a.ctrl + CTRL_EPOCH_WQ, wq_epoch + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (sn_run) __hip_atomic_store(a.ctrl + CTRL_EPOCH_SN, sn_epoch + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (end_of_run) __hip_atomic_store(a.ctrl + CTRL_EPOCH, epoch + 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
@@ -322,7 +343,15 @@ __device__ __forceinline__ void finish_kernel(const Args& a, bool roles, uint32_
 //                    items never wait, so every producer finishes and every
 //                    claimed queue slot is filled: no deadlock either.
 
-enum { PHASE_GEMM1 = 0, PHASE_GEMM2 = 1, PHASE_PIPELINED = 2, PHASE_WORKQUEUE = 3 };
+//   PHASE_SENTINEL:  the pipelined rank table and claims, with the Lamport-
+//                    style synchronisation of Sec. V-A: GEMM1 items store Z at
+//                    device scope with no fence and no ready counter; GEMM2
+//                    items wait for nothing but re-read each stage's Z pieces
+//                    while any still holds the sentinel.  A GEMM2 item still
+//                    depends only on lower-ranked GEMM1 items, so the
+//                    deadlock argument above holds unchanged.
+
+enum { PHASE_GEMM1 = 0, PHASE_GEMM2 = 1, PHASE_PIPELINED = 2, PHASE_WORKQUEUE = 3, PHASE_SENTINEL = 4 };
 
 template <int A, int B>
 struct MaxI {
@@ -354,11 +383,21 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
   __shared__ int s_item, s_slot;
   const uint32_t epoch = uniform(ld_relaxed(a.ctrl + CTRL_EPOCH));
   const uint32_t wq_epoch = PHASE == PHASE_WORKQUEUE ? uniform(ld_relaxed(a.ctrl + CTRL_EPOCH_WQ)) : 0u;
+  // Sentinel runs alternate between two intermediates: this run's producers
+  // write one and refill the other with sentinels for the next sentinel run.
+  const uint32_t sn_epoch =
+      PHASE == PHASE_SENTINEL || PHASE == PHASE_PIPELINED ? uniform(ld_relaxed(a.ctrl + CTRL_EPOCH_SN)) : 0u;
+  // Earlier runs whose GEMM1 tiles signalled the ready counters: every run but the sentinel runs.
+  const uint32_t ready_runs = epoch - sn_epoch;
+  if constexpr (PHASE == PHASE_SENTINEL) {
+    a.Z = a.Zs + (long)(sn_epoch & 1u) * a.zs_elems;
+    a.Zr = a.Zs + (long)((sn_epoch + 1u) & 1u) * a.zs_elems;
+  }
   // A role split (pipelined launch only): this work-group takes the items of
   // one kind, in that kind's order table; otherwise both kinds from one order.
   const ListPos lp = list_pos(a, PHASE == PHASE_PIPELINED && a.p1 > 0);
   const int g1 = PHASE == PHASE_GEMM2 || lp.role == 1 ? 0 : a.items1;
-  const int g2 = (PHASE == PHASE_GEMM2 || PHASE == PHASE_PIPELINED) && lp.role != 0 ? a.items2 : 0;
+  const int g2 = (PHASE == PHASE_GEMM2 || PHASE == PHASE_PIPELINED || PHASE == PHASE_SENTINEL) && lp.role != 0 ? a.items2 : 0;
   const int total = g1 + g2;
   int p;
   if (lp.role < 0 && (int)blockIdx.x < a.first_static) {
@@ -379,10 +418,16 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
     const uint64_t t_start = trace_now();
     Claim next = make_claim(a, lp.role >= 0);
     uint32_t e;  // order-table entry: item id, bit 31 set for a GEMM2 item
-    if constexpr (PHASE == PHASE_PIPELINED) {
+    if constexpr (PHASE == PHASE_SENTINEL) {
+      e = uniform(a.orderp[p]);
+      if (e & 0x80000000u)
+        gemm2_item<T2, HV, false, Claim, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr);
+      else
+        gemm1_item<T1, NB, false, true>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
+    } else if constexpr (PHASE == PHASE_PIPELINED) {
       e = lp.role < 0 ? uniform(a.orderp[p]) : lp.role == 0 ? uniform(a.order1[p]) : (uniform(a.order2[p]) | 0x80000000u);
       if (e & 0x80000000u)
-        gemm2_item<T2, HV, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr);
+        gemm2_item<T2, HV, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr, ready_runs);
       else
         gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
     } else if constexpr (PHASE == PHASE_GEMM1 || PHASE == PHASE_WORKQUEUE) {
@@ -413,7 +458,8 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
       c_pop = trace_clock();
     }
   }
-  finish_kernel(a, lp.role >= 0, epoch, PHASE != PHASE_GEMM1, PHASE == PHASE_WORKQUEUE, wq_epoch);
+  finish_kernel(a, lp.role >= 0, epoch, PHASE != PHASE_GEMM1, PHASE == PHASE_WORKQUEUE, wq_epoch,
+                PHASE == PHASE_SENTINEL, sn_epoch);
 }
 
 // ------------------------------------------------------------------ dispatch table
@@ -448,6 +494,7 @@ struct Entry {
   const void* seq2;
   const void* pipe;
   const void* wq;
+  const void* sn;
 };
 
 // GEMM2 of BN2 columns as one tile (HV = 1), or as two halves of BN2 / 2 that
@@ -459,7 +506,7 @@ struct Entry {
   Entry {                                                                                                         \
     BM, BN1, BN2, NB, NS, W, MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_GEMM1),                                   \
         MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_GEMM2), MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_PIPELINED), \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_WORKQUEUE)                                                     \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_WORKQUEUE), MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_SENTINEL) \
   }
 #define MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, HV) MLP2_ENTRY_W(BM, BN1, BN2, NB, NS, HV, 4)
 #define MLP2_ENTRY(BM, BN1, BN2, NB, NS) MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, 1)
@@ -606,7 +653,7 @@ bool config_supported(const KernelConfig& c) { return find_entry(c) != nullptr; 
 hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu) {
   const Entry* e = find_entry(c);
   if (!e) return hipErrorInvalidValue;
-  const void* k = which == 0 ? e->seq1 : which == 1 ? e->seq2 : which == 2 ? e->pipe : e->wq;
+  const void* k = which == 0 ? e->seq1 : which == 1 ? e->seq2 : which == 2 ? e->pipe : which == 3 ? e->wq : e->sn;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, 64 * e->waves, 0);
 }
 
@@ -638,6 +685,13 @@ hipError_t launch_workqueue(const KernelConfig& c, const Args& a, int grid, hipS
   if (!e) return hipErrorInvalidValue;
   void* args[] = {const_cast<Args*>(&a)};
   return hipLaunchKernel(e->wq, dim3(grid), dim3(64 * e->waves), args, 0, stream);
+}
+
+hipError_t launch_sentinel(const KernelConfig& c, const Args& a, int grid, hipStream_t stream) {
+  const Entry* e = find_entry(c);
+  if (!e) return hipErrorInvalidValue;
+  void* args[] = {const_cast<Args*>(&a)};
+  return hipLaunchKernel(e->sn, dim3(grid), dim3(64 * e->waves), args, 0, stream);
 }
 
 }  // namespace mlp2

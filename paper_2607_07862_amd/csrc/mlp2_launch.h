@@ -16,7 +16,7 @@ struct KernelConfig {
 
 bool config_supported(const KernelConfig& c);
 // Resident work-groups per CU of a kernel: which = 0 (GEMM1 phase), 1 (GEMM2 phase), 2 (pipelined),
-// 3 (workqueue).
+// 3 (workqueue), 4 (sentinel).
 hipError_t occupancy(const KernelConfig& c, int which, int* blocks_per_cu);
 // a1 / a2: arguments of the GEMM1 / GEMM2 launch (they differ only in `lists`); stages: 1 = the
 // GEMM1 kernel, 2 = the GEMM2 kernel, 3 = both in that order.
@@ -24,6 +24,7 @@ hipError_t launch_sequential(const KernelConfig& c, const Args& a1, const Args& 
                              int stages);
 hipError_t launch_pipelined(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
 hipError_t launch_workqueue(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
+hipError_t launch_sentinel(const KernelConfig& c, const Args& a, int grid, hipStream_t stream);
 
 // ---- GEMM chain: Z_l = act(Z_{l-1} W_l), Y = Z_{L-1} W_L, no split-K.
 constexpr int kChainMaxLayers = 8;

@@ -100,7 +100,7 @@ extern "C" int mlp2_run_noalloc(int64_t M, int64_t H, int64_t F, int act, int dt
   rc = configure_plan(&p, M, H, F, act, tz, dev, num_cus);
   if (rc != MLP2_OK) return record_error(rc);
   PlanLayout L;
-  if (plan_layout(&p, true, &L) > kScratchBytes) return record_error(MLP2_ERR_UNSUPPORTED);  // beyond the scratch
+  if (plan_layout(&p, true, &L, false) > kScratchBytes) return record_error(MLP2_ERR_UNSUPPORTED);  // beyond the scratch
   bind_plan(&p, base, L, nullptr);
   p.ws = base;
   p.ws_bytes = L.bytes;

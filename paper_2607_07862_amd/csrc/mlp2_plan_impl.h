@@ -30,6 +30,7 @@ struct mlp2_plan_s {
   void* ws = nullptr;
   size_t ws_bytes = 0;
   uint16_t* Z = nullptr;
+  uint16_t* Zs = nullptr;  // sentinel mode: two intermediates of Mpad x F, one after the other (or null)
   float* part1 = nullptr;
   float* part2 = nullptr;
   uint32_t* cnt1 = nullptr;
@@ -58,12 +59,13 @@ namespace mlp2 {
 // [cnt_off, cnt_end) holds every counter and control word that starts at zero.
 struct PlanLayout {
   size_t z_off, p1_off, p2_off, c1_off, c2_off, r_off, b_off, q_off, ctrl_off, cnt_off, cnt_end, ord_off, ord2_off,
-      ordp_off, bytes;
+      ordp_off, zs_off, zs_bytes, bytes;
 };
 
 int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, const mlp2_tuning_t& tz, int dev,
                    int num_cus);
-size_t plan_layout(const mlp2_plan_s* p, bool own_z, PlanLayout* L);
+// with_zs: room for the sentinel mode's two intermediates (zs_bytes, else 0).
+size_t plan_layout(const mlp2_plan_s* p, bool own_z, PlanLayout* L, bool with_zs = true);
 void bind_plan(mlp2_plan_s* p, char* base, const PlanLayout& L, uint16_t* z_ext);
 int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void* W2, void* Y, uint16_t* Z,
                 hipStream_t s, int mode);

@@ -35,6 +35,14 @@ def workqueue_mode(plan: B.Plan, g: dict):
     return Yq, plan.intermediate()
 
 
+def sentinel_mode(plan: B.Plan, g: dict):
+    """Y of a sentinel-mode run (synchronised)."""
+    Yn = run(plan, g, B.MODE_SENTINEL)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    return Yn
+
+
 def both_modes(plan: B.Plan, g: dict):
     """Y and Z of a sequential run and of a pipelined run (each synchronised)."""
     Ys = run(plan, g, B.MODE_SEQUENTIAL)

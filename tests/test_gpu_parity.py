@@ -19,7 +19,8 @@ from oracle import mlp2_oracle as O
 from paper_2607_07862_amd import binding as B
 from paper_2607_07862_amd import inputs as I
 
-from _gpu import assert_bit_equal, assert_matches_oracle, both_modes, bits_of, device_inputs, run, workqueue_mode
+from _gpu import (assert_bit_equal, assert_matches_oracle, both_modes, bits_of, device_inputs, run, sentinel_mode,
+                  workqueue_mode)
 
 pytestmark = pytest.mark.gpu
 
@@ -71,10 +72,12 @@ def test_small_shapes_against_full_oracle(lib, M, H, F, act, tuning):
         assert info["bn2"] == 2 * info["bn1"], info
     Ys, Zs, Yp, Zp = both_modes(plan, g)
     Yq, Zq = workqueue_mode(plan, g)
+    Yn = sentinel_mode(plan, g)
     ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
     assert_matches_oracle(Yp, ref, "pipelined Y")
     assert_matches_oracle(Ys, ref, "sequential Y")
     assert_bit_equal(Ys, Yp, "Y sequential vs pipelined")
+    assert_bit_equal(Ys, Yn, "Y sequential vs sentinel")
     assert_bit_equal(Zs, Zp, "Z sequential vs pipelined")
     assert_bit_equal(Ys, Yq, "Y sequential vs workqueue")
     assert_bit_equal(Zs, Zq, "Z sequential vs workqueue")
@@ -106,6 +109,8 @@ def test_workloads_full_size_sampled_rows(lib, key):
     Yq, Zq = workqueue_mode(plan, g)
     assert_bit_equal(Ys, Yq, "Y sequential vs workqueue")
     assert_bit_equal(Zs, Zq, "Z sequential vs workqueue")
+    if not plan.info()["row_group"]:  # the sentinel mode runs without row groups
+        assert_bit_equal(Ys, sentinel_mode(plan, g), "Y sequential vs sentinel")
     # one row in every row block of the plan's tiles (a grouped plan's blocks
     # tile each group, and groups are whole blocks) beside 24 seeded rows
     rows = I.sample_rows_per_block(w.M, plan.info()["bm"], 24, w.seed)

@@ -15,7 +15,11 @@
 * so do the stage splits of the pipelined launch: the rank-table lag at its
   extremes (one rank; every GEMM2 item after every GEMM1 item) and static
   producer / consumer role splits of the grid;
-* a run captured into a graph replays with the eager bits, in every mode.
+* a run captured into a graph replays with the eager bits, in every mode;
+* the sentinel mode (no fence, no flag: consumers re-read the intermediate
+  until no sentinel is left) gives the same bits, alternating with the other
+  modes; a dropped tile times out and the plan recovers; the sentinel value
+  is never an output of the epilogue.
 """
 import pytest
 import torch
@@ -154,8 +158,10 @@ def test_alternating_inputs_and_modes(lib, act):
     torch.cuda.synchronize()
     outs = []
     seq = [0, 1, 2, 2, 0, 1, 0, 0, 2, 1] * 3
+    modes = (B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_WORKQUEUE, B.MODE_SENTINEL, B.MODE_SENTINEL,
+             B.MODE_TILE_PIPELINED, B.MODE_SENTINEL)
     for n, i in enumerate(seq):
-        mode = (B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_WORKQUEUE)[n % 3]
+        mode = modes[n % len(modes)]
         outs.append((i, run(plan, sets[i], mode)))
     torch.cuda.synchronize()
     assert plan.check() == B.OK
@@ -198,6 +204,61 @@ def test_dropped_signal_times_out_and_recovers(lib):
     assert_bit_equal(Ys, Yp, "after recovery")
     ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
     assert_matches_oracle(Yp, ref, "after recovery")
+    plan.close()
+
+
+def test_sentinel_mode_dropped_tile_times_out_and_recovers(lib):
+    """Sentinel mode: a GEMM1 tile whose intermediate stores are skipped leaves
+    sentinels that its consumers keep re-reading until the bounded wait gives
+    up; every kernel still exits, mlp2_check reports the timeout and refills
+    both sentinel intermediates, and the following runs of every mode (two
+    sentinel runs: both intermediates) are correct."""
+    M, H, F, act = 130, 256, 512, 1
+    d = I.make_inputs(M, H, F, act, seed=71)
+    g = device_inputs(d)
+    plan = B.Plan(M, H, F, act, {"splitk1": 2})
+    plan.set_option(B.OPT_SPIN_LIMIT, 200)
+    plan.set_option(B.OPT_DROP_SIGNAL, 1)
+    run(plan, g, B.MODE_SENTINEL)
+    torch.cuda.synchronize()
+    assert plan.check() == B.ERR_TIMEOUT
+    plan.set_option(B.OPT_DROP_SIGNAL, -1)
+    plan.set_option(B.OPT_SPIN_LIMIT, 1 << 20)
+    Ys = run(plan, g, B.MODE_SEQUENTIAL).clone()
+    Yn1 = run(plan, g, B.MODE_SENTINEL).clone()
+    Yn2 = run(plan, g, B.MODE_SENTINEL).clone()
+    Yp = run(plan, g, B.MODE_TILE_PIPELINED)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    for y, what in ((Yn1, "sentinel run 1"), (Yn2, "sentinel run 2"), (Yp, "pipelined")):
+        assert_bit_equal(Ys, y, f"after recovery: {what}")
+    ref = O.mlp2(I.bits(d["X"]), I.bits(d["W1"]), I.bits(d["W2"]), M, H, F, act)
+    assert_matches_oracle(Yn2, ref, "after recovery")
+    plan.close()
+
+
+def test_sentinel_value_is_never_an_output(lib):
+    """The epilogue turns the sentinel pattern into the canonical NaN in every
+    mode: X holding NaNs whose bf16 pattern is 0xFFFF gives no 0xFFFF in Z,
+    and the modes still agree bit for bit (identity weights pass X through)."""
+    M, H = 64, 128
+    X = torch.randn(M, H).to(torch.bfloat16)
+    xb = X.view(torch.int16)
+    xb[3, 5] = -1  # 0xFFFF
+    xb[10, 64] = -1
+    eye = torch.eye(H, dtype=torch.bfloat16)
+    g = device_inputs({"X": X, "W1": eye, "W2": eye.clone()})
+    plan = B.Plan(M, H, H, 0)
+    outs = {}
+    for mode in (B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_SENTINEL):
+        outs[mode] = run(plan, g, mode).clone()
+        torch.cuda.synchronize()
+        Z = bits_of(plan.intermediate())
+        if mode != B.MODE_SENTINEL:
+            assert not (Z == 0xFFFF).any()
+    assert plan.check() == B.OK
+    assert_bit_equal(outs[B.MODE_SEQUENTIAL], outs[B.MODE_SENTINEL], "sentinel mode with NaN inputs")
+    assert_bit_equal(outs[B.MODE_SEQUENTIAL], outs[B.MODE_TILE_PIPELINED], "pipelined mode with NaN inputs")
     plan.close()
 
 
@@ -309,7 +370,7 @@ def test_workqueue_dropped_signal_times_out_and_recovers(lib):
     plan.close()
 
 
-@pytest.mark.parametrize("mode", [B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_WORKQUEUE])
+@pytest.mark.parametrize("mode", [B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_WORKQUEUE, B.MODE_SENTINEL])
 def test_graph_replays_match_eager_runs(lib, mode):
     """mlp2_run records into a graph (kernel launches only: no memset, no
     synchronisation), and every replay gives the eager bits: the counters and
@@ -336,7 +397,7 @@ def test_graph_replays_match_eager_runs(lib, mode):
         graph.replay()
         torch.cuda.synchronize()
         outs.append(Y.clone())
-        run(plan, g, (B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_WORKQUEUE)[i % 3])
+        run(plan, g, (B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED, B.MODE_WORKQUEUE, B.MODE_SENTINEL)[i % 4])
         torch.cuda.synchronize()
     assert plan.check() == B.OK
     for n, y in enumerate(outs):
@@ -352,7 +413,7 @@ def test_run_argument_errors(lib):
     Y = torch.empty(M, H, dtype=torch.bfloat16, device="cuda")
     s = torch.cuda.current_stream().cuda_stream
     X, W1, W2, y = (t.data_ptr() for t in (g["X"], g["W1"], g["W2"], Y))
-    assert plan.run_raw(X, W1, W2, y, s, 5) == B.ERR_INVALID_ARG
+    assert plan.run_raw(X, W1, W2, y, s, 6) == B.ERR_INVALID_ARG
     assert plan.run_raw(X, W1, W2, y, s, -1) == B.ERR_INVALID_ARG
     assert plan.run_raw(X + 2, W1, W2, y, s, 0) == B.ERR_ALIGNMENT
     assert plan.run_raw(X, W1, W2, X, s, 0) == B.ERR_INVALID_ARG  # Y aliases X

@@ -367,23 +367,36 @@ def test_workqueue_schedule_with_parts_sharing_a_column_block():
 @pytest.mark.parametrize("seed", range(5))
 def test_counter_targets_hold_across_any_sequence_of_modes(seed):
     """Counters carry over from run to run without host resets.  Ready counters
-    advance once per run in every mode (workqueue producers signal them too),
-    so a pipelined consumer's target is epoch + 1; scoreboards advance only in
-    workqueue runs, so a unit with n producers completes at (w + 1) * n, w the
-    number of earlier workqueue runs; split-K arrivals count S per run."""
+    advance once per run in every mode but the sentinel mode (workqueue
+    producers signal them too; sentinel producers signal nothing), so a
+    pipelined consumer's target is (epoch - s) + 1, s the number of earlier
+    sentinel runs, and a counter never reaches the target before its tile
+    signals in this run; scoreboards advance only in workqueue runs, so a unit
+    with n producers completes at (w + 1) * n, w the number of earlier
+    workqueue runs; split-K arrivals count S per run in every mode; sentinel
+    runs alternate between two intermediates by the parity of s."""
     rng = random.Random(seed)
     tiles, n_of = list(range(6)), {"u0": 2, "u1": 3, "u2": 1}
     users = {"u0": [0, 1], "u1": [2, 3, 4], "u2": [5]}
     ready = {t: 0 for t in tiles}
     board = {u: 0 for u in n_of}
     arrivals, S = 0, 3
-    epoch = wq = 0
-    for _ in range(60):
-        mode = rng.choice(["sequential", "pipelined", "workqueue"])
-        for t in tiles:  # every GEMM1 tile signals once per run
-            ready[t] += 1
-        if mode == "pipelined":
-            assert all(ready[t] >= epoch + 1 for t in tiles)
+    epoch = wq = sn = 0
+    fresh = [True, True]  # each sentinel intermediate holds sentinels before its run
+    for _ in range(80):
+        mode = rng.choice(["sequential", "pipelined", "workqueue", "sentinel"])
+        if mode == "sentinel":
+            buf = sn & 1
+            assert fresh[buf]
+            fresh[buf] = False      # this run writes it ...
+            fresh[1 - buf] = True   # ... and refills the other one
+        else:
+            if mode == "pipelined":  # before this run's signals: not yet ready
+                assert all(ready[t] < (epoch - sn) + 1 for t in tiles)
+            for t in tiles:  # every GEMM1 tile signals once per run
+                ready[t] += 1
+            if mode == "pipelined":
+                assert all(ready[t] >= (epoch - sn) + 1 for t in tiles)
         if mode == "workqueue":
             for u, ts in users.items():
                 for k, t in enumerate(ts):
@@ -394,6 +407,7 @@ def test_counter_targets_hold_across_any_sequence_of_modes(seed):
             assert (arrivals == (epoch + 1) * S) == (s == S - 1)
         epoch += 1
         wq += mode == "workqueue"
+        sn += mode == "sentinel"
 
 
 @pytest.mark.parametrize("Mb,N,wave,band", [(128, 64, 512, 8), (16, 112, 512, 4), (5, 7, 8, 2), (3, 10, 17, 1), (40, 3, 64, 21)])
