@@ -22,7 +22,9 @@ the stream it is launched on).  Beside it the line carries:
   the current kernel sources, and what the GPU attains outside the library
   (a 4 GiB read-only stream, an 8192^3 hipBLASLt GEMM) as context;
 * every MLP workload on its own seeded inputs (the seeds of its
-  configuration): both modes blocked, interleaved and cold, eager PyTorch on
+  configuration): both modes blocked, interleaved and cold, the workqueue
+  and sentinel modes (the paper's scoreboard queue, and its Lamport-style
+  synchronisation without fences or flags), eager PyTorch on
   the same inputs (hipBLASLt GEMMs plus an activation kernel), and the same
   roofline object with traffic;
 * the paper's micro-batching comparison on one GPU: 8192 x 8192 weights at
@@ -382,15 +384,16 @@ class Runner:
         torch.cuda.synchronize()
         return {m: [a.elapsed_time(b) * 1e3 for a, b in v] for m, v in out.items()}
 
-    def interleaved(self, iters):
-        """Per-run µs of both modes, run by run in alternating order (ABBA...), warm.
+    def interleaved(self, iters, modes=None):
+        """Per-run µs of the modes (default: pipelined and sequential), run by
+        run in alternating order (ABBA...), warm.
 
-        Clock and thermal drift then reach both modes alike, which back-to-back
+        Clock and thermal drift then reach every mode alike, which back-to-back
         blocks of one mode do not guarantee."""
         import torch
 
-        out = {self.B.MODE_TILE_PIPELINED: [], self.B.MODE_SEQUENTIAL: []}
-        order = (self.B.MODE_TILE_PIPELINED, self.B.MODE_SEQUENTIAL)
+        order = tuple(modes or (self.B.MODE_TILE_PIPELINED, self.B.MODE_SEQUENTIAL))
+        out = {m: [] for m in order}
         for i in range(iters):
             for m in (order if i % 2 == 0 else order[::-1]):
                 a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -512,12 +515,15 @@ def table_row(B, I, key: str, stream, steps: int, iters: int, cold_iters: int, f
         rr.run(B.MODE_TILE_PIPELINED)
         rr.run(B.MODE_SEQUENTIAL)
         rr.run(B.MODE_WORKQUEUE)
+        rr.run(B.MODE_SENTINEL)
     s_before = rr.block(B.MODE_SEQUENTIAL, steps)
     p_us = rr.block(B.MODE_TILE_PIPELINED, steps)
     s_us = (s_before + rr.block(B.MODE_SEQUENTIAL, steps)) / 2
     q_us = rr.block(B.MODE_WORKQUEUE, steps)
-    ivk = rr.interleaved(iters)
+    n_us = rr.block(B.MODE_SENTINEL, steps)
+    ivk = rr.interleaved(iters, (B.MODE_TILE_PIPELINED, B.MODE_SEQUENTIAL, B.MODE_SENTINEL))
     mp, ms = statistics.median(ivk[B.MODE_TILE_PIPELINED]), statistics.median(ivk[B.MODE_SEQUENTIAL])
+    mn = statistics.median(ivk[B.MODE_SENTINEL])
     cold = rr.cold([B.MODE_TILE_PIPELINED, B.MODE_SEQUENTIAL], cold_iters, flush) if cold_iters else None
     rr.check()
     inf = rr.info
@@ -531,7 +537,8 @@ def table_row(B, I, key: str, stream, steps: int, iters: int, cold_iters: int, f
         "sequential_us": round(s_us, 2),
         "gain_pct": round((s_us - p_us) / s_us * 100, 1),
         "workqueue_us": round(q_us, 2),
-        "interleaved_median_us": {"pipelined": round(mp, 2), "sequential": round(ms, 2),
+        "sentinel_us": round(n_us, 2),
+        "interleaved_median_us": {"pipelined": round(mp, 2), "sequential": round(ms, 2), "sentinel": round(mn, 2),
                                   "gain_pct": round((ms - mp) / ms * 100, 1)},
         "torch_eager_us": round(te, 2),
         "roofline": rf,

@@ -154,7 +154,8 @@ typedef struct mlp2_tuning {
                     item from one rank order); else work-groups with index g % 64 < p1
                     take only GEMM1 items and the others only GEMM2 items (a static
                     producer / consumer split of the grid, p1 in 1..63 of every 64)       */
-  int reserved[2];
+  int bk;        /* K depth of one LDS stage: 64 or 32 (as built for the shape)            */
+  int reserved[1];
 } mlp2_tuning_t;
 
 /* What a plan chose, for reports and tests. */

@@ -62,7 +62,8 @@ class Tuning(ctypes.Structure):
         ("waves", ctypes.c_int),
         ("lag", ctypes.c_int),
         ("p1", ctypes.c_int),
-        ("reserved", ctypes.c_int * 2),
+        ("bk", ctypes.c_int),
+        ("reserved", ctypes.c_int * 1),
     ]
 
 

@@ -379,7 +379,8 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   if (t) tz = *t;
   if (tz.bm < 0 || tz.bn1 < 0 || tz.bn2 < 0 || tz.splitk1 < 0 || tz.splitk2 < 0 || tz.grid < 0 || tz.order < 0 || tz.stages < 0 ||
       tz.order > MLP2_ORDER_BANDED || tz.row_group < -1 || (tz.row_group > 0 && tz.row_group % 256) ||
-      (tz.waves != 0 && tz.waves != 4 && tz.waves != 8) || tz.lag < -1 || tz.p1 < 0 || tz.p1 > 63 || tz.p1 % 8) {
+      (tz.waves != 0 && tz.waves != 4 && tz.waves != 8) || tz.lag < -1 || tz.p1 < 0 || tz.p1 > 63 || tz.p1 % 8 ||
+      (tz.bk != 0 && tz.bk != 32 && tz.bk != 64)) {
     fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
   }
@@ -463,7 +464,7 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
   // weigh more than idle CUs, so both GEMMs keep their K ranges deep; at 64
   // rows small tiles shorten the latency-bound critical path.  Beyond 256 rows (MFMA-bound): 128 x 128 tiles, two work-groups
   // per CU.
-  int pref[5] = {0, 0, 0, 0, 4};  // bm, bn1, bn2, ring depth, waves
+  int pref[6] = {0, 0, 0, 0, 4, 64};  // bm, bn1, bn2, ring depth, waves, stage depth
   int min_k1 = 256, min_k2 = 256;  // shallowest K range of one split-K part
   if (M <= 32) {
     pref[0] = 32; pref[1] = 64; pref[2] = 128; pref[3] = 4;
@@ -501,6 +502,7 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
   }
   // Fallbacks when the preferred tiles do not divide F / H or are not built.
   const int w = pref[4];
+  const int bk = pref[5];
   const int cand[][5] = {
       {pref[0], pref[1], pref[2], pref[3], w}, {pref[0], pref[1], 64, pref[3], w}, {pref[0], 64, 64, pref[3], w},
       {pref[0], pref[1], pref[2], 4, w},       {pref[0], pref[1], 64, 4, w},       {pref[0], 64, 64, 4, w},
@@ -509,13 +511,16 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
       {128, 64, 64, 4, 4},                     {64, 64, 64, 4, 4},                 {32, 64, 64, 4, 4},
   };
   bool found = false;
-  for (const auto& c : cand) {
-    KernelConfig k{tz.bm ? tz.bm : c[0], tz.bn1 ? tz.bn1 : c[1], tz.bn2 ? tz.bn2 : c[2], nb, tz.stages ? tz.stages : c[3],
-                   tz.waves ? tz.waves : c[4]};
-    if (F % k.bn1 == 0 && H % k.bn2 == 0 && mlp2::config_supported(k)) {
-      p->kc = k;
-      found = true;
-      break;
+  // The preferred stage depth first; the fallbacks with 64-deep stages.
+  for (int pass = 0; pass < 2 && !found; ++pass) {
+    for (const auto& c : cand) {
+      KernelConfig k{tz.bm ? tz.bm : c[0], tz.bn1 ? tz.bn1 : c[1], tz.bn2 ? tz.bn2 : c[2], nb,
+                     tz.stages ? tz.stages : c[3], tz.waves ? tz.waves : c[4], tz.bk ? tz.bk : pass ? 64 : bk};
+      if (F % k.bn1 == 0 && H % k.bn2 == 0 && mlp2::config_supported(k)) {
+        p->kc = k;
+        found = true;
+        break;
+      }
     }
   }
   if (!found) return MLP2_ERR_UNSUPPORTED;
@@ -856,7 +861,7 @@ int mlp2_plan_info(mlp2_plan_t p, mlp2_info_t* out) {
   out->splitk1 = p->S1;
   out->bn2 = p->kc.bn2;
   out->splitk2 = p->S2;
-  out->bk = mlp2::kBK;
+  out->bk = p->kc.bk;
   out->stages = p->kc.ns;
   out->row_blocks = p->Mb;
   out->col_blocks1 = p->Nb1;

@@ -31,7 +31,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
 
-constexpr int kBK = 64;        // K depth of one LDS stage
+constexpr int kBK = 64;        // K granularity of the plans (split-K ranges); the deepest LDS stage
 
 // Words per 128-byte line.  Every counter that work-groups update with device-
 // scope atomics sits on a line of its own: such atomics are performed at the
@@ -191,15 +191,22 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 // LDS stage layout (bytes), both parts unpadded and XOR-swizzled in 16-byte
 // chunks, because the direct-to-LDS loads write each wave's 1 KB contiguously
 // (lane i -> bytes 16 i):
-//   activation tile [BM][kBK] bf16, rows of 128 B: chunk c of row r sits at
-//     position c ^ ((r >> 1) & 7), so the 16 rows read by one ds_read_b128
-//     group land in 16 distinct 4-bank groups;
-//   weight tile [kBK][BN] bf16 per operand: chunk c of row k at c ^ swzB(k),
+//   activation tile [BM][BK] bf16, rows of BK * 2 bytes, XOR-swizzled per
+//     chunk (swz_a) so that the 16 rows read by one ds_read_b128 group land
+//     in 16 distinct 4-bank groups;
+//   weight tile [BK][BN] bf16 per operand: chunk c of row k at c ^ swzB(k),
 //     which puts the 4 rows read by one ds_read_b64_tr_b16 group in
 //     different banks.
-template <int BM_, int BN_, int WM_, int WN_, int NS_>
+template <int BM_, int BN_, int WM_, int WN_, int NS_, int BK_ = kBK>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NS = NS_;
+  // K depth of one stage: 64, or 32 (half the bytes per stage, so a ring of
+  // the same LDS holds twice the stages: more loads in flight for the
+  // weight-streaming shapes).  The activation tile's rows are BK * 2 bytes.
+  static constexpr int BK = BK_;
+  static_assert(BK == 64 || BK == 32, "stage depth");
+  static constexpr int ROW_BYTES = BK * 2;      // activation tile row pitch in LDS
+  static constexpr int CHUNKS = BK / 8;         // 16-byte chunks per activation row
   static constexpr int NWAVES = WM * WN;
   static constexpr int THREADS = 64 * NWAVES;
   static_assert(NWAVES == 4 || NWAVES == 8, "four or eight waves");
@@ -210,8 +217,8 @@ struct Tile {
   static constexpr int TM = MW / 16;
   static constexpr int TN = NW / 16;
   static_assert(TM >= 1 && TN >= 2 && TN % 2 == 0, "wave tile shape");
-  static constexpr int A_BYTES = BM * kBK * 2;
-  static constexpr int B_BYTES = kBK * BN * 2;
+  static constexpr int A_BYTES = BM * BK * 2;
+  static constexpr int B_BYTES = BK * BN * 2;
   static constexpr int A_DMA = A_BYTES / 1024 / NWAVES;  // 1 KB wave loads per wave and stage
   static constexpr int B_DMA = B_BYTES / 1024 / NWAVES;
   static_assert(A_DMA >= 1 && B_DMA >= 1 && A_BYTES % (1024 * NWAVES) == 0 && B_BYTES % (1024 * NWAVES) == 0,
@@ -224,7 +231,14 @@ struct Tile {
   static constexpr int dma_per_stage() { return A_DMA + NB * B_DMA; }
 };
 
-__device__ __forceinline__ int swz_a(int row) { return (row >> 1) & 7; }
+// Activation tile swizzle: 128-byte rows (BK = 64) put chunk c of row r at
+// c ^ ((r >> 1) & 7); 64-byte rows (BK = 32), four to a bank period, at
+// c ^ ((r >> 2) & 3).  Either way the 16 rows one ds_read_b128 group reads
+// land in 16 distinct 4-bank groups.
+template <int BK = kBK>
+__device__ __forceinline__ int swz_a(int row) {
+  return BK == 64 ? (row >> 1) & 7 : (row >> 2) & 3;
+}
 template <int BN>
 __device__ __forceinline__ int swz_b(int k) {
   return BN >= 128 ? 4 * (k & 3) : 4 * ((k >> 1) & 1);
@@ -347,7 +361,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
 #pragma unroll
       for (int j = 0; j < T::TM; ++j) acc[b][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = (kend - kbeg) / kBK;
+  const int nk = (kend - kbeg) / T::BK;
   if (nk <= 0) return;
 
   const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
@@ -358,9 +372,9 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   uint32_t a_off[T::A_DMA];
 #pragma unroll
   for (int j = 0; j < T::A_DMA; ++j) {
-    const int ch = wave + T::NWAVES * j;  // 1 KB chunk = 8 rows of 128 B
-    const int row = 8 * ch + (lane >> 3);
-    const int lc = (lane & 7) ^ swz_a(row);
+    const int ch = wave + T::NWAVES * j;  // 1 KB chunk = 8 rows of 128 B (16 rows of 64 B)
+    const int row = (1024 / T::ROW_BYTES) * ch + lane / T::CHUNKS;
+    const int lc = (lane % T::CHUNKS) ^ swz_a<T::BK>(row);
     int gr = m0 + row;
     gr = gr > mlast ? mlast : gr;
     a_off[j] = (uint32_t)(((long)gr * lda + 8 * lc) * 2);
@@ -377,7 +391,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   }
 
   auto issue = [&](int st) {
-    const int k = kbeg + st * kBK;
+    const int k = kbeg + st * T::BK;
     const uint32_t sbase = lds_base + (uint32_t)((st % T::NS) * SB);
 #pragma unroll
     for (int b = 0; b < NB; ++b)
@@ -401,8 +415,8 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   //     lane 4r+c of group g addresses row 8g+r (+4 for the upper half), columns 8c + 4*t2 .. +3,
   //     and receives column (8*(i/4) + 4*t2 + i%4) of those 4 rows, i = lane % 16.
   const int arow = wm * T::MW + (lane & 15);
-  const int a_frag0 = arow * 128 + (((lane >> 4) ^ swz_a(arow)) << 4);          // ks = 0
-  const int a_frag1 = arow * 128 + (((4 + (lane >> 4)) ^ swz_a(arow)) << 4);    // ks = 1
+  const int a_frag0 = arow * T::ROW_BYTES + (((lane >> 4) ^ swz_a<T::BK>(arow)) << 4);        // ks = 0
+  const int a_frag1 = arow * T::ROW_BYTES + (((4 + (lane >> 4)) ^ swz_a<T::BK>(arow)) << 4);  // ks = 1 (BK = 64)
   const int g = lane >> 4, r4 = (lane & 15) >> 2, c4 = lane & 3;
   const int brow = 8 * g + r4;
   int b_frag[T::TN / 2];
@@ -426,15 +440,15 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     return (bf16x8)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   };
   auto act_frag = [&](const char* base, int ks, int tm) {
-    return *reinterpret_cast<const bf16x8*>(base + (ks ? a_frag1 : a_frag0) + tm * 16 * 128);
+    return *reinterpret_cast<const bf16x8*>(base + (ks ? a_frag1 : a_frag0) + tm * 16 * T::ROW_BYTES);
   };
   auto compute = [&](int st) {
     const char* base = lds + (st % T::NS) * SB;
     if constexpr (T::NS == 2) {
-      bf16x8 xf[kBK / 32][T::TM];
-      bf16x8 wf[kBK / 32][NB][T::TN];
+      bf16x8 xf[T::BK / 32][T::TM];
+      bf16x8 wf[T::BK / 32][NB][T::TN];
 #pragma unroll
-      for (int ks = 0; ks < kBK / 32; ++ks) {
+      for (int ks = 0; ks < T::BK / 32; ++ks) {
 #pragma unroll
         for (int tm = 0; tm < T::TM; ++tm) xf[ks][tm] = act_frag(base, ks, tm);
 #pragma unroll
@@ -443,7 +457,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
           for (int i = 0; i < T::TN; ++i) wf[ks][b][i] = weight_frag(base, ks, b, i);
       }
 #pragma unroll
-      for (int ks = 0; ks < kBK / 32; ++ks)
+      for (int ks = 0; ks < T::BK / 32; ++ks)
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -453,7 +467,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
               acc[b][i][tm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[ks][b][i], xf[ks][tm], acc[b][i][tm], 0, 0, 0);
     } else {
 #pragma unroll
-      for (int ks = 0; ks < kBK / 32; ++ks) {
+      for (int ks = 0; ks < T::BK / 32; ++ks) {
         bf16x8 xf[T::TM];
 #pragma unroll
         for (int tm = 0; tm < T::TM; ++tm) xf[tm] = act_frag(base, ks, tm);
@@ -483,7 +497,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
       // The stage's activation pieces this wave loaded are in LDS: check them
       // (and reload any piece that still holds a sentinel) before the barrier
       // hands the stage to the other waves.
-      const int k = kbeg + it * kBK;
+      const int k = kbeg + it * T::BK;
       const uint32_t sbase = lds_base + (uint32_t)((it % T::NS) * SB);
       check.template operator()<T>(A, a_off, k, sbase, lds + (it % T::NS) * SB, wave, lane);
     }
@@ -505,15 +519,22 @@ struct SentinelCheck {
   static constexpr bool kCoherentA = true;
   uint32_t* err;  // CTRL_ERROR word
   uint32_t spin_limit;
+  TraceAcc* tr;   // re-read time is counted as flag-wait time (trace builds)
   template <class T>
   __device__ __forceinline__ void operator()(const uint16_t* A, const uint32_t (&a_off)[T::A_DMA], int k,
                                              uint32_t sbase, const char* stage, int wave, int lane) {
 #pragma unroll
     for (int j = 0; j < T::A_DMA; ++j) {
       const int piece = (wave + T::NWAVES * j) * 1024;
+      const uint64_t t0 = trace_now();
       for (uint32_t tries = 0;; ++tries) {
         const u32x4 v = *reinterpret_cast<const u32x4*>(stage + piece + 16 * lane);
-        if (__builtin_amdgcn_ballot_w64(has_sentinel(v)) == 0) break;  // the same in every lane
+        if (__builtin_amdgcn_ballot_w64(has_sentinel(v)) == 0) {  // the same in every lane
+          if constexpr (kTrace) {
+            if (tries) tr->flag += trace_now() - t0;
+          }
+          break;
+        }
         if (tries >= spin_limit || ((tries & 63u) == 63u && uniform(ld_relaxed(err)) != 0u)) {
           if (lane == 0) __hip_atomic_fetch_or(err, 4u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           break;

@@ -173,7 +173,7 @@ __device__ __forceinline__ void gemm1_item(const Args& a, int id_in, uint32_t ep
   Bp[0] = a.W1;
   if constexpr (NB == 2) Bp[1] = a.W1 + (long)a.H * a.F;
   NoWait nowait;  // a GEMM1 item never waits
-  ClaimAtLastStage<NoWait> hook{nowait, &next, kend - kBK};
+  ClaimAtLastStage<NoWait> hook{nowait, &next, kend - T::BK};
   mainloop<T, NB>(a.X, a.H, m0, a.M - 1, Bp, a.F, n0, kbeg, kend, acc, lds, hook, tr);
   if constexpr (kTrace) tr_mark_mainloop(tr);
 
@@ -239,18 +239,18 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
     // Sentinel mode: no ready counters; each stage's Z pieces are loaded at
     // device scope and checked for sentinels before the stage is used.
     NoWait nowait;
-    ClaimAtLastStage<NoWait, C> hook{nowait, &next, kend - kBK};
-    SentinelCheck check{a.ctrl + CTRL_ERROR, a.spin_limit};
+    ClaimAtLastStage<NoWait, C> hook{nowait, &next, kend - T::BK};
+    SentinelCheck check{a.ctrl + CTRL_ERROR, a.spin_limit, &tr};
     mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr, check);
   } else if constexpr (WAIT) {
     // ready counters advance once per run of every mode but the sentinel mode
     ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1, ready_runs + 1u, a.spin_limit,
                 s_slot, 0, &tr};
-    ClaimAtLastStage<ReadyWait, C> hook{w, &next, kend - kBK};
+    ClaimAtLastStage<ReadyWait, C> hook{w, &next, kend - T::BK};
     mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   } else {
     NoWait nowait;
-    ClaimAtLastStage<NoWait, C> hook{nowait, &next, kend - kBK};
+    ClaimAtLastStage<NoWait, C> hook{nowait, &next, kend - T::BK};
     mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   }
   if constexpr (kTrace) tr_mark_mainloop(tr);
@@ -464,7 +464,8 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
 
 // ------------------------------------------------------------------ dispatch table
 
-// Tile shapes by (rows, columns, ring depth, waves).
+// Tile shapes by (rows, columns, ring depth, waves); the stage depth is a
+// parameter of the eight-wave shapes (TileForK).
 template <int BM, int BN, int NS, int W = 4>
 struct TileFor;
 template <int NS> struct TileFor<32, 64, NS> { using type = Tile<32, 64, 2, 2, NS>; };
@@ -487,9 +488,14 @@ template <int NS> struct TileFor<128, 128, NS, 8> { using type = Tile<128, 128, 
 template <int NS> struct TileFor<128, 64, NS, 8> { using type = Tile<128, 64, 4, 2, NS>; };
 template <int NS> struct TileFor<64, 256, NS, 8> { using type = Tile<64, 256, 2, 4, NS>; };
 template <int NS> struct TileFor<32, 256, NS, 8> { using type = Tile<32, 256, 1, 8, NS>; };
+template <int BM, int BN, int NS, int W, int BK>
+struct TileForK {
+  using base = typename TileFor<BM, BN, NS, W>::type;
+  using type = Tile<BM, BN, base::WM, base::WN, NS, BK>;
+};
 
 struct Entry {
-  int bm, bn1, bn2, nb, ns, waves;
+  int bm, bn1, bn2, nb, ns, waves, bk;
   const void* seq1;
   const void* seq2;
   const void* pipe;
@@ -499,15 +505,18 @@ struct Entry {
 
 // GEMM2 of BN2 columns as one tile (HV = 1), or as two halves of BN2 / 2 that
 // share the GEMM1 tile shape (HV = 2).
-#define MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PH)                                                                   \
-  (const void*)&k_mlp2<typename TileFor<BM, BN1, NS, W>::type, NB, typename TileFor<BM, (BN2) / (HV), NS, W>::type, \
-                       HV, PH>
-#define MLP2_ENTRY_W(BM, BN1, BN2, NB, NS, HV, W)                                                                 \
-  Entry {                                                                                                         \
-    BM, BN1, BN2, NB, NS, W, MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_GEMM1),                                   \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_GEMM2), MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_PIPELINED), \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_WORKQUEUE), MLP2_K(BM, BN1, BN2, NB, NS, HV, W, PHASE_SENTINEL) \
+#define MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PH)                                          \
+  (const void*)&k_mlp2<typename TileForK<BM, BN1, NS, W, BK>::type, NB,                       \
+                       typename TileForK<BM, (BN2) / (HV), NS, W, BK>::type, HV, PH>
+#define MLP2_ENTRY_WK(BM, BN1, BN2, NB, NS, HV, W, BK)                                        \
+  Entry {                                                                                     \
+    BM, BN1, BN2, NB, NS, W, BK, MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_GEMM1),       \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_GEMM2),                                 \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_PIPELINED),                             \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_WORKQUEUE),                             \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_SENTINEL)                               \
   }
+#define MLP2_ENTRY_W(BM, BN1, BN2, NB, NS, HV, W) MLP2_ENTRY_WK(BM, BN1, BN2, NB, NS, HV, W, 64)
 #define MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, HV) MLP2_ENTRY_W(BM, BN1, BN2, NB, NS, HV, 4)
 #define MLP2_ENTRY(BM, BN1, BN2, NB, NS) MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, 1)
 
@@ -533,11 +542,16 @@ static const Entry kEntries[] = {
     MLP2_ENTRY_W(256, 128, 256, 2, 2, 2, 8), MLP2_ENTRY_W(256, 64, 128, 2, 3, 2, 8),
     MLP2_ENTRY_W(128, 128, 128, 1, 4, 1, 8), MLP2_ENTRY_W(128, 256, 256, 1, 3, 1, 8),
     MLP2_ENTRY_W(128, 64, 64, 1, 4, 1, 8),
+    // 32-deep stages: twice the ring depth in the same LDS (measured slower
+    // than 64-deep stages on every workload: one barrier per half the work)
+    MLP2_ENTRY_WK(256, 128, 256, 2, 4, 2, 8, 32), MLP2_ENTRY_WK(128, 64, 64, 1, 8, 1, 4, 32),
 };
 
 static const Entry* find_entry(const KernelConfig& c) {
   for (const Entry& e : kEntries)
-    if (e.bm == c.bm && e.bn1 == c.bn1 && e.bn2 == c.bn2 && e.nb == c.nb && e.ns == c.ns && e.waves == c.waves) return &e;
+    if (e.bm == c.bm && e.bn1 == c.bn1 && e.bn2 == c.bn2 && e.nb == c.nb && e.ns == c.ns && e.waves == c.waves &&
+        e.bk == c.bk)
+      return &e;
   return nullptr;
 }
 
@@ -575,11 +589,11 @@ __device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int ti
   if (c.wait && L.ready_in) {
     ReadyWait w{L.ready_in, a.ctrl + CTRL_ERROR, mb, a.Mb, T::BN, (K - 1) / T::BN, epoch + 1u, a.spin_limit, s_slot,
                 0, &tr};
-    ClaimAtLastStage<ReadyWait> hook{w, &next, K - kBK};
+    ClaimAtLastStage<ReadyWait> hook{w, &next, K - T::BK};
     mainloop<T, 1>(L.A, K, m0, L.alast, Bp, L.N, n0, 0, K, acc, lds, hook, tr);
   } else {
     NoWait nowait;
-    ClaimAtLastStage<NoWait> hook{nowait, &next, K - kBK};
+    ClaimAtLastStage<NoWait> hook{nowait, &next, K - T::BK};
     mainloop<T, 1>(L.A, K, m0, L.alast, Bp, L.N, n0, 0, K, acc, lds, hook, tr);
   }
   if constexpr (kTrace) tr_mark_mainloop(tr);

@@ -8,10 +8,10 @@
 namespace mlp2 {
 
 // A compiled kernel family: row block, GEMM1 / GEMM2 column-block widths, the
-// number of GEMM1 weight operands (2 for SwiGLU), the LDS ring depth and the
-// waves per work-group (4 or 8).
+// number of GEMM1 weight operands (2 for SwiGLU), the LDS ring depth, the
+// waves per work-group (4 or 8) and the K depth of a stage (64 or 32).
 struct KernelConfig {
-  int bm, bn1, bn2, nb, ns, waves;
+  int bm, bn1, bn2, nb, ns, waves, bk;
 };
 
 bool config_supported(const KernelConfig& c);

@@ -6,7 +6,8 @@ Needs the trace build (``python -m paper_2607_07862_amd.build --trace``) and
 a GPU.  For each workload (device-drawn inputs of its shapes): warm-up runs,
 then one traced warm run per mode.  Per item kind it reports the mean item
 time split into mainloop, waits for the work-group's own ring loads, flag
-waits (ready counters in the pipelined mode; in the workqueue mode the wait
+waits (ready counters in the pipelined mode; re-reads of intermediate pieces
+still holding the sentinel in the sentinel mode; in the workqueue mode the wait
 for the popped queue slot to fill, counted from when the work-group began to
 pop) and epilogue, the item's core clock cycles and the clock they imply
 (cycles over real time), and for the GEMM2 items of the two one-launch modes
@@ -78,10 +79,11 @@ def summarise(B, I, bench, key):
     for _ in range(5):
         r.run(B.MODE_TILE_PIPELINED)
         r.run(B.MODE_SEQUENTIAL)
+        r.run(B.MODE_SENTINEL)
     torch.cuda.synchronize()
     rows, clocks = [], []
     for mode, name in ((B.MODE_SEQUENTIAL, "sequential"), (B.MODE_TILE_PIPELINED, "pipelined"),
-                       (B.MODE_WORKQUEUE, "workqueue")):
+                       (B.MODE_WORKQUEUE, "workqueue"), (B.MODE_SENTINEL, "sentinel")):
         buf.zero_()
         r.plan.attach_trace(buf, CAP)
         r.run(mode)
@@ -210,8 +212,9 @@ def main():
             "```", cmd, "```", "",
             "Times are means over the items of a kind; the flag share is the kind's flag-wait time over its item",
             "time (pipelined: waits on ready counters; workqueue: the wait for the popped queue slot to fill, the",
-            "item starting when its work-group began to pop); the producer-implied wait is, per GEMM2 item of the",
-            "two one-launch modes, the latest end among the GEMM1 items writing the Z columns it reads minus its",
+            "item starting when its work-group began to pop; sentinel: re-reads of Z pieces that still held the",
+            "sentinel); the producer-implied wait is, per GEMM2 item of the",
+            "one-launch modes, the latest end among the GEMM1 items writing the Z columns it reads minus its",
             "start (0 when they were done before it started).  Cycles are the item's core clock cycles",
             "(shader-clock counter); the clock is cycles over the item's real time.", ""]
     chain_lines = []

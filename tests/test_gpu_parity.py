@@ -55,6 +55,10 @@ SMALL = [
     (130, 512, 1024, 1, {"waves": 8, "bm": 128, "bn1": 128, "bn2": 128, "stages": 4, "splitk1": 2, "splitk2": 2}),
     (100, 1024, 768, 0, {"waves": 8, "bm": 128, "bn1": 256, "bn2": 256, "stages": 3, "splitk1": 2}),
     (90, 256, 384, 1, {"waves": 8, "bm": 128, "bn1": 64, "bn2": 64, "stages": 4}),
+    # 32-deep stages (64-byte activation rows, twice the ring depth)
+    (200, 512, 640, 2, {"waves": 8, "bm": 256, "bn1": 128, "bn2": 256, "stages": 4, "bk": 32, "splitk2": 3}),
+    (77, 320, 448, 0, {"bm": 128, "bn1": 64, "bn2": 64, "stages": 8, "bk": 32, "splitk2": 2}),
+    (300, 256, 512, 1, {"bm": 128, "bn1": 64, "bn2": 64, "stages": 8, "bk": 32, "splitk1": 2}),
 ]
 
 
