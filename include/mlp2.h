@@ -208,7 +208,9 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
  * every mode uses the same groups, so the modes still agree bit for bit. */
 int mlp2_run(mlp2_plan_t plan, const void* X, const void* W1, const void* W2, void* Y, void* stream, int mode);
 
-/* Free the plan and its workspace (synchronises the device first).  NULL-safe. */
+/* Free the plan and its workspace.  NULL-safe.  It first waits for all work on
+ * the plan's device: the plan does not record which streams ran it, and no
+ * kernel of it may still use the workspace when it is freed. */
 void mlp2_destroy(mlp2_plan_t plan);
 
 /* Code of the last failing call on this host thread (MLP2_OK if none). */
@@ -219,7 +221,9 @@ const char* mlp2_strerror(int code);
 
 /* After the caller has synchronised the stream: MLP2_OK, or MLP2_ERR_TIMEOUT
  * if a flag wait gave up during an earlier run.  On a timeout it clears the
- * latched error and resets the plan's counters so the plan is usable again. */
+ * latched error and resets the plan's counters so the plan is usable again
+ * (the reset runs on the null stream, and the call waits for that stream
+ * only). */
 int mlp2_check(mlp2_plan_t plan);
 
 /* Fill *out with what the plan chose. */

@@ -833,8 +833,9 @@ int mlp2_check(mlp2_plan_t p) {
   // Recover: counters and epoch back to zero, both sentinel intermediates
   // back to sentinels (the stream is idle by contract).
   const size_t zs_bytes = p->Zs ? (size_t)2 * p->Mb * p->kc.bm * p->F * 2 : 0;
-  if (hipMemset((char*)p->ws + p->counters_off, 0, p->counters_bytes) != hipSuccess ||
-      (zs_bytes && hipMemset(p->Zs, 0xFF, zs_bytes) != hipSuccess) || hipDeviceSynchronize() != hipSuccess)
+  if (hipMemsetAsync((char*)p->ws + p->counters_off, 0, p->counters_bytes, nullptr) != hipSuccess ||
+      (zs_bytes && hipMemsetAsync(p->Zs, 0xFF, zs_bytes, nullptr) != hipSuccess) ||
+      hipStreamSynchronize(nullptr) != hipSuccess)
     return fail(MLP2_ERR_HIP);
   return fail(MLP2_ERR_TIMEOUT);
 }
@@ -1226,7 +1227,8 @@ int mlp2_chain_check(mlp2_chain_t p) {
   uint32_t ctrl[mlp2::CTRL_WORDS];
   if (hipMemcpy(ctrl, p->ctrl, sizeof(ctrl), hipMemcpyDeviceToHost) != hipSuccess) return fail(MLP2_ERR_HIP);
   if (ctrl[mlp2::CTRL_ERROR] == 0) return MLP2_OK;
-  if (hipMemset((char*)p->ws + p->counters_off, 0, p->counters_bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+  if (hipMemsetAsync((char*)p->ws + p->counters_off, 0, p->counters_bytes, nullptr) != hipSuccess ||
+      hipStreamSynchronize(nullptr) != hipSuccess)
     return fail(MLP2_ERR_HIP);
   return fail(MLP2_ERR_TIMEOUT);
 }

@@ -33,13 +33,15 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def short_name(n: str) -> str:
-    m = re.search(r"k_mlp2<mlp2::Tile<(\d+), (\d+), (\d+), (\d+), (\d+)>, (\d), mlp2::Tile<(\d+), (\d+), \d+, \d+, \d+>, (\d), (\d)>", n)
+    m = re.search(r"k_mlp2<mlp2::Tile<(\d+), (\d+), (\d+), (\d+), (\d+)(?:, (\d+))?>, (\d), "
+                  r"mlp2::Tile<(\d+), (\d+), \d+, \d+, \d+(?:, \d+)?>, (\d), (\d)>", n)
     if m:
-        phase = ["gemm1", "gemm2", "pipelined", "workqueue"][int(m.group(10))]
-        bn2 = int(m.group(8)) * int(m.group(9))
+        phase = ["gemm1", "gemm2", "pipelined", "workqueue", "sentinel"][int(m.group(11))]
+        bn2 = int(m.group(9)) * int(m.group(10))
         waves = int(m.group(3)) * int(m.group(4))
-        return (f"k_mlp2 {phase} (bm {m.group(1)}, bn1 {m.group(2)}, bn2 {bn2}, nb {m.group(6)}, stages {m.group(5)}, "
-                f"waves {waves})")
+        bk = f", bk {m.group(6)}" if m.group(6) and m.group(6) != "64" else ""
+        return (f"k_mlp2 {phase} (bm {m.group(1)}, bn1 {m.group(2)}, bn2 {bn2}, nb {m.group(7)}, stages {m.group(5)}, "
+                f"waves {waves}{bk})")
     return n if len(n) < 90 else n[:87] + "..."
 
 
@@ -176,8 +178,48 @@ def counters(args):
             if per[k][hit] and per[k][miss]:
                 h, m = sum(per[k][hit]) / len(per[k][hit]), sum(per[k][miss]) / len(per[k][miss])
                 lines.append(f"- {short_name(k)}: {100 * h / (h + m):.1f} %")
+    lines += derived_lines(per)
     open(args.out, "w").write("\n".join(lines) + "\n")
     print(args.out)
+
+
+# MI355X: 8 XCDs of 32 CUs, 4 SIMDs per CU.  GRBM_GUI_ACTIVE is collected per
+# XCD and summed, so one XCD's active cycles are an eighth of it.
+XCDS, CUS, SIMDS = 8, 256, 1024
+
+
+def derived_lines(per) -> list:
+    """Utilisations over the kernel's active cycles (per-dispatch means).
+
+    * MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES (summed over SIMDs; a
+      v_mfma_f32_16x16x32_bf16 counts the 16 cycles it holds its SIMD) over
+      the cycles of all 1024 SIMDs;
+    * texture-data busy: TD_TD_BUSY (summed over CUs) over the cycles of all
+      256 CUs.
+    """
+    def mean(k, c):
+        v = per[k].get(c) or []
+        return sum(v) / len(v) if v else None
+
+    out = []
+    for k in sorted(per, key=short_name):
+        g = mean(k, "GRBM_GUI_ACTIVE")
+        if not g:
+            continue
+        cyc = g / XCDS
+        parts = []
+        b = mean(k, "SQ_VALU_MFMA_BUSY_CYCLES")
+        if b is not None:
+            parts.append(f"MFMA busy {100 * b / (cyc * SIMDS):.1f} %")
+        t = mean(k, "TD_TD_BUSY")
+        if t is not None:
+            parts.append(f"texture-data busy {100 * t / (cyc * CUS):.1f} %")
+        if parts:
+            out.append(f"- {short_name(k)}: " + ", ".join(parts) + f" (over {cyc:,.0f} active cycles per XCD)")
+    if out:
+        out = ["", "Utilisation over the kernel's active cycles (GRBM_GUI_ACTIVE / 8 per XCD; MFMA busy over "
+               "1024 SIMDs, texture-data busy over 256 CUs):", ""] + out
+    return out
 
 
 def main():

@@ -28,6 +28,11 @@ def test_short_names():
     assert P.short_name(GATED2) == "k_mlp2 gemm2 (bm 256, bn1 64, bn2 128, nb 2, stages 3, waves 4)"
     wide = "void mlp2::k_mlp2<mlp2::Tile<256, 256, 2, 4, 2>, 1, mlp2::Tile<256, 256, 2, 4, 2>, 1, 2>(mlp2::Args)"
     assert P.short_name(wide) == "k_mlp2 pipelined (bm 256, bn1 256, bn2 256, nb 1, stages 2, waves 8)"
+    # the stage depth as a sixth tile parameter (named only when it is not 64), the sentinel phase
+    deep = "void mlp2::k_mlp2<mlp2::Tile<256, 128, 4, 2, 2, 64>, 2, mlp2::Tile<256, 128, 4, 2, 2, 64>, 2, 4>(mlp2::Args)"
+    assert P.short_name(deep) == "k_mlp2 sentinel (bm 256, bn1 128, bn2 256, nb 2, stages 2, waves 8)"
+    bk32 = "void mlp2::k_mlp2<mlp2::Tile<128, 64, 2, 2, 8, 32>, 1, mlp2::Tile<128, 64, 2, 2, 8, 32>, 1, 3>(mlp2::Args)"
+    assert P.short_name(bk32) == "k_mlp2 workqueue (bm 128, bn1 64, bn2 64, nb 1, stages 8, waves 4, bk 32)"
     assert P.short_name("x" * 200).endswith("...")
 
 
@@ -73,3 +78,19 @@ def test_stats_table(tmp_path):
     text = open(out).read()
     assert "| k_mlp2 pipelined (bm 128, bn1 64, bn2 64, nb 1, stages 4, waves 4) | 10 | 75.00 | 70.00 | 90.00 | 61.5 % |" in text
     assert "the cmd" in text
+
+
+def test_counter_utilisations(tmp_path):
+    # two dispatches of 1000 cycles per XCD; MFMA busy half of every SIMD's cycles,
+    # the texture-data units a quarter of every CU's; two passes merged per kernel
+    a, b = str(tmp_path / "mfma"), str(tmp_path / "path")
+    _counters(a, [(1, PIPE, "GRBM_GUI_ACTIVE", 8000), (1, PIPE, "SQ_VALU_MFMA_BUSY_CYCLES", 1024 * 500),
+                  (2, PIPE, "GRBM_GUI_ACTIVE", 8000), (2, PIPE, "SQ_VALU_MFMA_BUSY_CYCLES", 1024 * 500),
+                  (3, COPY, "GRBM_GUI_ACTIVE", 10)])
+    _counters(b, [(5, PIPE, "GRBM_GUI_ACTIVE", 8000), (5, PIPE, "TD_TD_BUSY", 256 * 250)])
+    out = str(tmp_path / "c.md")
+    P.counters(argparse.Namespace(dirs=[a, b], out=out, cmd=["pass 1", "pass 2"], title="t"))
+    text = open(out).read()
+    assert ("- k_mlp2 pipelined (bm 128, bn1 64, bn2 64, nb 1, stages 4, waves 4): MFMA busy 50.0 %, "
+            "texture-data busy 25.0 % (over 1,000 active cycles per XCD)") in text
+    assert "pass 1" in text and "pass 2" in text and COPY not in text
