@@ -81,8 +81,11 @@ enum mlp2_dtype { MLP2_DTYPE_BF16 = 0 };
  * of the sequential mode alone, for callers that schedule the two stages
  * themselves (e.g. a micro-batch pipeline over chunks of rows on two streams,
  * one plan per chunk).  The caller orders a plan's STAGE2 after its STAGE1
- * (same stream, or an event), and the pair after the plan's previous run;
- * together they compute what MLP2_MODE_SEQUENTIAL computes, bit for bit.
+ * (same stream, or an event), and the pair after the plan's previous run:
+ * every STAGE1 is followed by its STAGE2 before the plan runs again (the
+ * device epoch advances with STAGE2, so two STAGE1 runs in a row leave the
+ * split-K arrival counts past their targets).  Together they compute what
+ * MLP2_MODE_SEQUENTIAL computes, bit for bit.
  * Not for plans run in row groups (MLP2_ERR_UNSUPPORTED). */
 enum mlp2_mode {
   MLP2_MODE_SEQUENTIAL = 0,
@@ -154,7 +157,8 @@ typedef struct mlp2_tuning {
                     item from one rank order); else work-groups with index g % 64 < p1
                     take only GEMM1 items and the others only GEMM2 items (a static
                     producer / consumer split of the grid, p1 in 1..63 of every 64)       */
-  int bk;        /* K depth of one LDS stage: 64 or 32 (as built for the shape)            */
+  int bk;        /* K depth of one LDS stage: 64, 32 or 128 (as built for the shape; 128   */
+                 /* only where H and F are multiples of 128)                               */
   int reserved[1];
 } mlp2_tuning_t;
 

@@ -93,10 +93,10 @@ bool roles_ok(int p1, int grid) {
 // Split K into S ranges of kc (a multiple of the stage depth): as many parts
 // as keep the tile count times S within `want` items (one round of the
 // persistent grid), each range at least `min_k` deep.  Returns S and sets *kc.
-int choose_split(int64_t K, int tiles, int want, int min_k, int* kc) {
+int choose_split(int64_t K, int tiles, int want, int min_k, int gran, int* kc) {
   int S = std::max(1, want / std::max(1, tiles));
   S = std::min<int64_t>(S, std::max<int64_t>(1, K / min_k));
-  int64_t k = align_up((size_t)ceil_div(K, S), mlp2::kBK);
+  int64_t k = align_up((size_t)ceil_div(K, S), gran);
   *kc = (int)k;
   return ceil_div(K, k);
 }
@@ -380,7 +380,7 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   if (tz.bm < 0 || tz.bn1 < 0 || tz.bn2 < 0 || tz.splitk1 < 0 || tz.splitk2 < 0 || tz.grid < 0 || tz.order < 0 || tz.stages < 0 ||
       tz.order > MLP2_ORDER_BANDED || tz.row_group < -1 || (tz.row_group > 0 && tz.row_group % 256) ||
       (tz.waves != 0 && tz.waves != 4 && tz.waves != 8) || tz.lag < -1 || tz.p1 < 0 || tz.p1 > 63 || tz.p1 % 8 ||
-      (tz.bk != 0 && tz.bk != 32 && tz.bk != 64)) {
+      (tz.bk != 0 && tz.bk != 32 && tz.bk != 64 && tz.bk != 128)) {
     fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
   }
@@ -516,7 +516,9 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
     for (const auto& c : cand) {
       KernelConfig k{tz.bm ? tz.bm : c[0], tz.bn1 ? tz.bn1 : c[1], tz.bn2 ? tz.bn2 : c[2], nb,
                      tz.stages ? tz.stages : c[3], tz.waves ? tz.waves : c[4], tz.bk ? tz.bk : pass ? 64 : bk};
-      if (F % k.bn1 == 0 && H % k.bn2 == 0 && mlp2::config_supported(k)) {
+      // 128-deep stages need every K range (H; F; the split-K parts) in whole stages
+      if (F % k.bn1 == 0 && H % k.bn2 == 0 && (k.bk < 128 || (H % k.bk == 0 && F % k.bk == 0)) &&
+          mlp2::config_supported(k)) {
         p->kc = k;
         found = true;
         break;
@@ -539,17 +541,18 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
     if (mlp2::occupancy(p->kc, w, &occ[w]) != hipSuccess || occ[w] < 1) return MLP2_ERR_HIP;
   }
   const int tiles1 = p->Mb * p->Nb1, tiles2 = p->Mb * p->Nb2;
+  const int gran = std::max(mlp2::kBK, p->kc.bk);  // split-K parts hold whole stages
   if (tz.splitk1) {
-    p->kc1 = (int)align_up((size_t)ceil_div(H, tz.splitk1), mlp2::kBK);
+    p->kc1 = (int)align_up((size_t)ceil_div(H, tz.splitk1), gran);
     p->S1 = ceil_div(H, p->kc1);
   } else {
-    p->S1 = choose_split(H, tiles1, occ[0] * p->num_cus, min_k1, &p->kc1);
+    p->S1 = choose_split(H, tiles1, occ[0] * p->num_cus, min_k1, gran, &p->kc1);
   }
   if (tz.splitk2) {
-    p->kc2 = (int)align_up((size_t)ceil_div(F, tz.splitk2), mlp2::kBK);
+    p->kc2 = (int)align_up((size_t)ceil_div(F, tz.splitk2), gran);
     p->S2 = ceil_div(F, p->kc2);
   } else {
-    p->S2 = choose_split(F, tiles2, occ[1] * p->num_cus, min_k2, &p->kc2);
+    p->S2 = choose_split(F, tiles2, occ[1] * p->num_cus, min_k2, gran, &p->kc2);
   }
   p->order = tz.order;
   p->lag = tz.lag;

@@ -31,7 +31,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
 
-constexpr int kBK = 64;        // K granularity of the plans (split-K ranges); the deepest LDS stage
+constexpr int kBK = 64;        // K granularity of the plans (split-K ranges); a plan whose tiles take
+                               // 128-deep stages keeps its K ranges multiples of 128
 
 // Words per 128-byte line.  Every counter that work-groups update with device-
 // scope atomics sits on a line of its own: such atomics are performed at the
@@ -200,11 +201,13 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 template <int BM_, int BN_, int WM_, int WN_, int NS_, int BK_ = kBK>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NS = NS_;
-  // K depth of one stage: 64, or 32 (half the bytes per stage, so a ring of
-  // the same LDS holds twice the stages: more loads in flight for the
-  // weight-streaming shapes).  The activation tile's rows are BK * 2 bytes.
+  // K depth of one stage: 64; 32 (half the bytes per stage, so a ring of the
+  // same LDS holds twice the stages); or 128 (twice the products per stage
+  // for the same per-stage costs: the wait, the barrier, the DMA issue and
+  // the first fragment reads, which a small tile with one wave per SIMD pays
+  // in series).  The activation tile's rows are BK * 2 bytes.
   static constexpr int BK = BK_;
-  static_assert(BK == 64 || BK == 32, "stage depth");
+  static_assert(BK == 128 || BK == 64 || BK == 32, "stage depth");
   static constexpr int ROW_BYTES = BK * 2;      // activation tile row pitch in LDS
   static constexpr int CHUNKS = BK / 8;         // 16-byte chunks per activation row
   static constexpr int NWAVES = WM * WN;
@@ -231,13 +234,14 @@ struct Tile {
   static constexpr int dma_per_stage() { return A_DMA + NB * B_DMA; }
 };
 
-// Activation tile swizzle: 128-byte rows (BK = 64) put chunk c of row r at
+// Activation tile swizzle: 256-byte rows (BK = 128), one to a bank period,
+// put chunk c of row r at c ^ (r & 15); 128-byte rows (BK = 64) at
 // c ^ ((r >> 1) & 7); 64-byte rows (BK = 32), four to a bank period, at
 // c ^ ((r >> 2) & 3).  Either way the 16 rows one ds_read_b128 group reads
 // land in 16 distinct 4-bank groups.
 template <int BK = kBK>
 __device__ __forceinline__ int swz_a(int row) {
-  return BK == 64 ? (row >> 1) & 7 : (row >> 2) & 3;
+  return BK == 128 ? row & 15 : BK == 64 ? (row >> 1) & 7 : (row >> 2) & 3;
 }
 template <int BN>
 __device__ __forceinline__ int swz_b(int k) {
@@ -325,11 +329,12 @@ __device__ __forceinline__ void wait_stages_behind(int after) {
 // are never stored).  `wait(k)` runs, in every wave, before the activation
 // operand of the stage starting at k is requested (after its weight loads).
 //
-// Pipeline: stages k0, k0 + kBK, ... are loaded NS - 1 ahead of use.  At
+// Pipeline: stages k0, k0 + BK, ... are loaded NS - 1 ahead of use.  At
 // iteration it a wave waits for its own loads of stage it, a barrier makes
 // every wave's loads of stage it visible and retires every wave's reads of
 // stage it - 1, then the loads of stage it + NS - 1 go into that freed buffer
-// and stage it is multiplied.
+// and stage it is multiplied.  Four-wave tiles with three or more stages read
+// one stage ahead into registers instead (below), and keep NS stages loading.
 // A stage check that does nothing (every mode but the sentinel mode).
 struct NoCheck {
   static constexpr bool kCoherentA = false;
@@ -372,7 +377,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   uint32_t a_off[T::A_DMA];
 #pragma unroll
   for (int j = 0; j < T::A_DMA; ++j) {
-    const int ch = wave + T::NWAVES * j;  // 1 KB chunk = 8 rows of 128 B (16 rows of 64 B)
+    const int ch = wave + T::NWAVES * j;  // 1 KB chunk = 8 rows of 128 B (4 of 256 B, 16 of 64 B)
     const int row = (1024 / T::ROW_BYTES) * ch + lane / T::CHUNKS;
     const int lc = (lane % T::CHUNKS) ^ swz_a<T::BK>(row);
     int gr = m0 + row;
@@ -399,7 +404,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
       for (int j = 0; j < T::B_DMA; ++j)
         dma16(Bp[b], b_off[j] + (uint32_t)((long)k * ldb * 2),
               uniform(sbase + (uint32_t)(T::A_BYTES + b * T::B_BYTES + (wave + T::NWAVES * j) * 1024)));
-    wait(k);
+    wait(k);  // covers the stage's columns [k, k + BK)
 #pragma unroll
     for (int j = 0; j < T::A_DMA; ++j) {
       if constexpr (Check::kCoherentA)
@@ -415,8 +420,10 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   //     lane 4r+c of group g addresses row 8g+r (+4 for the upper half), columns 8c + 4*t2 .. +3,
   //     and receives column (8*(i/4) + 4*t2 + i%4) of those 4 rows, i = lane % 16.
   const int arow = wm * T::MW + (lane & 15);
-  const int a_frag0 = arow * T::ROW_BYTES + (((lane >> 4) ^ swz_a<T::BK>(arow)) << 4);        // ks = 0
-  const int a_frag1 = arow * T::ROW_BYTES + (((4 + (lane >> 4)) ^ swz_a<T::BK>(arow)) << 4);  // ks = 1 (BK = 64)
+  int a_frag[T::BK / 32];  // K half ks: chunk 4 ks + lane / 16 of the row
+#pragma unroll
+  for (int ks = 0; ks < T::BK / 32; ++ks)
+    a_frag[ks] = arow * T::ROW_BYTES + (((4 * ks + (lane >> 4)) ^ swz_a<T::BK>(arow)) << 4);
   const int g = lane >> 4, r4 = (lane & 15) >> 2, c4 = lane & 3;
   const int brow = 8 * g + r4;
   int b_frag[T::TN / 2];
@@ -426,7 +433,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     b_frag[tp] = T::A_BYTES + brow * (2 * T::BN) + ((q ^ swz_b<T::BN>(brow)) << 4);
   }
 
-  // Two K halves of 32 per stage.  With a two-stage ring every fragment of
+  // K slices of 32 per stage (BK / 32 of them).  With a two-stage ring every fragment of
   // the stage is read before its first product: the reads of the second
   // half and of the later column pairs then overlap the first products in
   // whatever code the mainloop is inlined into (the one-launch kernels' item
@@ -440,7 +447,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     return (bf16x8)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   };
   auto act_frag = [&](const char* base, int ks, int tm) {
-    return *reinterpret_cast<const bf16x8*>(base + (ks ? a_frag1 : a_frag0) + tm * 16 * T::ROW_BYTES);
+    return *reinterpret_cast<const bf16x8*>(base + a_frag[ks] + tm * 16 * T::ROW_BYTES);
   };
   auto compute = [&](int st) {
     const char* base = lds + (st % T::NS) * SB;
@@ -484,25 +491,93 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     }
   };
 
+  // Own loads of stage st complete (the stages issued after it may stay in
+  // flight), then every wave's: the barrier also retires every wave's reads
+  // of the stages before st.
+  auto resident = [&](int st) {
+    const uint64_t t0 = trace_now();
+    wait_stages_behind<PER_STAGE, T::NS - 2>(min(T::NS - 2, nk - 1 - st));
+    if constexpr (!is_same_type<Check, NoCheck>::value) {
+      // The stage's activation pieces this wave loaded are in LDS: check them
+      // (and reload any piece that still holds a sentinel) before the barrier
+      // hands the stage to the other waves.
+      const int k = kbeg + st * T::BK;
+      const uint32_t sbase = lds_base + (uint32_t)((st % T::NS) * SB);
+      check.template operator()<T>(A, a_off, k, sbase, lds + (st % T::NS) * SB, wave, lane);
+    }
+    __syncthreads();
+    if constexpr (kTrace) tr.ring += trace_now() - t0;
+  };
+
   // Prologue: NS - 1 stages in flight.
 #pragma unroll
   for (int st = 0; st < T::NS - 1; ++st)
     if (st < nk) issue(st);
 
-  for (int it = 0; it < nk; ++it) {
-    const uint64_t t0 = trace_now();
-    // Own loads of stage `it` complete: the stages issued after it may stay in flight.
-    wait_stages_behind<PER_STAGE, T::NS - 2>(min(T::NS - 2, nk - 1 - it));
-    if constexpr (!is_same_type<Check, NoCheck>::value) {
-      // The stage's activation pieces this wave loaded are in LDS: check them
-      // (and reload any piece that still holds a sentinel) before the barrier
-      // hands the stage to the other waves.
-      const int k = kbeg + it * T::BK;
-      const uint32_t sbase = lds_base + (uint32_t)((it % T::NS) * SB);
-      check.template operator()<T>(A, a_off, k, sbase, lds + (it % T::NS) * SB, wave, lane);
+  if constexpr (T::NWAVES == 4 && T::NS >= 3) {
+    // One wave per SIMD: nothing else on the SIMD hides a stage's LDS read
+    // latency, so the fragments of stage it + 1 are read into a second set
+    // of registers while stage it is multiplied.  Stage it's slot is free
+    // once every wave holds its fragments (the barrier of stage it + 1), and
+    // takes the loads of stage it + NS.  Same products in the same order.
+    struct Frags {
+      bf16x8 x[T::BK / 32][T::TM];
+      bf16x8 w[T::BK / 32][NB][T::TN];
+    };
+    auto read = [&](Frags& f, int st) {
+      const char* base = lds + (st % T::NS) * SB;
+#pragma unroll
+      for (int ks = 0; ks < T::BK / 32; ++ks) {
+#pragma unroll
+        for (int tm = 0; tm < T::TM; ++tm) f.x[ks][tm] = act_frag(base, ks, tm);
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int i = 0; i < T::TN; ++i) f.w[ks][b][i] = weight_frag(base, ks, b, i);
+      }
+    };
+    auto mma = [&](const Frags& f) {
+#pragma unroll
+      for (int ks = 0; ks < T::BK / 32; ++ks)
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int i = 0; i < T::TN; ++i)
+#pragma unroll
+            for (int tm = 0; tm < T::TM; ++tm)
+              acc[b][i][tm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.w[ks][b][i], f.x[ks][tm], acc[b][i][tm], 0, 0, 0);
+    };
+    // Stage it is multiplied while stage it + 1 (< nk) is read.
+    auto advance = [&](int it, Frags& cur, Frags& nxt) {
+      resident(it + 1);
+      if (it + T::NS < nk) issue(it + T::NS);
+      read(nxt, it + 1);
+      mma(cur);
+    };
+    resident(0);
+    if (T::NS - 1 < nk) issue(T::NS - 1);
+    Frags fa, fb;
+    read(fa, 0);
+    // Two stages per trip, the fragment sets swapping roles; every trip reads
+    // a next stage, so both sets keep their registers (no conditional read
+    // merges into the products' control flow).
+    int it = 0;
+    for (; it + 2 < nk; it += 2) {
+      advance(it, fa, fb);
+      advance(it + 1, fb, fa);
     }
-    __syncthreads();
-    if constexpr (kTrace) tr.ring += trace_now() - t0;
+    if (it + 1 < nk) {  // two stages left
+      advance(it, fa, fb);
+      mma(fb);
+    } else {            // one stage left
+      mma(fa);
+    }
+    __syncthreads();  // every wave is done reading the ring before it is reused
+    return;
+  }
+
+  for (int it = 0; it < nk; ++it) {
+    resident(it);
     if (it + T::NS - 1 < nk) issue(it + T::NS - 1);
     compute(it);
   }
@@ -767,9 +842,12 @@ struct NoClaim {
 // release increment of the tile's ready counter.
 __device__ __forceinline__ void signal_ready(uint32_t* flag) { release_add(flag); }
 
-// Consumer side: before loading Z columns [k, k + kBK) of row block mb, the
-// GEMM1 tile (mb, k / bn1) must have signalled in this run (once per tile and
-// run), i.e. its counter must have reached epoch + 1 (compared wrap-safe).
+// Consumer side: before loading Z columns [k, k + span) of row block mb (one
+// stage), every GEMM1 tile (mb, kb) whose columns they overlap must have
+// signalled in this run (once per tile and run), i.e. its counter must have
+// reached epoch + 1 (compared wrap-safe).  A stage deeper than a GEMM1 tile
+// is wide (128-deep stages over 64-column tiles) can need two tiles; the
+// wait then repeats from the first tile still unknown.
 //
 // Wave 0 polls the first counter it needs; once that is ready it reads up to
 // 64 consecutive counters of the item's K range in one vector load and takes
@@ -803,10 +881,19 @@ struct ReadyWait {
   int* s_known;   // LDS broadcast slot
   int k_ready;    // K offsets below this are in column blocks this work-group has acquired (uniform)
   TraceAcc* tr;
+  int span;       // K depth of one stage
   __device__ __forceinline__ void operator()(int k) {
-    if (k < k_ready) return;  // one compare per stage; the division below only on a miss
-    const int kb = k / bn1;
+    const int k_hi = k + span - 1;  // the stage's last column
+    if (k_hi < k_ready) return;     // one compare per stage; the division below only on a miss
     const uint64_t t0 = trace_now();
+    // Each round acquires at least the first unknown column block, or gives up
+    // (k_ready then covers everything), so the loop ends.
+    do acquire((k > k_ready ? k : k_ready) / bn1);
+    while (k_hi >= k_ready);
+    if constexpr (kTrace) tr->flag += trace_now() - t0;
+  }
+  // One poll-and-gather round from column block kb; updates k_ready.
+  __device__ __forceinline__ void acquire(int kb) {
     if (uniform((int)(threadIdx.x >> 6)) == 0) {  // wave 0, as a scalar branch
       const int lane = threadIdx.x & 63;
       const int j = kb + lane;
@@ -845,7 +932,6 @@ struct ReadyWait {
     // Every wave has read *s_known before wave 0 may write it again: the
     // pipeline prologue calls this back to back, with no other barrier between.
     __syncthreads();
-    if constexpr (kTrace) tr->flag += trace_now() - t0;
   }
 };
 

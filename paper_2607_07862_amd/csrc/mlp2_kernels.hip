@@ -245,7 +245,7 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
   } else if constexpr (WAIT) {
     // ready counters advance once per run of every mode but the sentinel mode
     ReadyWait w{a.ready, a.ctrl + CTRL_ERROR, mb, a.Mb, a.bn1, (kend - 1) / a.bn1, ready_runs + 1u, a.spin_limit,
-                s_slot, 0, &tr};
+                s_slot, 0, &tr, T::BK};
     ClaimAtLastStage<ReadyWait, C> hook{w, &next, kend - T::BK};
     mainloop<T, HV>(a.Z, a.F, m0, zlast, Bp, a.H, n0, kbeg, kend, acc, lds, hook, tr);
   } else {
@@ -545,6 +545,9 @@ static const Entry kEntries[] = {
     // 32-deep stages: twice the ring depth in the same LDS (measured slower
     // than 64-deep stages on every workload: one barrier per half the work)
     MLP2_ENTRY_WK(256, 128, 256, 2, 4, 2, 8, 32), MLP2_ENTRY_WK(128, 64, 64, 1, 8, 1, 4, 32),
+    // 128-deep stages for the weight-streaming shapes of one wave per SIMD
+    MLP2_ENTRY_WK(128, 64, 64, 1, 3, 1, 4, 128), MLP2_ENTRY_WK(32, 64, 128, 1, 3, 1, 4, 128),
+    MLP2_ENTRY_WK(32, 64, 64, 1, 4, 1, 4, 128), MLP2_ENTRY_WK(64, 64, 64, 1, 4, 1, 4, 128),
 };
 
 static const Entry* find_entry(const KernelConfig& c) {
@@ -588,7 +591,7 @@ __device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int ti
   const uint16_t* Bp[1] = {L.W};
   if (c.wait && L.ready_in) {
     ReadyWait w{L.ready_in, a.ctrl + CTRL_ERROR, mb, a.Mb, T::BN, (K - 1) / T::BN, epoch + 1u, a.spin_limit, s_slot,
-                0, &tr};
+                0, &tr, T::BK};
     ClaimAtLastStage<ReadyWait> hook{w, &next, K - T::BK};
     mainloop<T, 1>(L.A, K, m0, L.alast, Bp, L.N, n0, 0, K, acc, lds, hook, tr);
   } else {

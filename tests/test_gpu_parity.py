@@ -59,6 +59,13 @@ SMALL = [
     (200, 512, 640, 2, {"waves": 8, "bm": 256, "bn1": 128, "bn2": 256, "stages": 4, "bk": 32, "splitk2": 3}),
     (77, 320, 448, 0, {"bm": 128, "bn1": 64, "bn2": 64, "stages": 8, "bk": 32, "splitk2": 2}),
     (300, 256, 512, 1, {"bm": 128, "bn1": 64, "bn2": 64, "stages": 8, "bk": 32, "splitk1": 2}),
+    # 128-deep stages: every GEMM2 stage reads the Z of two 64-column GEMM1
+    # tiles (the consumer waits for both); split-K parts in whole stages
+    (77, 256, 384, 1, {"bm": 128, "bn1": 64, "bn2": 64, "stages": 3, "bk": 128, "splitk2": 3}),
+    (130, 512, 1024, 0, {"bm": 128, "bn1": 64, "bn2": 64, "stages": 3, "bk": 128, "splitk1": 2}),
+    (20, 1024, 768, 1, {"bm": 32, "bn1": 64, "bn2": 128, "stages": 3, "bk": 128, "splitk1": 4, "splitk2": 2}),
+    (50, 640, 1280, 1, {"bm": 32, "bn1": 64, "bn2": 64, "stages": 4, "bk": 128, "splitk2": 4}),
+    (64, 384, 512, 0, {"bm": 64, "bn1": 64, "bn2": 64, "stages": 4, "bk": 128}),
 ]
 
 
@@ -87,6 +94,17 @@ def test_small_shapes_against_full_oracle(lib, M, H, F, act, tuning):
     assert_bit_equal(Zs, Zq, "Z sequential vs workqueue")
     zref = O.intermediate(I.bits(d["X"]), I.bits(d["W1"]), M, H, F, act)
     assert_matches_oracle(Zp[:M], zref, "Z")
+    plan.close()
+
+
+def test_deep_stages_need_whole_stages_of_k(lib):
+    """128-deep stages are refused where H or F is not a multiple of 128, and split-K parts round up to whole stages."""
+    for M, H, F in [(64, 320, 512), (64, 512, 320)]:
+        with pytest.raises(B.Mlp2Error):
+            B.Plan(M, H, F, 1, {"bm": 64, "bn1": 64, "bn2": 64, "stages": 4, "bk": 128})
+    plan = B.Plan(50, 640, 1280, 1, {"bm": 32, "bn1": 64, "bn2": 64, "stages": 4, "bk": 128, "splitk2": 4})
+    info = plan.info()
+    assert info["bk"] == 128 and info["splitk2"] == 4, info  # parts of 384, 384, 384 and 128 columns
     plan.close()
 
 
