@@ -59,6 +59,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 KERNEL_SOURCES = ["paper_2607_07862_amd/csrc/mlp2_device.hpp", "paper_2607_07862_amd/csrc/mlp2_kernels.hip"]
 FLUSH_BYTES = 1 << 30
+SETTLE_MS = 200
 
 
 def log(*a):
@@ -621,6 +622,17 @@ def main():
     g = {k: v.to("cuda") for k, v in d.items()}
     r = Runner(B, w, g, tuning, stream)
     log(f"plan {r.info}")
+    # Clock settling: the chip raises its clocks over the first tens of
+    # milliseconds of load, so the modes run untimed for SETTLE_MS first (a
+    # first timed block otherwise reads a few percent slow); then the
+    # warm-up steps.
+    t_settle = time.perf_counter()
+    while (time.perf_counter() - t_settle) * 1e3 < SETTLE_MS:
+        for _ in range(5):
+            r.run(B.MODE_TILE_PIPELINED)
+            if not args.only_pipelined:
+                r.run(B.MODE_SEQUENTIAL)
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         r.run(B.MODE_TILE_PIPELINED)
         if not args.only_pipelined:
@@ -771,6 +783,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "clock_settle_ms": SETTLE_MS,
         "ms_per_step": round(value / 1e3, 6),
         "higher_is_better": False,
         "scaling": "strong",

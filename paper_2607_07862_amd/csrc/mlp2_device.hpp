@@ -395,22 +395,42 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     b_off[j] = (uint32_t)(((long)row * ldb + n0 + 8 * lc) * 2);
   }
 
+  // A stage's loads: an item that waits for its activation rows (a GEMM2
+  // item behind ready counters) requests the weights first, so they stream
+  // during the wait; every other item requests the activation rows first
+  // (measured on the gated GEMM1 operand stream without math, 256 activation
+  // rows and two 128-column weight stripes per stage: 216 -> 202 us).  The
+  // choice is made per item kind at compile time: choosing per stage from
+  // the counters already seen complete made the one-launch kernels' code
+  // much slower (decode 74 -> 113 us).
   auto issue = [&](int st) {
     const int k = kbeg + st * T::BK;
     const uint32_t sbase = lds_base + (uint32_t)((st % T::NS) * SB);
+    auto weights = [&]() {
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
+      for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int j = 0; j < T::B_DMA; ++j)
-        dma16(Bp[b], b_off[j] + (uint32_t)((long)k * ldb * 2),
-              uniform(sbase + (uint32_t)(T::A_BYTES + b * T::B_BYTES + (wave + T::NWAVES * j) * 1024)));
-    wait(k);  // covers the stage's columns [k, k + BK)
+        for (int j = 0; j < T::B_DMA; ++j)
+          dma16(Bp[b], b_off[j] + (uint32_t)((long)k * ldb * 2),
+                uniform(sbase + (uint32_t)(T::A_BYTES + b * T::B_BYTES + (wave + T::NWAVES * j) * 1024)));
+    };
+    auto activations = [&]() {
 #pragma unroll
-    for (int j = 0; j < T::A_DMA; ++j) {
-      if constexpr (Check::kCoherentA)
-        dma16_coherent(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + T::NWAVES * j) * 1024)));
-      else
-        dma16(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + T::NWAVES * j) * 1024)));
+      for (int j = 0; j < T::A_DMA; ++j) {
+        if constexpr (Check::kCoherentA)
+          dma16_coherent(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + T::NWAVES * j) * 1024)));
+        else
+          dma16(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + T::NWAVES * j) * 1024)));
+      }
+    };
+    if constexpr (Wait::kBlocks) {
+      weights();
+      wait(k);  // covers the stage's columns [k, k + BK)
+      activations();
+    } else {
+      activations();
+      wait(k);  // takes the next ticket at the last stage
+      weights();
     }
   };
 
@@ -814,11 +834,13 @@ struct Claim {
 // committed to its next item a whole item ahead would keep it from a
 // work-group that frees up sooner, and lengthen the launch's tail.
 struct NoWait {
+  static constexpr bool kBlocks = false;  // never waits
   __device__ __forceinline__ void operator()(int) {}
 };
 
 template <class Wait, class C = Claim>
 struct ClaimAtLastStage {
+  static constexpr bool kBlocks = Wait::kBlocks;
   Wait& wait;
   C* next;
   int k_last;  // K offset of the item's last stage
@@ -872,6 +894,7 @@ __device__ __forceinline__ void signal_ready(uint32_t* flag) { release_add(flag)
 // point of coherence; the Z loads are issued after it, in program order,
 // and a work-group-scope acquire orders them for the compiler.
 struct ReadyWait {
+  static constexpr bool kBlocks = true;  // waits on ready counters before the activation loads
   const uint32_t* ready;
   uint32_t* err;  // CTRL_ERROR word
   int mb, Mb, bn1;
