@@ -24,6 +24,10 @@ template <class A>
 struct is_same_type<A, A> {
   static constexpr bool value = true;
 };
+template <bool V>
+struct bool_constant {
+  static constexpr bool value = V;
+};
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
@@ -395,15 +399,18 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     b_off[j] = (uint32_t)(((long)row * ldb + n0 + 8 * lc) * 2);
   }
 
-  // A stage's loads: an item that waits for its activation rows (a GEMM2
-  // item behind ready counters) requests the weights first, so they stream
-  // during the wait; every other item requests the activation rows first
-  // (measured on the gated GEMM1 operand stream without math, 256 activation
-  // rows and two 128-column weight stripes per stage: 216 -> 202 us).  The
-  // choice is made per item kind at compile time: choosing per stage from
-  // the counters already seen complete made the one-launch kernels' code
-  // much slower (decode 74 -> 113 us).
-  auto issue = [&](int st) {
+  // A stage's loads: the activation rows first (measured on the gated GEMM1
+  // operand stream without math, 256 activation rows and two 128-column
+  // weight stripes per stage: 216 -> 202 us), except while a GEMM2 item may
+  // still have to wait for its activation rows: then the weights first, so
+  // they stream during the wait.  The order is fixed per loop, not chosen
+  // per stage: in the plain stage loop (every tile but the four-wave tiles
+  // with three or more stages, below) an item that waits runs its stages
+  // in the weights-first loop until its wait has seen every producer of its K
+  // range complete, then in the activation-first loop (gated 396 -> 388 us,
+  // prefill 440 -> 421 us pipelined; a choice per stage inside one loop made
+  // the one-launch kernels much slower: decode 74 -> 113 us).
+  auto issue = [&](int st, auto weights_first) {
     const int k = kbeg + st * T::BK;
     const uint32_t sbase = lds_base + (uint32_t)((st % T::NS) * SB);
     auto weights = [&]() {
@@ -423,16 +430,18 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
           dma16(A, a_off[j] + (uint32_t)(k * 2), uniform(sbase + (uint32_t)((wave + T::NWAVES * j) * 1024)));
       }
     };
-    if constexpr (Wait::kBlocks) {
+    if constexpr (decltype(weights_first)::value) {
       weights();
       wait(k);  // covers the stage's columns [k, k + BK)
       activations();
     } else {
       activations();
-      wait(k);  // takes the next ticket at the last stage
+      wait(k);  // returns at once (takes the next ticket at the last stage)
       weights();
     }
   };
+  using WaitFirst = bool_constant<Wait::kBlocks>;  // weights first where the item may wait
+  using ActFirst = bool_constant<false>;
 
   // Fragment addressing (bytes inside a stage).
   //   activation (MFMA B operand): lane holds A[row = l%16][k = 8(l/16) .. +7]  -> ds_read_b128
@@ -532,7 +541,7 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
   // Prologue: NS - 1 stages in flight.
 #pragma unroll
   for (int st = 0; st < T::NS - 1; ++st)
-    if (st < nk) issue(st);
+    if (st < nk) issue(st, WaitFirst());
 
   if constexpr (T::NWAVES == 4 && T::NS >= 3) {
     // One wave per SIMD: nothing else on the SIMD hides a stage's LDS read
@@ -568,26 +577,29 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
               acc[b][i][tm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.w[ks][b][i], f.x[ks][tm], acc[b][i][tm], 0, 0, 0);
     };
     // Stage it is multiplied while stage it + 1 (< nk) is read.
-    auto advance = [&](int it, Frags& cur, Frags& nxt) {
+    auto advance = [&](int it, Frags& cur, Frags& nxt, auto order) {
       resident(it + 1);
-      if (it + T::NS < nk) issue(it + T::NS);
+      if (it + T::NS < nk) issue(it + T::NS, order);
       read(nxt, it + 1);
       mma(cur);
     };
     resident(0);
-    if (T::NS - 1 < nk) issue(T::NS - 1);
+    if (T::NS - 1 < nk) issue(T::NS - 1, WaitFirst());
     Frags fa, fb;
     read(fa, 0);
     // Two stages per trip, the fragment sets swapping roles; every trip reads
     // a next stage, so both sets keep their registers (no conditional read
     // merges into the products' control flow).
+    // (One loop: a waiting item keeps the weights-first order throughout; a
+    // second, activation-first loop after the item's producers were all seen
+    // complete made these kernels slower: decode 76 -> 88 us.)
     int it = 0;
     for (; it + 2 < nk; it += 2) {
-      advance(it, fa, fb);
-      advance(it + 1, fb, fa);
+      advance(it, fa, fb, WaitFirst());
+      advance(it + 1, fb, fa, WaitFirst());
     }
     if (it + 1 < nk) {  // two stages left
-      advance(it, fa, fb);
+      advance(it, fa, fb, WaitFirst());
       mma(fb);
     } else {            // one stage left
       mma(fa);
@@ -596,9 +608,17 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
     return;
   }
 
-  for (int it = 0; it < nk; ++it) {
+  int it = 0;
+  if constexpr (Wait::kBlocks) {
+    for (; it < nk && !wait.all_known(); ++it) {
+      resident(it);
+      if (it + T::NS - 1 < nk) issue(it + T::NS - 1, WaitFirst());
+      compute(it);
+    }
+  }
+  for (; it < nk; ++it) {
     resident(it);
-    if (it + T::NS - 1 < nk) issue(it + T::NS - 1);
+    if (it + T::NS - 1 < nk) issue(it + T::NS - 1, ActFirst());
     compute(it);
   }
   __syncthreads();  // every wave is done reading the ring before it is reused
@@ -835,6 +855,7 @@ struct Claim {
 // work-group that frees up sooner, and lengthen the launch's tail.
 struct NoWait {
   static constexpr bool kBlocks = false;  // never waits
+  __device__ __forceinline__ bool all_known() const { return true; }
   __device__ __forceinline__ void operator()(int) {}
 };
 
@@ -844,6 +865,7 @@ struct ClaimAtLastStage {
   Wait& wait;
   C* next;
   int k_last;  // K offset of the item's last stage
+  __device__ __forceinline__ bool all_known() const { return wait.all_known(); }
   __device__ __forceinline__ void operator()(int k) {
     wait(k);
     if (k == k_last) next->issue();
@@ -905,6 +927,8 @@ struct ReadyWait {
   int k_ready;    // K offsets below this are in column blocks this work-group has acquired (uniform)
   TraceAcc* tr;
   int span;       // K depth of one stage
+  // Every producer of the item's K range was seen complete (uniform).
+  __device__ __forceinline__ bool all_known() const { return k_ready == 0x7fffffff; }
   __device__ __forceinline__ void operator()(int k) {
     const int k_hi = k + span - 1;  // the stage's last column
     if (k_hi < k_ready) return;     // one compare per stage; the division below only on a miss
