@@ -76,14 +76,16 @@ def summarise(B, I, bench, key):
     info = r.info
     G = max(info["grid_pipelined"], info["grid_gemm1"], info["grid_gemm2"])
     buf = torch.zeros(2 * G * (1 + 8 * CAP), dtype=torch.int64, device="cuda")
+    # (the sentinel mode runs without row groups: a grouped plan skips it)
+    modes = [(B.MODE_SEQUENTIAL, "sequential"), (B.MODE_TILE_PIPELINED, "pipelined"), (B.MODE_WORKQUEUE, "workqueue")]
+    if not info["row_group"]:
+        modes.append((B.MODE_SENTINEL, "sentinel"))
     for _ in range(5):
-        r.run(B.MODE_TILE_PIPELINED)
-        r.run(B.MODE_SEQUENTIAL)
-        r.run(B.MODE_SENTINEL)
+        for mode, _name in modes:
+            r.run(mode)
     torch.cuda.synchronize()
     rows, clocks = [], []
-    for mode, name in ((B.MODE_SEQUENTIAL, "sequential"), (B.MODE_TILE_PIPELINED, "pipelined"),
-                       (B.MODE_WORKQUEUE, "workqueue"), (B.MODE_SENTINEL, "sentinel")):
+    for mode, name in modes:
         buf.zero_()
         r.plan.attach_trace(buf, CAP)
         r.run(mode)
