@@ -159,7 +159,9 @@ typedef struct mlp2_tuning {
                     producer / consumer split of the grid, p1 in 1..63 of every 64)       */
   int bk;        /* K depth of one LDS stage: 64, 32 or 128 (as built for the shape; 128   */
                  /* only where H and F are multiples of 128)                               */
-  int reserved[1];
+  int weights_nt; /* weight loads with the non-temporal hint: 0 = automatic (on when W1 and
+                     W2 together exceed the 256 MiB last-level cache and the tile is built
+                     with it), 1 = on (refused where not built), -1 = off                 */
 } mlp2_tuning_t;
 
 /* What a plan chose, for reports and tests. */
@@ -185,7 +187,7 @@ typedef struct mlp2_info {
   int waves;             /* 64-wide waves per work-group                    */
   int lag;               /* pipelined rank-table lag in ranks (shared roles) */
   int p1;                /* static GEMM1 share of every 64 work-groups (0: shared roles) */
-  int reserved[1];
+  int weights_nt;        /* 1: the weight loads carry the non-temporal hint  */
 } mlp2_info_t;
 
 /* Create a plan for Y[M,H] = act(X[M,H] . W1) . W2 on the current HIP device.

@@ -63,7 +63,7 @@ class Tuning(ctypes.Structure):
         ("lag", ctypes.c_int),
         ("p1", ctypes.c_int),
         ("bk", ctypes.c_int),
-        ("reserved", ctypes.c_int * 1),
+        ("weights_nt", ctypes.c_int),
     ]
 
 
@@ -97,7 +97,7 @@ class Info(ctypes.Structure):
         ("waves", ctypes.c_int),
         ("lag", ctypes.c_int),
         ("p1", ctypes.c_int),
-        ("reserved", ctypes.c_int * 1),
+        ("weights_nt", ctypes.c_int),
     ]
 
 
@@ -258,7 +258,7 @@ class Plan:
         rc = self.lib.mlp2_plan_info(self.handle, ctypes.byref(i))
         if rc != OK:
             raise Mlp2Error(rc, "mlp2_plan_info")
-        return {f: getattr(i, f) for f, _ in Info._fields_ if f != "reserved"}
+        return {f: getattr(i, f) for f, _ in Info._fields_}
 
     def set_option(self, key: int, value: int) -> None:
         rc = self.lib.mlp2_set_option(self.handle, int(key), int(value))

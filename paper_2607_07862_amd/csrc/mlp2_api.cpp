@@ -380,7 +380,7 @@ mlp2_plan_t mlp2_plan_ex(int64_t M, int64_t H, int64_t F, int act, int dtype, co
   if (tz.bm < 0 || tz.bn1 < 0 || tz.bn2 < 0 || tz.splitk1 < 0 || tz.splitk2 < 0 || tz.grid < 0 || tz.order < 0 || tz.stages < 0 ||
       tz.order > MLP2_ORDER_BANDED || tz.row_group < -1 || (tz.row_group > 0 && tz.row_group % 256) ||
       (tz.waves != 0 && tz.waves != 4 && tz.waves != 8) || tz.lag < -1 || tz.p1 < 0 || tz.p1 > 63 || tz.p1 % 8 ||
-      (tz.bk != 0 && tz.bk != 32 && tz.bk != 64 && tz.bk != 128)) {
+      (tz.bk != 0 && tz.bk != 32 && tz.bk != 64 && tz.bk != 128) || tz.weights_nt < -1 || tz.weights_nt > 1) {
     fail(MLP2_ERR_UNSUPPORTED);
     return nullptr;
   }
@@ -513,19 +513,33 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
       {pref[0], pref[1], pref[2], 4, 4},       {pref[0], pref[1], 64, 4, 4},       {pref[0], 64, 64, 4, 4},
       {128, 64, 64, 4, 4},                     {64, 64, 64, 4, 4},                 {32, 64, 64, 4, 4},
   };
+  // Weight loads with the non-temporal hint once the two weight matrices
+  // together exceed the 256 MiB last-level cache: streamed weights then stop
+  // displacing the lines the activation and Z loads reuse (70B gated MLP,
+  // 1.4 GB of weights, back-to-back runs: 390 -> 378 us pipelined,
+  // 405 -> 390 us sequential; after a 1 GiB flush: 389 -> 393 us pipelined,
+  // 405 -> 398 us sequential).  Where the weights fit, a warm run reads part
+  // of them from that cache, and the hint loses it (decode 80 -> 101 us,
+  // prefill 430 -> 452 us): off.
+  const bool big_weights = (uint64_t)(nb + 1) * (uint64_t)H * (uint64_t)F * 2 > ((uint64_t)256 << 20);
+  const int nt_first = tz.weights_nt == 1 || (tz.weights_nt == 0 && big_weights) ? 1 : 0;
+  const int nt_last = tz.weights_nt == 1 ? 1 : 0;  // forced on: no fallback without it
   bool found = false;
-  // The preferred stage depth first; the fallbacks with 64-deep stages.
+  // The preferred stage depth first; the fallbacks with 64-deep stages; with
+  // the hint where wanted and built, else without.
   for (int pass = 0; pass < 2 && !found; ++pass) {
     for (const auto& c : cand) {
-      KernelConfig k{tz.bm ? tz.bm : c[0], tz.bn1 ? tz.bn1 : c[1], tz.bn2 ? tz.bn2 : c[2], nb,
-                     tz.stages ? tz.stages : c[3], tz.waves ? tz.waves : c[4], tz.bk ? tz.bk : pass ? 64 : bk};
-      // 128-deep stages need every K range (H; F; the split-K parts) in whole stages
-      if (F % k.bn1 == 0 && H % k.bn2 == 0 && (k.bk < 128 || (H % k.bk == 0 && F % k.bk == 0)) &&
-          mlp2::config_supported(k)) {
-        p->kc = k;
-        found = true;
-        break;
+      for (int nt = nt_first; nt >= nt_last && !found; --nt) {
+        KernelConfig k{tz.bm ? tz.bm : c[0], tz.bn1 ? tz.bn1 : c[1], tz.bn2 ? tz.bn2 : c[2], nb,
+                       tz.stages ? tz.stages : c[3], tz.waves ? tz.waves : c[4], tz.bk ? tz.bk : pass ? 64 : bk, nt};
+        // 128-deep stages need every K range (H; F; the split-K parts) in whole stages
+        if (F % k.bn1 == 0 && H % k.bn2 == 0 && (k.bk < 128 || (H % k.bk == 0 && F % k.bk == 0)) &&
+            mlp2::config_supported(k)) {
+          p->kc = k;
+          found = true;
+        }
       }
+      if (found) break;
     }
   }
   if (!found) return MLP2_ERR_UNSUPPORTED;
@@ -886,6 +900,7 @@ int mlp2_plan_info(mlp2_plan_t p, mlp2_info_t* out) {
   out->waves = p->kc.waves;
   out->lag = merged_lag(p);
   out->p1 = p->p1;
+  out->weights_nt = p->kc.wnt;
   return MLP2_OK;
 }
 

@@ -202,9 +202,13 @@ __device__ __forceinline__ u32x4 pack_bf16x8(const float (&v)[8]) {
 //   weight tile [BK][BN] bf16 per operand: chunk c of row k at c ^ swzB(k),
 //     which puts the 4 rows read by one ds_read_b64_tr_b16 group in
 //     different banks.
-template <int BM_, int BN_, int WM_, int WN_, int NS_, int BK_ = kBK>
+template <int BM_, int BN_, int WM_, int WN_, int NS_, int BK_ = kBK, bool WNT_ = false>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NS = NS_;
+  // Weight loads with the non-temporal hint (plans whose weights exceed the
+  // last-level cache): the streamed weights then stop displacing the lines
+  // that the activation loads reuse.
+  static constexpr bool WNT = WNT_;
   // K depth of one stage: 64; 32 (half the bytes per stage, so a ring of the
   // same LDS holds twice the stages); or 128 (twice the products per stage
   // for the same per-stage costs: the wait, the barrier, the DMA issue and
@@ -267,6 +271,11 @@ __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t 
 // agent-scope atomic loads): it reads the device's point of coherence rather
 // than a line the consumer's XCD L2 may hold.  The sentinel mode's consumers
 // read the intermediate this way, since no release and acquire order it.
+// The same load with the non-temporal hint (a streamed operand read once).
+__device__ __forceinline__ void dma16_nt(const void* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("global_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(base), "{m0}"(lds_addr) : "memory");
+}
+
 __device__ __forceinline__ void dma16_coherent(const void* base, uint32_t voff, uint32_t lds_addr) {
   asm volatile("global_load_lds_dwordx4 %0, %1 sc1" ::"v"(voff), "s"(base), "{m0}"(lds_addr) : "memory");
 }
@@ -417,9 +426,13 @@ __device__ __forceinline__ void mainloop(const uint16_t* __restrict__ A, long ld
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int j = 0; j < T::B_DMA; ++j)
-          dma16(Bp[b], b_off[j] + (uint32_t)((long)k * ldb * 2),
-                uniform(sbase + (uint32_t)(T::A_BYTES + b * T::B_BYTES + (wave + T::NWAVES * j) * 1024)));
+        for (int j = 0; j < T::B_DMA; ++j) {
+          const uint32_t dst = uniform(sbase + (uint32_t)(T::A_BYTES + b * T::B_BYTES + (wave + T::NWAVES * j) * 1024));
+          if constexpr (T::WNT)
+            dma16_nt(Bp[b], b_off[j] + (uint32_t)((long)k * ldb * 2), dst);
+          else
+            dma16(Bp[b], b_off[j] + (uint32_t)((long)k * ldb * 2), dst);
+        }
     };
     auto activations = [&]() {
 #pragma unroll

@@ -488,14 +488,14 @@ template <int NS> struct TileFor<128, 128, NS, 8> { using type = Tile<128, 128, 
 template <int NS> struct TileFor<128, 64, NS, 8> { using type = Tile<128, 64, 4, 2, NS>; };
 template <int NS> struct TileFor<64, 256, NS, 8> { using type = Tile<64, 256, 2, 4, NS>; };
 template <int NS> struct TileFor<32, 256, NS, 8> { using type = Tile<32, 256, 1, 8, NS>; };
-template <int BM, int BN, int NS, int W, int BK>
+template <int BM, int BN, int NS, int W, int BK, bool WNT = false>
 struct TileForK {
   using base = typename TileFor<BM, BN, NS, W>::type;
-  using type = Tile<BM, BN, base::WM, base::WN, NS, BK>;
+  using type = Tile<BM, BN, base::WM, base::WN, NS, BK, WNT>;
 };
 
 struct Entry {
-  int bm, bn1, bn2, nb, ns, waves, bk;
+  int bm, bn1, bn2, nb, ns, waves, bk, wnt;
   const void* seq1;
   const void* seq2;
   const void* pipe;
@@ -505,17 +505,18 @@ struct Entry {
 
 // GEMM2 of BN2 columns as one tile (HV = 1), or as two halves of BN2 / 2 that
 // share the GEMM1 tile shape (HV = 2).
-#define MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PH)                                          \
-  (const void*)&k_mlp2<typename TileForK<BM, BN1, NS, W, BK>::type, NB,                       \
-                       typename TileForK<BM, (BN2) / (HV), NS, W, BK>::type, HV, PH>
-#define MLP2_ENTRY_WK(BM, BN1, BN2, NB, NS, HV, W, BK)                                        \
+#define MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, NT, PH)                                      \
+  (const void*)&k_mlp2<typename TileForK<BM, BN1, NS, W, BK, NT>::type, NB,                   \
+                       typename TileForK<BM, (BN2) / (HV), NS, W, BK, NT>::type, HV, PH>
+#define MLP2_ENTRY_WKN(BM, BN1, BN2, NB, NS, HV, W, BK, NT)                                   \
   Entry {                                                                                     \
-    BM, BN1, BN2, NB, NS, W, BK, MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_GEMM1),       \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_GEMM2),                                 \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_PIPELINED),                             \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_WORKQUEUE),                             \
-        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, PHASE_SENTINEL)                               \
+    BM, BN1, BN2, NB, NS, W, BK, NT, MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, NT, PHASE_GEMM1), \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, NT, PHASE_GEMM2),                             \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, NT, PHASE_PIPELINED),                         \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, NT, PHASE_WORKQUEUE),                         \
+        MLP2_K(BM, BN1, BN2, NB, NS, HV, W, BK, NT, PHASE_SENTINEL)                           \
   }
+#define MLP2_ENTRY_WK(BM, BN1, BN2, NB, NS, HV, W, BK) MLP2_ENTRY_WKN(BM, BN1, BN2, NB, NS, HV, W, BK, false)
 #define MLP2_ENTRY_W(BM, BN1, BN2, NB, NS, HV, W) MLP2_ENTRY_WK(BM, BN1, BN2, NB, NS, HV, W, 64)
 #define MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, HV) MLP2_ENTRY_W(BM, BN1, BN2, NB, NS, HV, 4)
 #define MLP2_ENTRY(BM, BN1, BN2, NB, NS) MLP2_ENTRY_HV(BM, BN1, BN2, NB, NS, 1)
@@ -540,6 +541,8 @@ static const Entry kEntries[] = {
     MLP2_ENTRY_W(256, 256, 256, 1, 2, 1, 8), MLP2_ENTRY_W(256, 128, 128, 1, 3, 1, 8),
     MLP2_ENTRY_W(256, 256, 128, 1, 2, 1, 8), MLP2_ENTRY_W(256, 128, 256, 1, 2, 2, 8),
     MLP2_ENTRY_W(256, 128, 256, 2, 2, 2, 8), MLP2_ENTRY_W(256, 64, 128, 2, 3, 2, 8),
+    // the gated tile with non-temporal weight loads (weights beyond the last-level cache)
+    MLP2_ENTRY_WKN(256, 128, 256, 2, 2, 2, 8, 64, true),
     MLP2_ENTRY_W(128, 128, 128, 1, 4, 1, 8), MLP2_ENTRY_W(128, 256, 256, 1, 3, 1, 8),
     MLP2_ENTRY_W(128, 64, 64, 1, 4, 1, 8),
     // 32-deep stages: twice the ring depth in the same LDS (measured slower
@@ -553,7 +556,7 @@ static const Entry kEntries[] = {
 static const Entry* find_entry(const KernelConfig& c) {
   for (const Entry& e : kEntries)
     if (e.bm == c.bm && e.bn1 == c.bn1 && e.bn2 == c.bn2 && e.nb == c.nb && e.ns == c.ns && e.waves == c.waves &&
-        e.bk == c.bk)
+        e.bk == c.bk && e.wnt == c.wnt)
       return &e;
   return nullptr;
 }

@@ -12,6 +12,7 @@ namespace mlp2 {
 // waves per work-group (4 or 8) and the K depth of a stage (64 or 32).
 struct KernelConfig {
   int bm, bn1, bn2, nb, ns, waves, bk;
+  int wnt;  // weight loads with the non-temporal hint
 };
 
 bool config_supported(const KernelConfig& c);

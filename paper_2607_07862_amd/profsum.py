@@ -33,15 +33,21 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def short_name(n: str) -> str:
-    m = re.search(r"k_mlp2<mlp2::Tile<(\d+), (\d+), (\d+), (\d+), (\d+)(?:, (\d+))?>, (\d), "
-                  r"mlp2::Tile<(\d+), (\d+), \d+, \d+, \d+(?:, \d+)?>, (\d), (\d)>", n)
+    """k_mlp2<Tile<BM, BN, WM, WN, NS[, BK[, NT]]>, NB, Tile<...>, HV, PHASE> -> phase and tile shape."""
+    m = re.search(r"k_mlp2<mlp2::Tile<([^>]*)>, (\d), mlp2::Tile<([^>]*)>, (\d), (\d)>", n)
     if m:
-        phase = ["gemm1", "gemm2", "pipelined", "workqueue", "sentinel"][int(m.group(11))]
-        bn2 = int(m.group(9)) * int(m.group(10))
-        waves = int(m.group(3)) * int(m.group(4))
-        bk = f", bk {m.group(6)}" if m.group(6) and m.group(6) != "64" else ""
-        return (f"k_mlp2 {phase} (bm {m.group(1)}, bn1 {m.group(2)}, bn2 {bn2}, nb {m.group(7)}, stages {m.group(5)}, "
-                f"waves {waves}{bk})")
+        t1 = [x.strip() for x in m.group(1).split(",")]
+        t2 = [x.strip() for x in m.group(3).split(",")]
+        phase = ["gemm1", "gemm2", "pipelined", "workqueue", "sentinel"][int(m.group(5))]
+        bm, bn1, wm, wn, ns = (int(x) for x in t1[:5])
+        bn2 = int(t2[1]) * int(m.group(4))
+        extra = ""
+        if len(t1) > 5 and t1[5] != "64":
+            extra += f", bk {t1[5]}"
+        if len(t1) > 6 and t1[6] in ("true", "1"):
+            extra += ", weights nt"
+        return (f"k_mlp2 {phase} (bm {bm}, bn1 {bn1}, bn2 {bn2}, nb {m.group(2)}, stages {ns}, "
+                f"waves {wm * wn}{extra})")
     return n if len(n) < 90 else n[:87] + "..."
 
 

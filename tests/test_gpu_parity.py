@@ -66,6 +66,8 @@ SMALL = [
     (20, 1024, 768, 1, {"bm": 32, "bn1": 64, "bn2": 128, "stages": 3, "bk": 128, "splitk1": 4, "splitk2": 2}),
     (50, 640, 1280, 1, {"bm": 32, "bn1": 64, "bn2": 64, "stages": 4, "bk": 128, "splitk2": 4}),
     (64, 384, 512, 0, {"bm": 64, "bn1": 64, "bn2": 64, "stages": 4, "bk": 128}),
+    # the gated tile with non-temporal weight loads (a cache policy: same bits)
+    (200, 512, 640, 2, {"waves": 8, "bm": 256, "bn1": 128, "bn2": 256, "stages": 2, "weights_nt": 1}),
 ]
 
 
@@ -106,6 +108,26 @@ def test_deep_stages_need_whole_stages_of_k(lib):
     info = plan.info()
     assert info["bk"] == 128 and info["splitk2"] == 4, info  # parts of 384, 384, 384 and 128 columns
     plan.close()
+
+
+def test_weights_nt_choice(lib):
+    """The non-temporal weight hint: on by itself where W1 and W2 exceed 256 MiB, off
+    where they fit; forced off on request; refused where no tile is built with it."""
+    w = I.WORKLOADS["l70b_gated"]
+    plan = B.Plan(w.M, w.H, w.F, w.act)
+    assert plan.info()["weights_nt"] == 1, plan.info()
+    plan.close()
+    plan = B.Plan(w.M, w.H, w.F, w.act, {"weights_nt": -1})
+    assert plan.info()["weights_nt"] == 0, plan.info()
+    plan.close()
+    w = I.WORKLOADS["l8b_decode"]
+    plan = B.Plan(w.M, w.H, w.F, w.act)
+    assert plan.info()["weights_nt"] == 0, plan.info()
+    plan.close()
+    with pytest.raises(B.Mlp2Error):
+        B.Plan(64, 256, 512, 1, {"weights_nt": 1})
+    with pytest.raises(B.Mlp2Error):
+        B.Plan(64, 256, 512, 1, {"weights_nt": 2})
 
 
 def _workload_params():

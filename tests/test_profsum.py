@@ -33,6 +33,11 @@ def test_short_names():
     assert P.short_name(deep) == "k_mlp2 sentinel (bm 256, bn1 128, bn2 256, nb 2, stages 2, waves 8)"
     bk32 = "void mlp2::k_mlp2<mlp2::Tile<128, 64, 2, 2, 8, 32>, 1, mlp2::Tile<128, 64, 2, 2, 8, 32>, 1, 3>(mlp2::Args)"
     assert P.short_name(bk32) == "k_mlp2 workqueue (bm 128, bn1 64, bn2 64, nb 1, stages 8, waves 4, bk 32)"
+    # the non-temporal weight hint as a seventh tile parameter
+    nt = "void mlp2::k_mlp2<mlp2::Tile<256, 128, 4, 2, 2, 64, true>, 2, mlp2::Tile<256, 128, 4, 2, 2, 64, true>, 2, 2>(mlp2::Args)"
+    assert P.short_name(nt) == "k_mlp2 pipelined (bm 256, bn1 128, bn2 256, nb 2, stages 2, waves 8, weights nt)"
+    off = "void mlp2::k_mlp2<mlp2::Tile<128, 64, 2, 2, 4, 64, false>, 1, mlp2::Tile<128, 64, 2, 2, 4, 64, false>, 1, 0>(mlp2::Args)"
+    assert P.short_name(off) == "k_mlp2 gemm1 (bm 128, bn1 64, bn2 64, nb 1, stages 4, waves 4)"
     assert P.short_name("x" * 200).endswith("...")
 
 
