@@ -325,6 +325,23 @@ int upload_order(mlp2_plan_s* p) {
   build_merged(p, ord, ord2, lag, merged);
   p->lead1 = 0;
   while (p->lead1 < (int64_t)merged.size() && !(merged[p->lead1] & 0x80000000u)) ++p->lead1;
+  // Reduction items after everything else, tile by tile in the order in which
+  // the tiles' first parts are ranked (so the first tiles to finish come first).
+  if (p->items_red) {
+    std::vector<char> seen((size_t)p->Mb * p->Nb2, 0);
+    std::vector<uint32_t> red;
+    red.reserve((size_t)p->items_red);
+    for (const uint32_t q : ord2) {
+      const int tile = (int)q / p->S2;
+      if (seen[(size_t)tile]) continue;
+      seen[(size_t)tile] = 1;
+      for (int j = 0; j < p->red2; ++j) red.push_back((uint32_t)(tile * p->red2 + j));
+    }
+    for (const uint32_t r : red) {
+      ord2.push_back(0x40000000u | r);
+      merged.push_back(0xc0000000u | r);
+    }
+  }
   if (hipMemcpy(p->order1, ord.data(), ord.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(p->order2, ord2.data(), ord2.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess ||
       hipMemcpy(p->orderp, merged.data(), merged.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess)
@@ -576,6 +593,23 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
   p->p1 = tz.p1;
   p->items1 = tiles1 * p->S1;
   p->items2 = tiles2 * p->S2;
+  // A GEMM2 tile with split-K is summed by reduction items, one slice of its
+  // units each, ranked after every GEMM2 item: the sums of the launch's last
+  // round then run on as many work-groups as the tile has parts (up to a
+  // power of two that divides the tile's bm * bn2 / 1024 unit groups)
+  // instead of on the part that arrives last (70B gated MLP: the last
+  // round's 32 tiles of 8 parts took 42 us each on one work-group: 383 ->
+  // 364 us pipelined, 399 -> 378 us sequential).  Not where a tile's partials
+  // are small (under 64 KiB: the extra items then cost more than the sums;
+  // 64 x 512 x 2048, 32 KiB per tile: 16.2 -> 16.9 us).
+  p->red2 = 0;
+  if (p->S2 > 1 && (int64_t)p->S2 * p->kc.bm * p->kc.bn2 * 4 >= (64 << 10)) {
+    const int groups = p->kc.bm * p->kc.bn2 / 1024;
+    int r = 1;
+    while (2 * r <= p->S2 && 2 * r <= groups) r *= 2;
+    p->red2 = r > 1 ? r : 0;
+  }
+  p->items_red = p->red2 ? tiles2 * p->red2 : 0;
 
   p->occupancy = occ[2];
   p->max_grid = std::min(std::min(std::min(occ[0], occ[1]), std::min(occ[2], occ[3])), occ[4]) * p->num_cus;
@@ -585,7 +619,8 @@ int configure_plan(mlp2_plan_s* p, int64_t M, int64_t H, int64_t F, int act, con
   p->grid2 = std::min(occ[1] * p->num_cus, p->items2);
   p->grid = std::min(std::min(std::min(occ[2], occ[3]), occ[4]) * p->num_cus, p->items1 + p->items2);
   if (!roles_ok(p->p1, tz.grid ? tz.grid : p->grid)) return MLP2_ERR_UNSUPPORTED;  // both roles need work-groups
-  if (p->items2 >= (1 << 24)) return MLP2_ERR_UNSUPPORTED;  // workqueue entries hold a unit id in 24 bits
+  if (p->items2 >= (1 << 24) || p->items_red >= (1 << 24))
+    return MLP2_ERR_UNSUPPORTED;  // workqueue entries hold a unit id in 24 bits; rank entries flag kinds in bits 30, 31
   return MLP2_OK;
 }
 
@@ -623,9 +658,9 @@ size_t plan_layout(const mlp2_plan_s* p, bool own_z, PlanLayout* L, bool with_zs
   const size_t ord_off = off;
   off = align_up(off + (size_t)p->items1 * 4, 256);
   const size_t ord2_off = off;
-  off = align_up(off + (size_t)p->items2 * 4, 256);
+  off = align_up(off + ((size_t)p->items2 + p->items_red) * 4, 256);
   const size_t ordp_off = off;
-  off = align_up(off + ((size_t)p->items1 + p->items2) * 4, 256);
+  off = align_up(off + ((size_t)p->items1 + p->items2 + p->items_red) * 4, 256);
   const size_t zs_off = off;
   const size_t zs_bytes = with_zs ? align_up((size_t)2 * Mpad * F * 2, 256) : 0;
   off += zs_bytes;
@@ -743,6 +778,8 @@ int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void*
   a.trace_cap = p->trace_cap;
   a.p1 = 0;
   a.lists2 = 0;
+  a.red2 = p->red2;  // the sequential GEMM2 kernel and the pipelined launch use reduction items
+  a.items_red = p->items_red;
   a.Zs = p->Zs;
   a.zs_elems = (long)p->Mb * p->kc.bm * p->F;
   a.Zr = nullptr;
@@ -782,10 +819,14 @@ int launch_plan(const mlp2_plan_s* p, const void* X, const void* W1, const void*
     err = mlp2::launch_pipelined(p->kc, a, gridp, s);
   } else if (mode == MLP2_MODE_SENTINEL) {
     if (!p->Zs) return fail(MLP2_ERR_UNSUPPORTED);
+    a.red2 = 0;  // its last parts sum the tiles (same order, same bits)
+    a.items_red = 0;
     a.lists = claim_lists(gridp);
     a.first_static = statics(p->lead1, gridp);
     err = mlp2::launch_sentinel(p->kc, a, gridp, s);
   } else {
+    a.red2 = 0;  // workqueue units: the last part sums the tile (same order, same bits)
+    a.items_red = 0;
     a.lists = claim_lists(gridp);
     a.first_static = statics(p->items1, gridp);  // every ranked item is a GEMM1 item
     err = mlp2::launch_workqueue(p->kc, a, gridp, s);

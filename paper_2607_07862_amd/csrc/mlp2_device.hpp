@@ -84,9 +84,10 @@ struct Args {
                        // run, and a spare)
   uint32_t* ctrl;      // CTRL_* words
   const uint32_t* order1;  // GEMM1 item per rank of the GEMM1 kernel, length items1
-  const uint32_t* order2;  // GEMM2 item per rank of the GEMM2 kernel, length items2
-  const uint32_t* orderp;  // item per rank of the pipelined kernel, length items1 + items2
-                           // (bit 31 set: GEMM2 item; else GEMM1 item id)
+  const uint32_t* order2;  // GEMM2 item per rank of the GEMM2 kernel, length items2 + items_red
+                           // (bit 30 set: reduction item)
+  const uint32_t* orderp;  // item per rank of the pipelined kernel, length items1 + items2 + items_red
+                           // (bit 31 set: GEMM2 item, bits 31 and 30: reduction item; else GEMM1 item id)
   int M, H, F, act;
   int Mb, Nb1, Nb2;        // row blocks; GEMM1 / GEMM2 column blocks
   int S1, S2;              // split-K factors
@@ -104,6 +105,9 @@ struct Args {
   int p1;                  // pipelined launch: 0 = shared roles; else work-groups with g % 64 < p1 take
                            // GEMM1 items only (from order1) and the others GEMM2 items only (order2)
   int lists2;              // claim lists of the GEMM2 role (role split only; `lists` is the GEMM1 role's)
+  int red2;                // GEMM2 split-K: 0 = the part that arrives last sums the tile; else the tile is
+                           // summed by red2 reduction items (slices of its units), ranked after every GEMM2 item
+  int items_red;           // reduction items of the launch (tiles2 * red2, or 0)
 };
 
 // ------------------------------------------------------------------ optional timing trace

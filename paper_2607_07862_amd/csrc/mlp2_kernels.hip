@@ -148,6 +148,28 @@ __device__ __forceinline__ void reduce_epilogue(const float* part, long tile, in
   }
 }
 
+// One slice of a tile's reduction (reduction items): the tile's units in
+// groups of G, the slice's groups dealt to the waves; the same sums, in the
+// same order, as the completing part's reduction above.
+template <class T, int NB, class Epi>
+__device__ __forceinline__ void reduce_slice(const float* part, long tile, int S, int slice, int slices, Epi&& epi) {
+  constexpr int U = Partial<T, NB>::UNITS;
+  constexpr int G = NB == 1 ? 2 : 1;
+  static_assert(U % G == 0, "units per group");
+  const int per = U / G / slices;  // groups per slice (the plan makes `slices` divide U / G)
+  const int lane = threadIdx.x & 63;
+  for (int grp = uniform((int)(threadIdx.x >> 6)); grp < per; grp += T::NWAVES) {
+    const int u0 = (slice * per + grp) * G;
+    Unit<T> ug[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) ug[g] = Unit<T>(u0 + g);
+    float v[G][NB][8];
+    reduce_units<T, NB, G>(part, tile, S, ug, lane, v);
+#pragma unroll
+    for (int g = 0; g < G; ++g) epi(ug[g], lane, v[g]);
+  }
+}
+
 // ------------------------------------------------------------------ work items
 //
 // Split-K epilogue, shared by both GEMMs: each part stores its partial and
@@ -268,6 +290,17 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
           pair_values<T>(acc[h], tp, tm, v);
           store_y(a, fp.row0 + 16 * tm, fp.col0 + h * T::BN + 32 * tp, v);
         }
+  } else if (a.red2 > 0) {
+    // The tile is summed by its reduction items: store the partial and count
+    // the arrival (a release), then on to the next item.
+    store_partial<T, HV>(a.part2, tile, a.S2, s, acc);
+    if constexpr (kTrace) {
+      wait_all_mem();
+      tr.t_rel = trace_now();
+    }
+    release_add(a.cnt2 + (long)tile * kLine);
+    if constexpr (kTrace) tr.t_wait = trace_now();
+    next.park(s_next);
   } else {
     const bool last = arrive_split<T, HV>(a.part2, a.cnt2 + (long)tile * kLine, tile, a.S2, s,
                                           (epoch + 1u) * (uint32_t)a.S2, acc, s_slot, tr);
@@ -278,6 +311,59 @@ __device__ __forceinline__ void gemm2_item(const Args& a, int p_in, uint32_t epo
       for (int h = 0; h < HV; ++h) store_y(a, u.row(m0, lane), u.col(n0, lane) + h * T::BN, v[h]);
     });
   }
+}
+
+// Reduction item r = tile * red2 + slice of a GEMM2 tile with split-K: wait
+// until every part of the tile has arrived in this run (its arrival counter at
+// (epoch + 1) * S2, compared wrap-safe; thread 0 polls, the group waits at a
+// barrier), then sum the slice's units over the parts in the fixed order and
+// store them.  Reduction items rank after every GEMM2 item, so they wait only
+// for lower ranks, and the whole tile is summed by red2 work-groups at once
+// instead of by the part that arrives last.  The partials need no agent-scope
+// acquire, for the reason given at arrive_split (each slice's 1 KB runs are
+// read once per launch, by one item, after every part released them).  A wait
+// that gives up latches CTRL_ERROR (bit 0) and skips the sums; the kernel
+// still drains and mlp2_check reports the timeout.
+template <class T, int HV, class C = Claim>
+__device__ __forceinline__ void reduce_item(const Args& a, int r_in, uint32_t epoch, int* s_slot, C& next, int* s_next,
+                                            TraceAcc& tr) {
+  const int r = uniform(r_in);
+  const int tile = r / a.red2, slice = r - tile * a.red2;
+  const int mb = tile % a.Mb, nb = tile / a.Mb;
+  const int m0 = mb * T::BM, n0 = nb * T::BN * HV;
+  const uint32_t* cnt = a.cnt2 + (long)tile * kLine;
+  const uint32_t target = (epoch + 1u) * (uint32_t)a.S2;
+  const uint64_t t0 = trace_now();
+  if (threadIdx.x == 0) {
+    int ok = 0;
+    if (ld_relaxed(a.ctrl + CTRL_ERROR) == 0u) {
+      for (uint32_t polls = 0;; ++polls) {
+        if ((int32_t)(ld_relaxed(cnt) - target) >= 0) {
+          ok = 1;
+          break;
+        }
+        if (polls >= a.spin_limit) break;
+        __builtin_amdgcn_s_sleep(2);
+      }
+      if (!ok) __hip_atomic_fetch_or(a.ctrl + CTRL_ERROR, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    *s_slot = ok;
+  }
+  __syncthreads();
+  const bool ok = uniform(*s_slot) != 0;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  __syncthreads();  // *s_slot may be rewritten
+  if constexpr (kTrace) {
+    tr.flag += trace_now() - t0;
+    tr_mark_mainloop(tr);
+  }
+  next.issue();  // after the item's only wait
+  if (ok)
+    reduce_slice<T, HV>(a.part2, tile, a.S2, slice, a.red2, [&](const Unit<T>& u, int lane, const float (&v)[HV][8]) {
+#pragma unroll
+      for (int h = 0; h < HV; ++h) store_y(a, u.row(m0, lane), u.col(n0, lane) + h * T::BN, v[h]);
+    });
+  next.park(s_next);
 }
 
 // Counter lifetime across kernels and runs.  The last work-group of each
@@ -398,7 +484,9 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
   const ListPos lp = list_pos(a, PHASE == PHASE_PIPELINED && a.p1 > 0);
   const int g1 = PHASE == PHASE_GEMM2 || lp.role == 1 ? 0 : a.items1;
   const int g2 = (PHASE == PHASE_GEMM2 || PHASE == PHASE_PIPELINED || PHASE == PHASE_SENTINEL) && lp.role != 0 ? a.items2 : 0;
-  const int total = g1 + g2;
+  // reduction items (ranked last) in the launches that sum split-K tiles with them
+  const int gr = (PHASE == PHASE_GEMM2 || PHASE == PHASE_PIPELINED) && lp.role != 0 ? a.items_red : 0;
+  const int total = g1 + g2 + gr;
   int p;
   if (lp.role < 0 && (int)blockIdx.x < a.first_static) {
     p = (int)blockIdx.x;
@@ -426,7 +514,9 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
         gemm1_item<T1, NB, false, true>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
     } else if constexpr (PHASE == PHASE_PIPELINED) {
       e = lp.role < 0 ? uniform(a.orderp[p]) : lp.role == 0 ? uniform(a.order1[p]) : (uniform(a.order2[p]) | 0x80000000u);
-      if (e & 0x80000000u)
+      if ((e & 0xc0000000u) == 0xc0000000u)
+        reduce_item<T2, HV>(a, (int)(e & 0x3fffffffu), epoch, &s_slot, next, &s_item, tr);
+      else if (e & 0x80000000u)
         gemm2_item<T2, HV, true>(a, (int)(e & 0x7fffffffu), epoch, lds, &s_slot, next, &s_item, tr, ready_runs);
       else
         gemm1_item<T1, NB>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
@@ -435,7 +525,10 @@ __global__ __launch_bounds__(T1::THREADS, (min_blocks<T1, NB, T2, HV, PHASE>()))
       gemm1_item<T1, NB, PHASE == PHASE_WORKQUEUE>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr, wq_epoch);
     } else {
       e = uniform(a.order2[p]);
-      gemm2_item<T2, HV, false>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
+      if (e & 0x40000000u)
+        reduce_item<T2, HV>(a, (int)(e & 0x3fffffffu), epoch, &s_slot, next, &s_item, tr);
+      else
+        gemm2_item<T2, HV, false>(a, (int)e, epoch, lds, &s_slot, next, &s_item, tr);
       e |= 0x80000000u;
     }
     if constexpr (kTrace) tr_record(a, PHASE == PHASE_GEMM2 ? 1 : 0, n_items++, p, e, t_start, tr);

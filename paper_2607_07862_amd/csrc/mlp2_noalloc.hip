@@ -57,18 +57,22 @@ static int scratch_for(int dev, char** base, int* num_cus) {
 // Zero the counter region (every counter, scoreboard, queue slot and control
 // word, the epoch included, so each call starts from a fresh plan's state) and
 // write the rank tables: GEMM1 and GEMM2 items in id order (column blocks
-// first), the pipelined table every GEMM1 item, then every GEMM2 item.
+// first), the pipelined table every GEMM1 item, then every GEMM2 item, then
+// (GEMM2 split-K) every reduction item, which the GEMM2 table ends with too.
 __global__ void k_noalloc_init(uint32_t* counters, int counter_words, uint32_t* order1, int items1, uint32_t* order2,
-                               int items2, uint32_t* orderp) {
+                               int items2, int items_red, uint32_t* orderp) {
   const int stride = (int)(gridDim.x * blockDim.x);
   for (int i = (int)(blockIdx.x * blockDim.x + threadIdx.x); i < counter_words; i += stride) counters[i] = 0u;
-  for (int i = (int)(blockIdx.x * blockDim.x + threadIdx.x); i < items1 + items2; i += stride) {
+  for (int i = (int)(blockIdx.x * blockDim.x + threadIdx.x); i < items1 + items2 + items_red; i += stride) {
     if (i < items1) {
       order1[i] = (uint32_t)i;
       orderp[i] = (uint32_t)i;
-    } else {
+    } else if (i < items1 + items2) {
       order2[i - items1] = (uint32_t)(i - items1);
       orderp[i] = 0x80000000u | (uint32_t)(i - items1);
+    } else {
+      order2[i - items1] = 0x40000000u | (uint32_t)(i - items1 - items2);
+      orderp[i] = 0xc0000000u | (uint32_t)(i - items1 - items2);
     }
   }
 }
@@ -107,10 +111,10 @@ extern "C" int mlp2_run_noalloc(int64_t M, int64_t H, int64_t F, int act, int dt
 
   hipStream_t s = (hipStream_t)stream;
   const int words = (int)((L.cnt_end - L.cnt_off) / 4);
-  const int n = std::max(words, p.items1 + p.items2);
+  const int n = std::max(words, p.items1 + p.items2 + p.items_red);
   const int grid = std::min(1024, (n + 255) / 256);
   hipLaunchKernelGGL(k_noalloc_init, dim3(grid), dim3(256), 0, s, (uint32_t*)(base + L.cnt_off), words, p.order1,
-                     p.items1, p.order2, p.items2, p.orderp);
+                     p.items1, p.order2, p.items2, p.items_red, p.orderp);
   if (hipGetLastError() != hipSuccess) return record_error(MLP2_ERR_HIP);
   return launch_plan(&p, X, W1, W2, Y, p.Z, s, mode);
 }

@@ -16,6 +16,7 @@ struct mlp2_plan_s {
   int Mb = 0, Nb1 = 0, Nb2 = 0;
   int S1 = 1, S2 = 1, kc1 = 0, kc2 = 0;
   int items1 = 0, items2 = 0;
+  int red2 = 0, items_red = 0;  // GEMM2 split-K: reduction items per tile (0: the last part sums) and in all
   int grid = 0, grid1 = 0, grid2 = 0, occupancy = 0, num_cus = 0;
   int grid_override = 0;
   int max_grid = 0;  // work-groups of every kernel of the plan that fit the device at once

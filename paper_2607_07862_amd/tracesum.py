@@ -42,9 +42,10 @@ def _records(buf, G):
                 r = a[sec, g, 1 + 8 * j: 9 + 8 * j].astype(np.uint64)
                 w0 = int(r[0])
                 entry, rank = w0 & 0xFFFFFFFF, w0 >> 32
-                kind = 1 if entry & 0x80000000 else 0
+                # 0 GEMM1 item, 1 GEMM2 item, 2 reduction item (a slice of a split-K GEMM2 tile)
+                kind = 2 if (entry & 0xC0000000) == 0xC0000000 else 1 if entry & 0x80000000 else 0
                 ring, cycles = int(r[6]) & 0xFFFFFFFF, int(r[6]) >> 32
-                out.append((kind, entry & 0x7FFFFFFF, rank, int(r[1]), int(r[2]), int(r[5]), ring, int(r[7]), cycles))
+                out.append((kind, entry & 0x3FFFFFFF, rank, int(r[1]), int(r[2]), int(r[5]), ring, int(r[7]), cycles))
     return out
 
 
@@ -95,7 +96,7 @@ def summarise(B, I, bench, key):
         t0 = min(x[3] for x in recs)
         span = (max(x[5] for x in recs) - t0) * TICK_US
         clocks.append((name, span, clock_by_eighth(recs, t0)))
-        for kind in (0, 1):
+        for kind in (0, 1, 2):
             K = [x for x in recs if x[0] == kind]
             if not K:
                 continue
@@ -104,7 +105,7 @@ def summarise(B, I, bench, key):
             main = (R[:, 1] - R[:, 0]) * TICK_US
             ring, flag = R[:, 3] * TICK_US, R[:, 4] * TICK_US
             row = {
-                "mode": name, "kind": "GEMM1" if kind == 0 else "GEMM2", "n": len(K), "span": span,
+                "mode": name, "kind": ("GEMM1", "GEMM2", "reduce")[kind], "n": len(K), "span": span,
                 "item": item.mean(), "main": main.mean(), "ring": ring.mean(), "flag": flag.mean(),
                 "epi": (item - main).mean(), "flag_share": flag.sum() / item.sum(),
                 "kcycles": R[:, 5].mean() / 1e3, "mhz": R[:, 5].sum() / item.sum(),

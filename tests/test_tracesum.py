@@ -24,10 +24,13 @@ def _buffer(G, records):
 def test_records_split_rank_entry_kind_cycles_and_ring():
     gemm1 = [(7 << 32) | 42, 1000, 1800, 0, 0, 2000, (190000 << 32) | 35, 0]
     gemm2 = [(9 << 32) | 0x80000000 | 5, 2100, 2900, 0, 0, 3000, (170000 << 32) | 12, 40]
-    buf = _buffer(3, {(0, 1): [gemm1], (1, 2): [gemm2]})
+    # a reduction item (a slice of a split-K GEMM2 tile): bits 31 and 30 of the entry
+    red = [(11 << 32) | 0xC0000000 | 17, 3100, 3150, 0, 0, 3400, (50000 << 32) | 0, 30]
+    buf = _buffer(3, {(0, 1): [gemm1], (1, 2): [gemm2, red]})
     recs = sorted(T._records(buf, 3))
     assert recs[0] == (0, 42, 7, 1000, 1800, 2000, 35, 0, 190000)
     assert recs[1] == (1, 5, 9, 2100, 2900, 3000, 12, 40, 170000)
+    assert recs[2] == (2, 17, 11, 3100, 3150, 3400, 0, 30, 50000)
 
 
 def test_records_beyond_the_capacity_are_counted_not_read():
