@@ -1058,26 +1058,43 @@ extern "C" {
 
 namespace {
 
+// Chain tile (an index into kChainTiles): 256 x 256 over eight waves when
+// every layer's width is a multiple of 256 and the narrowest layer still
+// has a tile per CU; else 128 x 128, unless the narrowest layer would then
+// have fewer tiles than CUs: 64 x 64 (four times the items) for chains of
+// few rows.
+int chain_tile(int64_t M, int layers, const int64_t* dims, int cus) {
+  int64_t narrowest = dims[1];
+  bool wide = true;
+  for (int l = 1; l <= layers; ++l) {
+    narrowest = std::min(narrowest, dims[l]);
+    wide = wide && dims[l] % 256 == 0;
+  }
+  if (wide && (int64_t)ceil_div(M, 256) * (narrowest / 256) >= cus) return 2;
+  return (int64_t)ceil_div(M, 128) * (narrowest / 128) < cus ? 1 : 0;
+}
+
+// Multiply-adds per launch group of a chain (see chain_group_rows).
+constexpr double kChainGroupMacs = 2.2e12;
+
 // Rows per launch group of a chain: 0 runs each mode's launches over all
-// rows.  A launch of more than about 4.4 TFLOP lost its lead (and its
-// clock) in both the two-layer and the chain measurements; the chain runs
-// best in groups of about 1.1 TFLOP per launch (4 layers of 8192 x 8192 at
-// 16384 rows: one launch 10.5 ms pipelined and 9.5 sequential, groups of
-// 4096 rows 8.6 and 8.9, groups of 8192 rows 8.7 and 8.9), so it groups once
-// the rows exceed two such groups.
+// rows.  Long one-launch runs lose their lead and their clock (as in the
+// two-layer measurements); with 256 x 256 tiles the chain runs best in
+// groups of about 4.4 TFLOP (2.2 T multiply-adds) per launch.  Four layers of
+// 8192 x 8192, pipelined (sequential): at 16384 rows one launch 7.55 ms
+// (7.29), groups of 4096 rows 7.31 (7.29), of 8192 rows 6.90 (6.99); at
+// 32768 rows one launch 15.9 (15.9), groups of 4096 / 8192 / 16384 rows
+// 14.4 / 14.1 / 14.7 (14.5 / 14.1 / 15.0).  It groups once the rows reach
+// two such groups.
 int64_t chain_group_rows(int64_t M, int layers, const int64_t* dims) {
   double macs = 0;
   for (int l = 0; l < layers; ++l) macs += (double)dims[l] * (double)dims[l + 1];
-  const int64_t rows = (int64_t)(0.55e12 / macs) / 256 * 256;
-  return rows >= 256 && M > 2 * rows ? rows : 0;
+  const int64_t rows = (int64_t)(kChainGroupMacs / macs) / 256 * 256;
+  return rows >= 256 && M >= 2 * rows ? rows : 0;
 }
 
 mlp2_chain_s* make_chain(int64_t M, int layers, const int64_t* dims, int act, int dev, const hipDeviceProp_t& prop) {
-  // 128 x 128 tiles, unless the narrowest layer would then have fewer tiles
-  // than CUs: 64 x 64 tiles (four times the items) for chains of few rows.
-  int64_t narrowest = dims[1];
-  for (int l = 1; l <= layers; ++l) narrowest = std::min(narrowest, dims[l]);
-  const int tile = (int64_t)ceil_div(M, 128) * (narrowest / 128) < prop.multiProcessorCount ? 1 : 0;
+  const int tile = chain_tile(M, layers, dims, prop.multiProcessorCount);
   int occ = 0;
   if (mlp2::chain_occupancy(tile, &occ) != hipSuccess || occ < 1) { fail(MLP2_ERR_HIP); return nullptr; }
 

@@ -658,9 +658,10 @@ static const Entry* find_entry(const KernelConfig& c) {
 //
 // An L-layer chain Z_l = act(Z_{l-1} W_l), Y = Z_{L-1} W_L: the producer /
 // consumer relation of the two-layer kernel at every layer boundary (Sec.
-// III-A).  An item is a T output tile of one layer over its whole K (128 x
-// 128 with a two-stage ring, or 64 x 64 with four stages for chains of few
-// rows, whose 128-row tiles would leave most CUs idle).
+// III-A).  An item is a T output tile of one layer over its whole K: 256 x
+// 256 over eight waves with a two-stage ring for chains of many rows, 128 x
+// 128 over four waves (two work-groups per CU), or 64 x 64 with four stages
+// for chains of few rows, whose larger tiles would leave most CUs idle.
 // A middle layer's item consumes like a GEMM2 item (it waits per K-slice on
 // the ready counters of the layer below, row block mb) and produces like a
 // GEMM1 item (activation, its Z rows stored, then its own ready counter
@@ -672,8 +673,8 @@ static const Entry* find_entry(const KernelConfig& c) {
 // layer order, without waits; both modes run this item function.
 using ChainT128 = TileFor<128, 128, 2>::type;
 using ChainT64 = TileFor<64, 64, 4>::type;
-constexpr int kChainThreads = 256;
-static_assert(ChainT128::THREADS == kChainThreads && ChainT64::THREADS == kChainThreads, "chain tiles: four waves");
+using ChainT256 = TileFor<256, 256, 2, 8>::type;
+static_assert(ChainT128::NWAVES == 4 && ChainT64::NWAVES == 4 && ChainT256::NWAVES == 8, "chain tile waves");
 
 template <class T>
 __device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int tile, uint32_t epoch, char* lds,
@@ -715,8 +716,9 @@ __device__ __forceinline__ void chain_item(const ChainArgs& c, int layer, int ti
   if (L.ready_out) signal_ready(L.ready_out + (long)tile * kLine);
 }
 
+// Four-wave tiles run two work-groups per CU, the eight-wave tile one.
 template <class T>
-__global__ __launch_bounds__(kChainThreads, 2) void k_mlp2_chain(ChainArgs c) {
+__global__ __launch_bounds__(T::THREADS, T::NWAVES == 4 ? 2 : 1) void k_mlp2_chain(ChainArgs c) {
   __shared__ __attribute__((aligned(1024))) char lds[T::template lds_bytes<1>()];
   __shared__ int s_item, s_slot;
   const Args& a = c.a;
@@ -749,16 +751,22 @@ __global__ __launch_bounds__(kChainThreads, 2) void k_mlp2_chain(ChainArgs c) {
 }
 
 static const void* chain_kernel(int tile) {
-  return tile == 0 ? (const void*)&k_mlp2_chain<ChainT128> : (const void*)&k_mlp2_chain<ChainT64>;
+  return tile == 0   ? (const void*)&k_mlp2_chain<ChainT128>
+         : tile == 1 ? (const void*)&k_mlp2_chain<ChainT64>
+                     : (const void*)&k_mlp2_chain<ChainT256>;
 }
 
+static int chain_threads(int tile) { return tile == 2 ? ChainT256::THREADS : ChainT128::THREADS; }
+
 hipError_t chain_occupancy(int tile, int* blocks_per_cu) {
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, chain_kernel(tile), kChainThreads, 0);
+  if (tile < 0 || tile > 2) return hipErrorInvalidValue;
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, chain_kernel(tile), chain_threads(tile), 0);
 }
 
 hipError_t launch_chain(int tile, const ChainArgs& c, int grid, hipStream_t stream) {
+  if (tile < 0 || tile > 2) return hipErrorInvalidValue;
   void* args[] = {const_cast<ChainArgs*>(&c)};
-  return hipLaunchKernel(chain_kernel(tile), dim3(grid), dim3(kChainThreads), args, 0, stream);
+  return hipLaunchKernel(chain_kernel(tile), dim3(grid), dim3(chain_threads(tile)), args, 0, stream);
 }
 
 bool config_supported(const KernelConfig& c) { return find_entry(c) != nullptr; }

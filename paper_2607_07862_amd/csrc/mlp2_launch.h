@@ -30,8 +30,9 @@ hipError_t launch_sentinel(const KernelConfig& c, const Args& a, int grid, hipSt
 // ---- GEMM chain: Z_l = act(Z_{l-1} W_l), Y = Z_{L-1} W_L, no split-K.
 constexpr int kChainMaxLayers = 8;
 constexpr int kChainWidthUnit = 128;  // every width is a multiple of this
-// Tile shapes of the chain kernel: 0 = 128 x 128 (two-stage ring), 1 = 64 x 64 (four stages).
-constexpr int kChainTiles[2] = {128, 64};
+// Tile shapes of the chain kernel: 0 = 128 x 128 (four waves, two-stage ring), 1 = 64 x 64 (four
+// waves, four stages), 2 = 256 x 256 (eight waves, two-stage ring).
+constexpr int kChainTiles[3] = {128, 64, 256};
 
 // One layer of a chain launch (passed by value with every launch).
 struct ChainLayer {

@@ -8,9 +8,11 @@
 * with the flag waits cut to one poll a pipelined run may give up; the plan
   reports it, recovers, and its next runs are exact;
 * a run captured into a graph replays with the eager bits, in both modes;
+* chains wide enough for the 256 x 256 eight-wave tile (one work-group per
+  CU) match the oracle over every row, ragged row counts included;
 * at the paper's shape (four 8192 x 8192 layers, 4096 rows in one launch,
-  16684 rows in row groups with a shorter last one) sampled rows match the
-  oracle and the modes agree bit for bit.
+  16684 rows in row groups of 8192 with a shorter last one) sampled rows
+  match the oracle and the modes agree bit for bit.
 """
 import numpy as np
 import pytest
@@ -53,6 +55,30 @@ def test_modes_agree_and_match_the_oracle(lib, M, dims, act):
     d = I.chain_inputs(M, dims, seed=M + len(dims))
     X, Ws = _device(d)
     plan = B.ChainPlan(M, dims, act)
+    Ys = _run(plan, X, Ws, B.MODE_SEQUENTIAL)
+    Yp = _run(plan, X, Ws, B.MODE_TILE_PIPELINED)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    assert_bit_equal(Ys, Yp, "chain Y sequential vs pipelined")
+    assert_matches_oracle(Yp, _oracle(d, M, dims, act), "chain Y")
+    plan.close()
+
+
+WIDE_CASES = [
+    # M, dims, act: 16 and 9 row blocks of 256 rows (the last ragged), 256 and 288 tiles in the narrowest layer
+    (4000, [256, 4096, 4096], 1),
+    (2100, [384, 8192, 8192, 8192], 1),
+]
+
+
+@pytest.mark.parametrize("M,dims,act", WIDE_CASES, ids=[f"{c[0]}x{'-'.join(map(str, c[1]))}-a{c[2]}" for c in WIDE_CASES])
+def test_wide_tiles_match_the_oracle(lib, M, dims, act):
+    print(f"\n[chain wide] {M} rows, dims {dims}", flush=True)
+    d = I.chain_inputs(M, dims, seed=M + 7)
+    X, Ws = _device(d)
+    plan = B.ChainPlan(M, dims, act)
+    # the eight-wave tile runs one work-group per CU (the four-wave tiles two)
+    assert plan.grid() == torch.cuda.get_device_properties(0).multi_processor_count
     Ys = _run(plan, X, Ws, B.MODE_SEQUENTIAL)
     Yp = _run(plan, X, Ws, B.MODE_TILE_PIPELINED)
     torch.cuda.synchronize()
@@ -153,9 +179,9 @@ def test_argument_errors(lib):
 
 @pytest.mark.parametrize("M", [4096, 16684])
 def test_paper_shape_four_layers_sampled_rows(lib, M):
-    """4096 rows run as one launch per mode; 16684 rows in row groups of 4096
-    and a last group of 300 (the sampled rows include both sides of a group
-    boundary and the last row)."""
+    """4096 rows run as one launch per mode; 16684 rows in two row groups of
+    8192 and a last group of 300 (the sampled rows include both sides of the
+    group boundaries and the last row)."""
     dims, act = [8192] * 5, 1
     print(f"\n[chain] {M} rows, dims {dims}", flush=True)
     d = I.chain_inputs(M, dims, seed=45)
@@ -166,7 +192,7 @@ def test_paper_shape_four_layers_sampled_rows(lib, M):
     torch.cuda.synchronize()
     assert plan.check() == B.OK
     assert_bit_equal(Ys, Yp, "chain Y sequential vs pipelined")
-    rows = np.unique(np.concatenate([I.sample_rows(M, 12, 45), [min(4095, M - 1), min(4096, M - 1), M - 1]]))
+    rows = np.unique(np.concatenate([I.sample_rows(M, 12, 45), [min(8191, M - 1), min(8192, M - 1), min(16383, M - 1), min(16384, M - 1), M - 1]]))
     ref = _oracle(d, M, dims, act, rows=rows)
     assert_matches_oracle(Yp[torch.as_tensor(rows, device="cuda")], ref, "sampled rows")
     plan.close()
