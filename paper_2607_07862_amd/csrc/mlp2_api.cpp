@@ -1014,15 +1014,26 @@ int mlp2_trace_attach(mlp2_plan_t p, void* buffer, int records_per_group) {
 
 namespace {
 
-// Rank table of the chain's one-launch mode.  Layer 0's tiles come column
-// blocks first; each later layer is merged in layer by layer: the item of
+// Tile order of one chain layer (tile = nb * Mb + mb): the XCD-grouped
+// order of the two-layer plan's GEMMs when the chain has several row blocks
+// (each XCD's L2 then serves a sub-block of rows and columns instead of
+// every XCD reading every weight stripe), else column blocks in order.
+std::vector<uint32_t> chain_layer_order(const mlp2_chain_s* p, int l) {
+  const int nb = p->items[l] / p->Mb;
+  if (p->Mb > 1) return xcd_grouped(p->Mb, nb, p->grid);
+  std::vector<uint32_t> t((size_t)p->items[l]);
+  for (int i = 0; i < p->items[l]; ++i) t[(size_t)i] = (uint32_t)i;
+  return t;
+}
+
+// Rank table of the chain's one-launch mode.  Layer 0's tiles come in the
+// layer order; each later layer is merged in layer by layer: the item of
 // tile (mb, nb) goes right after rank h + lag of the table built so far,
 // where h is the highest rank among the tiles of the layer below in row
-// block mb (it reads all of them), and items of equal key keep their column
+// block mb (it reads all of them), and items of equal key keep their layer
 // order.  Every item therefore ranks above all of its producers.
 std::vector<uint32_t> chain_rank_table(const mlp2_chain_s* p, int lag) {
-  std::vector<uint32_t> list;
-  for (int t = 0; t < p->items[0]; ++t) list.push_back((uint32_t)t);
+  std::vector<uint32_t> list = chain_layer_order(p, 0);
   for (int l = 1; l < p->L; ++l) {
     std::vector<int64_t> row_last((size_t)p->Mb, -1);  // highest rank of layer l - 1 per row block
     for (size_t r = 0; r < list.size(); ++r)
@@ -1031,9 +1042,9 @@ std::vector<uint32_t> chain_rank_table(const mlp2_chain_s* p, int lag) {
         row_last[(size_t)mb] = std::max<int64_t>(row_last[(size_t)mb], (int64_t)r);
       }
     std::vector<std::pair<int64_t, uint32_t>> add;
-    for (int t = 0; t < p->items[l]; ++t) {
-      const int64_t key = std::min<int64_t>(row_last[(size_t)(t % p->Mb)] + lag, (int64_t)list.size() - 1);
-      add.push_back({key, ((uint32_t)l << 24) | (uint32_t)t});
+    for (uint32_t t : chain_layer_order(p, l)) {
+      const int64_t key = std::min<int64_t>(row_last[(size_t)(t % (uint32_t)p->Mb)] + lag, (int64_t)list.size() - 1);
+      add.push_back({key, ((uint32_t)l << 24) | t});
     }
     std::stable_sort(add.begin(), add.end(), [](const std::pair<int64_t, uint32_t>& x, const std::pair<int64_t, uint32_t>& y) {
       return x.first < y.first;
@@ -1159,7 +1170,7 @@ mlp2_chain_s* make_chain(int64_t M, int layers, const int64_t* dims, int act, in
   p->counters_bytes = cnt_end - cnt_off;
   std::vector<uint32_t> seq;
   for (int l = 0; l < layers; ++l)
-    for (int t = 0; t < p->items[l]; ++t) seq.push_back(((uint32_t)l << 24) | (uint32_t)t);
+    for (uint32_t t : chain_layer_order(p, l)) seq.push_back(((uint32_t)l << 24) | t);
   const std::vector<uint32_t> pipe = chain_rank_table(p, p->grid);
   if (hipMemset(b, 0, cnt_end) != hipSuccess ||
       hipMemcpy(p->order_seq, seq.data(), seq.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
