@@ -57,7 +57,16 @@ sys.path.insert(0, ROOT)
 METRIC = "2-layer MLP latency µs (pipelined vs sequential) + % HBM BW / MFMA peak"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
-KERNEL_SOURCES = ["paper_2607_07862_amd/csrc/mlp2_device.hpp", "paper_2607_07862_amd/csrc/mlp2_kernels.hip"]
+# Sources that decide what a planned launch runs (kernels, tiles, orders): the
+# committed HBM traffic of a workload is reported only while their hash matches.
+KERNEL_SOURCES = [
+    "include/mlp2.h",
+    "paper_2607_07862_amd/csrc/mlp2_api.cpp",
+    "paper_2607_07862_amd/csrc/mlp2_device.hpp",
+    "paper_2607_07862_amd/csrc/mlp2_kernels.hip",
+    "paper_2607_07862_amd/csrc/mlp2_launch.h",
+    "paper_2607_07862_amd/csrc/mlp2_plan_impl.h",
+]
 FLUSH_BYTES = 1 << 30
 SETTLE_MS = 200
 

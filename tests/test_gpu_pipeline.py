@@ -293,17 +293,19 @@ def test_wait_covers_blocks_past_one_full_window(lib, dropped):
     plan.close()
 
 
+@pytest.mark.parametrize("s2", [1, 2])
 @pytest.mark.parametrize("grid", [0, 1, 5, 24])
-def test_xcd_grouped_default_order(lib, grid):
-    """Several row blocks and no split-K: the default order deals the tiles of
-    both kernels to the XCDs in sub-blocks (ragged here: 5 row blocks).  The
-    pipelined mode gives the sequential mode's bits, within the oracle's bound."""
+def test_xcd_grouped_default_order(lib, grid, s2):
+    """Several row blocks: the default order deals the GEMM1 tiles to the XCDs
+    in sub-blocks (ragged here: 5 row blocks), and the GEMM2 tiles too
+    without split-K (with it, GEMM2 items go in item order).  The pipelined
+    mode gives the sequential mode's bits, within the oracle's bound."""
     M, H, F, act = 640, 256, 1024, 1
     d = I.make_inputs(M, H, F, act, seed=90)
     g = device_inputs(d)
-    plan = B.Plan(M, H, F, act, {"bm": 128, "bn1": 128, "bn2": 128, "splitk1": 1, "splitk2": 1})
+    plan = B.Plan(M, H, F, act, {"bm": 128, "bn1": 128, "bn2": 128, "splitk1": 1, "splitk2": s2})
     info = plan.info()
-    assert (info["row_blocks"], info["splitk1"], info["splitk2"], info["order"]) == (5, 1, 1, B.ORDER_AUTO)
+    assert (info["row_blocks"], info["splitk1"], info["splitk2"], info["order"]) == (5, 1, s2, B.ORDER_AUTO)
     if grid:
         plan.set_option(B.OPT_GRID, grid)
     Ys = run(plan, g, B.MODE_SEQUENTIAL).clone()
