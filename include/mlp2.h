@@ -305,8 +305,14 @@ int mlp2_run_noalloc(int64_t M, int64_t H, int64_t F, int act, int dtype, const 
  * and produce).  Z_0 = X [M, D_0]; Z_l = act(Z_{l-1} . W_l) for l < L;
  * Y = Z_{L-1} . W_L [M, D_L].  W_l is [D_{l-1}, D_l] row-major bf16; fp32
  * accumulation; the intermediates are stored as bf16 in the plan's
- * workspace.  Items are output tiles over their whole K: 128 x 128, or
- * 64 x 64 when the narrowest layer would have fewer 128-row tiles than CUs. */
+ * workspace.  Items are output tiles over their whole K: 256 x 256 (eight
+ * waves) when every width D_1 .. D_L is a multiple of 256 and the narrowest
+ * layer has a 256-row tile per CU, else 128 x 128, or 64 x 64 when the
+ * narrowest layer would have fewer 128-row tiles than CUs; each layer's
+ * tiles are dealt to the XCDs in sub-blocks of rows and columns.  Chains of
+ * many rows run as back-to-back launches over row groups of about 2.2 T
+ * multiply-adds each (once the rows reach two groups; rows do not interact,
+ * so the result is that of one launch). */
 typedef struct mlp2_chain_s* mlp2_chain_t; /* opaque; created by mlp2_chain_plan, freed by mlp2_chain_destroy */
 
 /* Plan an L-layer chain on the current device.  dims holds L + 1 widths
