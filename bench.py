@@ -60,7 +60,6 @@ BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 # Sources that decide what a planned launch runs (kernels, tiles, orders): the
 # committed HBM traffic of a workload is reported only while their hash matches.
 KERNEL_SOURCES = [
-    "include/mlp2.h",
     "paper_2607_07862_amd/csrc/mlp2_api.cpp",
     "paper_2607_07862_amd/csrc/mlp2_device.hpp",
     "paper_2607_07862_amd/csrc/mlp2_kernels.hip",
