@@ -569,14 +569,14 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5, help="untimed warm-up steps of the headline (each mode once per step)")
+    ap.add_argument("--warmup", type=int, default=20, help="untimed warm-up steps of the headline (each mode once per step)")
     ap.add_argument("--workload", default="l70b_gated",
                     help="headline workload (default: the largest single-GPU configuration, the 70B gated MLP)")
     ap.add_argument("--tuning", default="", help="JSON dict of mlp2_tuning_t fields")
     ap.add_argument("--cpu-budget", type=float, default=60.0,
                     help="longest the CPU oracle may take; beyond it a row sample is timed and scaled")
     ap.add_argument("--cold-iters", type=int, default=20)
-    ap.add_argument("--interleave-iters", type=int, default=60,
+    ap.add_argument("--interleave-iters", type=int, default=100,
                     help="warm runs per mode timed one by one in alternating order (0 skips; half of it per table row)")
     ap.add_argument("--no-attainable", action="store_true", help="skip the stream and library-GEMM references")
     ap.add_argument("--no-microbatch", action="store_true",
