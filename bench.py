@@ -466,6 +466,18 @@ def attainable():
     return out
 
 
+def host_cpu_model() -> str:
+    """The host CPU's model name (first processor in /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, d, budget_s: float):
     """The oracle as it stands, timed on this host: one full evaluation of the
     workload (every output row, the weights decoded once inside the call) when
@@ -487,7 +499,7 @@ def cpu_baseline(w, d, budget_s: float):
     t0 = time.perf_counter()
     O.mlp2(X, W1, W2, w.M, w.H, w.F, w.act, rows=np.arange(rows_per))
     t_first = time.perf_counter() - t0
-    host = {"cpu_count": os.cpu_count(), "blas_threads": blas}
+    host = {"cpu_count": os.cpu_count(), "blas_threads": blas, "cpu_model": host_cpu_model()}
     if t_first * max(1.0, w.M / rows_per) <= budget_s or w.M <= rows_per:
         t0 = time.perf_counter()
         O.mlp2(X, W1, W2, w.M, w.H, w.F, w.act)
@@ -783,6 +795,12 @@ def main():
         log(f"timing the CPU oracle (budget {args.cpu_budget}s)")
         cpu = cpu_baseline(w, d, args.cpu_budget)
         log(f"cpu baseline: {cpu}")
+        # the oracle on every table row's own seeded inputs (the headline's row: the timing above)
+        for key, row in table.items():
+            o = cpu if key == args.workload else cpu_baseline(I.WORKLOADS[key], I.workload_inputs(I.WORKLOADS[key]),
+                                                              args.cpu_budget)
+            row["cpu_oracle"] = {k: o[k] for k in ("value", "unit", "sample")}
+            log(f"cpu oracle {key:12s} {row['cpu_oracle']}")
 
     out = {
         "metric": METRIC,

@@ -201,7 +201,11 @@ def derived_lines(per) -> list:
       v_mfma_f32_16x16x32_bf16 counts the 16 cycles it holds its SIMD) over
       the cycles of all 1024 SIMDs;
     * texture-data busy: TD_TD_BUSY (summed over CUs) over the cycles of all
-      256 CUs.
+      256 CUs;
+    * wave wait share: SQ_WAIT_INST_ANY over SQ_WAVE_CYCLES (both summed over
+      waves in the same units): the share of the waves' lifetimes spent
+      waiting before an instruction could issue (s_waitcnt, barriers,
+      dependencies).
     """
     def mean(k, c):
         v = per[k].get(c) or []
@@ -220,11 +224,15 @@ def derived_lines(per) -> list:
         t = mean(k, "TD_TD_BUSY")
         if t is not None:
             parts.append(f"texture-data busy {100 * t / (cyc * CUS):.1f} %")
+        wi, wc = mean(k, "SQ_WAIT_INST_ANY"), mean(k, "SQ_WAVE_CYCLES")
+        if wi is not None and wc:
+            parts.append(f"wave wait share {100 * wi / wc:.1f} %")
         if parts:
             out.append(f"- {short_name(k)}: " + ", ".join(parts) + f" (over {cyc:,.0f} active cycles per XCD)")
     if out:
         out = ["", "Utilisation over the kernel's active cycles (GRBM_GUI_ACTIVE / 8 per XCD; MFMA busy over "
-               "1024 SIMDs, texture-data busy over 256 CUs):", ""] + out
+               "1024 SIMDs, texture-data busy over 256 CUs; wave wait share: SQ_WAIT_INST_ANY over SQ_WAVE_CYCLES):",
+               ""] + out
     return out
 
 

@@ -87,15 +87,18 @@ def test_stats_table(tmp_path):
 
 def test_counter_utilisations(tmp_path):
     # two dispatches of 1000 cycles per XCD; MFMA busy half of every SIMD's cycles,
-    # the texture-data units a quarter of every CU's; two passes merged per kernel
+    # the texture-data units a quarter of every CU's, the waves waiting 30 % of their
+    # cycles in one dispatch and 20 % in the other; two passes merged per kernel
     a, b = str(tmp_path / "mfma"), str(tmp_path / "path")
     _counters(a, [(1, PIPE, "GRBM_GUI_ACTIVE", 8000), (1, PIPE, "SQ_VALU_MFMA_BUSY_CYCLES", 1024 * 500),
+                  (1, PIPE, "SQ_WAIT_INST_ANY", 360), (1, PIPE, "SQ_WAVE_CYCLES", 1200),
                   (2, PIPE, "GRBM_GUI_ACTIVE", 8000), (2, PIPE, "SQ_VALU_MFMA_BUSY_CYCLES", 1024 * 500),
+                  (2, PIPE, "SQ_WAIT_INST_ANY", 240), (2, PIPE, "SQ_WAVE_CYCLES", 1200),
                   (3, COPY, "GRBM_GUI_ACTIVE", 10)])
     _counters(b, [(5, PIPE, "GRBM_GUI_ACTIVE", 8000), (5, PIPE, "TD_TD_BUSY", 256 * 250)])
     out = str(tmp_path / "c.md")
     P.counters(argparse.Namespace(dirs=[a, b], out=out, cmd=["pass 1", "pass 2"], title="t"))
     text = open(out).read()
     assert ("- k_mlp2 pipelined (bm 128, bn1 64, bn2 64, nb 1, stages 4, waves 4): MFMA busy 50.0 %, "
-            "texture-data busy 25.0 % (over 1,000 active cycles per XCD)") in text
+            "texture-data busy 25.0 %, wave wait share 25.0 % (over 1,000 active cycles per XCD)") in text
     assert "pass 1" in text and "pass 2" in text and COPY not in text
