@@ -410,6 +410,63 @@ def test_counter_targets_hold_across_any_sequence_of_modes(seed):
         sn += mode == "sentinel"
 
 
+MASK = 0xFFFFFFFF
+
+
+def reached(v, target):
+    """The kernels' wrap-safe test of a 32-bit counter against a 32-bit
+    target: the difference taken as a signed 32-bit value is >= 0."""
+    d = (v - target) & MASK
+    return d < 0x80000000
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_counter_targets_hold_across_the_32_bit_wrap(seed):
+    """The same run-to-run protocol with every counter and target a 32-bit
+    value, starting a few dozen runs before the epoch wraps, each counter in
+    the state those runs leave it in: the wrap-safe compare takes the same
+    decisions as exact counting (not ready before this run's signal, ready
+    after it; a unit or split tile complete exactly at its last producer)."""
+    rng = random.Random(100 + seed)
+    tiles, n_of = list(range(6)), {"u0": 2, "u1": 3, "u2": 1}
+    users = {"u0": [0, 1], "u1": [2, 3, 4], "u2": [5]}
+    S = 3
+    epoch, wq, sn = (1 << 32) - 37 - seed, 11 + seed, 5
+    ready = {t: (epoch - sn) & MASK for t in tiles}
+    board = {u: (wq * n) & MASK for u, n in n_of.items()}
+    arrivals = (epoch * S) & MASK
+    wrapped = False
+    for _ in range(80):
+        mode = rng.choice(["sequential", "pipelined", "workqueue", "sentinel"])
+        target = (epoch - sn + 1) & MASK
+        if mode != "sentinel":
+            if mode == "pipelined":
+                assert not any(reached(ready[t], target) for t in tiles)
+            for t in tiles:
+                ready[t] = (ready[t] + 1) & MASK
+            if mode == "pipelined":
+                assert all(reached(ready[t], target) for t in tiles)
+        if mode == "workqueue":
+            for u, ts in users.items():
+                for k, t in enumerate(ts):
+                    board[u] = (board[u] + 1) & MASK
+                    assert reached(board[u], ((wq + 1) * n_of[u]) & MASK) == (k == len(ts) - 1)
+        for s_ in range(S):
+            arrivals = (arrivals + 1) & MASK
+            assert reached(arrivals, ((epoch + 1) * S) & MASK) == (s_ == S - 1)
+        epoch = (epoch + 1) & MASK
+        wrapped |= epoch == 0
+        wq += mode == "workqueue"
+        sn += mode == "sentinel"
+    assert wrapped
+
+
+def test_wrap_safe_compare_pins():
+    assert reached(5, 5) and reached(6, 5) and not reached(4, 5)
+    assert reached(0, MASK) and reached(3, MASK - 2) and not reached(MASK, 0)
+    assert not reached(MASK - 2, 3) and reached(0x7FFFFFFF, 0) and not reached(0x80000000, 0)
+
+
 @pytest.mark.parametrize("Mb,N,wave,band", [(128, 64, 512, 8), (16, 112, 512, 4), (5, 7, 8, 2), (3, 10, 17, 1), (40, 3, 64, 21)])
 def test_banded_deal_is_a_permutation_band_by_band(Mb, N, wave, band):
     order = banded(Mb, N, wave, band)
