@@ -424,9 +424,11 @@ def reached(v, target):
 def test_counter_targets_hold_across_the_32_bit_wrap(seed):
     """The same run-to-run protocol with every counter and target a 32-bit
     value, starting a few dozen runs before the epoch wraps, each counter in
-    the state those runs leave it in: the wrap-safe compare takes the same
-    decisions as exact counting (not ready before this run's signal, ready
-    after it; a unit or split tile complete exactly at its last producer)."""
+    the state those runs leave it in, and each decision taken as the kernels
+    take it: a ready counter against its target with the wrap-safe compare
+    (not ready before this run's signal, ready after it); a split-K arrival
+    or a scoreboard increment by 32-bit equality of its fetch-and-add result
+    with the run's target (complete exactly at the last producer)."""
     rng = random.Random(100 + seed)
     tiles, n_of = list(range(6)), {"u0": 2, "u1": 3, "u2": 1}
     users = {"u0": [0, 1], "u1": [2, 3, 4], "u2": [5]}
@@ -449,11 +451,13 @@ def test_counter_targets_hold_across_the_32_bit_wrap(seed):
         if mode == "workqueue":
             for u, ts in users.items():
                 for k, t in enumerate(ts):
-                    board[u] = (board[u] + 1) & MASK
-                    assert reached(board[u], ((wq + 1) * n_of[u]) & MASK) == (k == len(ts) - 1)
+                    old = board[u]
+                    board[u] = (old + 1) & MASK
+                    assert (((old + 1) & MASK) == ((wq + 1) * n_of[u]) & MASK) == (k == len(ts) - 1)
         for s_ in range(S):
-            arrivals = (arrivals + 1) & MASK
-            assert reached(arrivals, ((epoch + 1) * S) & MASK) == (s_ == S - 1)
+            old = arrivals
+            arrivals = (old + 1) & MASK
+            assert (old == (((epoch + 1) * S) - 1) & MASK) == (s_ == S - 1)
         epoch = (epoch + 1) & MASK
         wrapped |= epoch == 0
         wq += mode == "workqueue"
