@@ -13,7 +13,7 @@ What it computes (CTA-pipelining, arXiv 2607.07862):
     the arithmetic: a consumer tile starts once every producer tile it reads
     is complete.  The method therefore reaches exactly the plain definition
     of the two-layer product, which is what this oracle writes out.
-  * The paper drops the activation "for simplicity" (Sec. IV); the workloads
+  * The paper leaves the activation out of its workload (Sec. IV); the workloads
     built here put one back between the GEMMs: identity, GELU with the tanh
     approximation, or SwiGLU ``silu(X Wg) * (X Wu)`` with the packed weight
     ``W1 = [Wg; Wu]`` of shape ``[2, H, F]``.
