@@ -6,7 +6,9 @@ counts from 1 to about 1100, H and F any multiples of 64 up to 1536 and 3072
 (odd ratios between them included), every activation.  Whatever tiles,
 split-K and orders the plan picks, every mode gives the sequential mode's
 bits on Y (and the one-launch modes on Z), and Y and Z match the fp64 oracle
-within the elementwise bound.
+within the elementwise bound.  GEMM chains likewise: one to four layers of
+widths that differ from layer to layer, both modes bit-equal, Y within the
+chain oracle's bound.
 """
 import random
 
@@ -51,4 +53,37 @@ def test_random_shapes_every_mode(lib, M, H, F, act):
     assert_matches_oracle(Yp, ref, "Y")
     zref = O.intermediate(I.bits(d["X"]), I.bits(d["W1"]), M, H, F, act)
     assert_matches_oracle(Zp[:M], zref, "Z")
+    plan.close()
+
+
+def _chain_cases(n, seed):
+    rng = random.Random(seed)
+    out = []
+    for _ in range(n):
+        L = rng.randint(1, 4)
+        M = rng.choice([rng.randint(1, 128), rng.randint(129, 700)])
+        out.append((M, [128 * rng.randint(1, 12) for _ in range(L + 1)], rng.randrange(2)))
+    return out
+
+
+CHAIN_CASES = _chain_cases(12, 20261203)
+
+
+@pytest.mark.parametrize("M,dims,act", CHAIN_CASES, ids=[f"{c[0]}x{'-'.join(map(str, c[1]))}-a{c[2]}" for c in CHAIN_CASES])
+def test_random_chains_both_modes(lib, M, dims, act):
+    import torch
+
+    print(f"\n[random chain] M={M} dims={dims} act={act}", flush=True)
+    d = I.chain_inputs(M, dims, seed=M + sum(dims) + act)
+    X, Ws = d["X"].to("cuda"), [w.to("cuda") for w in d["Ws"]]
+    plan = B.ChainPlan(M, dims, act)
+    Ys = torch.empty(M, dims[-1], dtype=torch.bfloat16, device="cuda")
+    Yp = torch.empty_like(Ys)
+    plan.run(X, Ws, Ys, B.MODE_SEQUENTIAL)
+    plan.run(X, Ws, Yp, B.MODE_TILE_PIPELINED)
+    torch.cuda.synchronize()
+    assert plan.check() == B.OK
+    assert_bit_equal(Ys, Yp, "chain Y sequential vs pipelined")
+    ref = O.chain(I.bits(d["X"]), [I.bits(w) for w in d["Ws"]], M, dims, act)
+    assert_matches_oracle(Yp, ref, "chain Y")
     plan.close()
