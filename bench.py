@@ -131,6 +131,7 @@ def device_random_inputs(w):
 
 
 CHAIN_LAYERS, CHAIN_WIDTH, CHAIN_ROWS = 4, 8192, (128, 1024, 4096, 16384)
+CHAIN_ROWS_SHORT = (128, 4096)  # the default run's chain leg (--chain: every row count above)
 
 
 def chain_row(B, M: int, steps: int, iters: int) -> dict:
@@ -595,9 +596,11 @@ def main():
                     help="skip the micro-batching comparison (8192 x 8192 weights at 8192 and 16384 rows)")
     ap.add_argument("--microbatch-replays", type=int, default=10)
     ap.add_argument("--chain", action="store_true",
-                    help="also time the GEMM chain: 4 layers of 8192 x 8192 weights, GELU between")
-    ap.add_argument("--chain-rows", default=",".join(str(m) for m in CHAIN_ROWS),
-                    help="row counts of the chain leg (comma-separated)")
+                    help="time the GEMM chain (4 layers of 8192 x 8192 weights, GELU between) at every row count "
+                         "(the default run times it at 128 and 4096 rows)")
+    ap.add_argument("--no-chain", action="store_true", help="skip the GEMM chain leg")
+    ap.add_argument("--chain-rows", default="",
+                    help="row counts of the chain leg (comma-separated; default 128,1024,4096,16384 with --chain)")
     ap.add_argument("--paper-shapes", action="store_true",
                     help="also time the paper's own workload: 8192x8192 weights, no activation, M = 1024 ... 32768")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle timing")
@@ -734,8 +737,10 @@ def main():
             torch.cuda.empty_cache()
 
     chain = {}
-    if args.chain:
-        for Mc in [int(x) for x in args.chain_rows.split(",")]:
+    # the chain leg: every row count with --chain, a short one in the full default run
+    if args.chain or (not args.no_chain and not args.no_table and not args.only_pipelined):
+        rows = args.chain_rows or ",".join(str(m) for m in (CHAIN_ROWS if args.chain else CHAIN_ROWS_SHORT))
+        for Mc in [int(x) for x in rows.split(",")]:
             row = chain_row(B, Mc, max(5, args.steps // 5), 10)
             chain[f"chain{CHAIN_LAYERS}x{CHAIN_WIDTH}_m{Mc}"] = row
             log(f"CHAIN m{Mc:<6d} {row}")
