@@ -127,12 +127,23 @@ def test_one_poll_waits_give_up_and_the_plan_recovers(lib):
     plan.close()
 
 
+GRAPH_CASES = [
+    # M, dims: 64 x 64 tiles; the eight-wave 256 x 256 tile (one work-group per CU)
+    (150, [128, 256, 256, 128]),
+    (4000, [256, 4096, 4096]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(GRAPH_CASES)))
 @pytest.mark.parametrize("mode", [B.MODE_SEQUENTIAL, B.MODE_TILE_PIPELINED])
-def test_graph_replays_match_eager_runs(lib, mode):
-    M, dims, act = 150, [128, 256, 256, 128], 1
+def test_graph_replays_match_eager_runs(lib, mode, case):
+    M, dims = GRAPH_CASES[case]
+    act = 1
     d = I.chain_inputs(M, dims, seed=43)
     X, Ws = _device(d)
     plan = B.ChainPlan(M, dims, act)
+    if case == 1:
+        assert plan.grid() == torch.cuda.get_device_properties(0).multi_processor_count
     ref = _run(plan, X, Ws, B.MODE_SEQUENTIAL).clone()
     Y = torch.empty(M, dims[-1], dtype=torch.bfloat16, device="cuda")
     side = torch.cuda.Stream()  # default priority
